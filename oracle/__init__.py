@@ -1,0 +1,47 @@
+"""CPU oracle for the doubly-pipelined, dual-root reduction-to-all (Traeff 2021).
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import, call or
+link this package: only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` use it.  It shares no code with the HIP
+library in ``paper_2109_12626_amd/`` and imports nothing from it.
+
+It is a plain, slow, obviously correct restatement of what the method
+computes (numpy, one array operation per rank, vectorised only over the
+independent columns):
+
+* ``trees``       -- the two post-order numbered, heap-shaped complete binary
+                     trees and their dual roots (Section 1.1).
+* ``ops``         -- the element operators: int32 SUM (two's-complement wrap),
+                     int32 MAX, fp32 SUM (IEEE binary32, round to nearest even)
+                     and the non-commutative 2x2 uint32 matrix product mod 2^32.
+* ``reduce``      -- the result y every rank receives, evaluated in the exact
+                     association the trees impose (Algorithm 1, lines for the
+                     two children and the dual root), plus the plain
+                     left-to-right definition of Section 1 for exact operators.
+* ``algorithm1``  -- a literal round-by-round rendezvous simulation of
+                     Algorithm 1 with blocking, virtual empty blocks and the
+                     telephone-model exchanges, used to pin the tree
+                     evaluation and the round counts.
+* ``blocks``      -- the block partition and the block-count rule of
+                     Section 1.2.
+
+Parity status: every function here is pinned by ``tests/test_oracle_*.py``
+(hand-derived worked examples, closed forms, brute force, the error bound of
+recursive summation and the independent Algorithm-1 simulation).  The
+``wbal`` tree shape is an experiment only and is "parity unpinned" beyond its
+p=9 structure.
+"""
+
+from .trees import Trees, build_trees, heap_postorder_tree
+from .ops import DTYPES, OPS, combine, valid_pair, element_shape, numpy_dtype
+from .reduce import allreduce_tree, allreduce_ltr, allreduce_all
+from .algorithm1 import simulate, DeadlockError
+from .blocks import block_bounds, block_rule_lit, block_rule_cal, log2_height
+
+__all__ = [
+    "Trees", "build_trees", "heap_postorder_tree",
+    "DTYPES", "OPS", "combine", "valid_pair", "element_shape", "numpy_dtype",
+    "allreduce_tree", "allreduce_ltr", "allreduce_all",
+    "simulate", "DeadlockError",
+    "block_bounds", "block_rule_lit", "block_rule_cal", "log2_height",
+]
