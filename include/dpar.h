@@ -1,0 +1,180 @@
+/*
+ * dpar.h -- doubly-pipelined, dual-root reduction-to-all on one MI355X.
+ *
+ * C ABI of libdpar.so.  p virtual ranks each hold a vector x_i of m elements
+ * in device memory; one call computes y = x_0 (.) x_1 (.) ... (.) x_{p-1}
+ * element-wise for an associative, not necessarily commutative operator (.)
+ * and writes y into every rank's output buffer y_i (Traeff 2021, Section 1:
+ * the reduction-to-all problem).  The operator applications follow exactly
+ * the association of Algorithm 1 on two post-order numbered binary trees with
+ * dual roots (Section 1.1), so floating-point results are bit-identical to a
+ * serial evaluation in that order, for every block count, executor and run.
+ *
+ * Conventions for every function below:
+ *   - Return 0 (DPAR_SUCCESS) or a negative dpar_status_t; no exception or
+ *     signal crosses the ABI.  dpar_last_error() gives a text for the last
+ *     failure on the calling thread's most recent call.
+ *   - Device work is enqueued on the caller's stream and is asynchronous with
+ *     respect to the host.
+ *   - Nothing is written to any output on an argument error.
+ */
+#ifndef DPAR_H
+#define DPAR_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DPAR_SUCCESS = 0,
+    DPAR_ERR_INVALID_ARG = -1, /* null array or entry, p < 1, b < 0, b > m, bad rank */
+    DPAR_ERR_UNSUPPORTED = -2, /* dtype/op pair, or a size beyond the index range */
+    DPAR_ERR_ALIAS = -3,       /* outputs overlap, or partially overlap an input */
+    DPAR_ERR_NOMEM = -4,       /* library scratch could not be allocated */
+    DPAR_ERR_HIP = -5,         /* HIP runtime or launch error (text in dpar_last_error) */
+    DPAR_ERR_TIMEOUT = -6      /* a grid-barrier wait gave up (see dpar_check_status) */
+} dpar_status_t;
+
+/* Element types.  A DPAR_U32_MAT2X2 element is a 2x2 matrix of uint32 stored
+ * row-major as [a00, a01, a10, a11] (16 bytes). */
+typedef enum {
+    DPAR_INT32 = 0,
+    DPAR_FLOAT32 = 1,
+    DPAR_U32_MAT2X2 = 2
+} dpar_dtype_t;
+
+/* Operators (Section 1: associative, possibly non-commutative).  Valid
+ * pairs: INT32 x {SUM, MAX}, FLOAT32 x {SUM}, U32_MAT2X2 x {MATMUL}.
+ *   INT32 SUM   two's-complement addition wrapping modulo 2^32;
+ *   INT32 MAX   signed maximum;
+ *   FLOAT32 SUM IEEE binary32 addition, round to nearest even, subnormals kept;
+ *   MATMUL      C = A.B with every entry mod 2^32 (A is the left operand). */
+typedef enum {
+    DPAR_SUM = 0,
+    DPAR_MAX = 1,
+    DPAR_MATMUL = 2
+} dpar_op_t;
+
+/* How the b pipeline rounds are sequenced on the device (Algorithm 1's round
+ * loop).  All give bit-identical results.
+ *   LAUNCH_PER_ROUND  one kernel launch per round j = 0 .. b-1;
+ *   GRID_BARRIER      one persistent (co-resident) launch, a device-wide
+ *                     barrier after each round;
+ *   TICKET            one persistent launch; workgroups claim (round, chunk)
+ *                     work items from an atomic counter in increasing round
+ *                     order, no barrier, several rounds in flight;
+ *   AUTO              TICKET. */
+typedef enum {
+    DPAR_EXEC_AUTO = 0,
+    DPAR_EXEC_LAUNCH_PER_ROUND = 1,
+    DPAR_EXEC_GRID_BARRIER = 2,
+    DPAR_EXEC_TICKET = 3
+} dpar_exec_t;
+
+/* One rank's place in the two trees (Section 1.1).  -1 means "none". */
+typedef struct {
+    int parent;
+    int child0;     /* first child: rank-1 whenever the rank has a child */
+    int child1;     /* second child (the i'' of Section 1.1) */
+    int depth;      /* d_i: 0 at the roots */
+    int subtree_lo; /* the rank's subtree is [subtree_lo, rank] */
+    int dual;       /* the other root, for the two roots only */
+} dpar_node_t;
+
+/* Block decomposition chosen for a call (Section 1.1: b successive blocks of
+ * roughly m/b elements; Section 1.3).  Blocks are made of whole "quanta":
+ * granularity = 4 elements (16 bytes) on the vector path for INT32/FLOAT32,
+ * 1 element otherwise.  Block j holds quanta
+ *     [floor(j*Q/b), floor((j+1)*Q/b)),   Q = nquanta,
+ * and the last block also holds the tail_elems elements that do not fill a
+ * quantum.  Inside a round a block is cut into chunks_per_block near-equal
+ * chunks of at most 64 quanta, one wavefront lane per quantum. */
+typedef struct {
+    int b;                  /* number of blocks / rounds actually used */
+    int granularity;        /* elements per quantum: 4 or 1 */
+    size_t nquanta;         /* Q */
+    size_t tail_elems;      /* elements after the last whole quantum */
+    int chunks_per_block;
+    int height;             /* H: largest depth over both trees */
+    int waves_per_chunk;    /* wavefronts that cooperate on one chunk */
+} dpar_schedule_t;
+
+/* Reduction-to-all (Section 1; Algorithm 1).
+ *   x, y    HOST arrays of p DEVICE pointers; x[i] and y[i] each address
+ *           m elements of dtype (m*16 bytes for DPAR_U32_MAT2X2).  Pointers
+ *           must be aligned to 4 bytes; when all 2p are 16-byte aligned the
+ *           vector path is used.  The library copies both arrays before
+ *           returning; the caller owns and may free them at once.  The
+ *           buffers must stay valid, and x unmodified, until the stream work
+ *           completes.
+ *   p       number of virtual ranks, >= 1.
+ *   m       elements per rank; m == 0 is a successful no-op.
+ *   b       number of pipeline blocks, 1 <= b <= m; b == 0 chooses
+ *           ceil(sqrt(m log2 p)) (dpar_block_rule with alpha = beta = 0).
+ *   stream  HIP stream (0 = the null stream).
+ * Aliasing: output buffers must not overlap each other.  An output buffer may
+ * coincide exactly with an input buffer (in place, e.g. y[i] == x[i] like
+ * the paper's Y array); any partial overlap between an output and an input
+ * returns DPAR_ERR_ALIAS.  Inputs may overlap each other.
+ * Result: for every i, y[i][k] = S(root A)[k] (.) S(root B)[k], with
+ * S(r) = S(child1) (.) (S(child0) (.) x_r[k]) (Algorithm 1's two "t (.) Y"
+ * steps and the dual-root step).  p == 1 copies x_0 to y_0. */
+int dpar_allreduce(const void* const* x, void* const* y, int p, size_t m,
+                   dpar_dtype_t dtype, dpar_op_t op, int b, hipStream_t stream);
+
+/* Same as dpar_allreduce with an explicit round executor. */
+int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
+                      dpar_dtype_t dtype, dpar_op_t op, int b,
+                      dpar_exec_t exec, hipStream_t stream);
+
+/* Tree tables of the library's host-side tree builder (Section 1.1: two
+ * post-order numbered, heap-shaped complete binary trees; tree A holds ranks
+ * [0, ceil(p/2)), tree B the rest; roots ceil(p/2)-1 and p-1 are duals).
+ * Fills *out for 0 <= rank < p.  No device work. */
+int dpar_tree_info(int p, int rank, dpar_node_t* out);
+
+/* Block-count rule (Section 1.2).  With alpha > 0 and beta > 0 it returns
+ * clamp(round(sqrt((4h - 6) beta m / (3 alpha))), 1, m) with h = log2(p + 2)
+ * (the pipelining optimum of (4h - 3 + 3(b - 1))(alpha + beta m / b));
+ * otherwise clamp(ceil(sqrt(m log2 p)), 1, m).  Returns 0 for m == 0 and a
+ * negative status for p < 1. */
+int dpar_block_rule(int p, size_t m, double alpha, double beta);
+
+/* Number of rounds in which a rank performs a non-empty exchange under
+ * Algorithm 1 with b blocks, void exchanges skipped (Sections 1.1, 1.3):
+ * b + d_i for a leaf, b + d_i + 1 for a non-leaf, b for a root without
+ * children, 0 for p == 1.  rank == -1 gives the overall count b + H.
+ * No device work. */
+int dpar_rounds(int p, int b, int rank);
+
+/* The decomposition dpar_allreduce would use for these arguments when all
+ * pointers are 16-byte aligned (aligned != 0) or not.  b == 0 applies the
+ * rule.  No device work. */
+int dpar_schedule_info(int p, size_t m, dpar_dtype_t dtype, int b, int aligned,
+                       dpar_schedule_t* out);
+
+/* Element range [*start, *end) of block j of a schedule.  No device work. */
+int dpar_block_bounds(const dpar_schedule_t* s, size_t m, int j, size_t* start,
+                      size_t* end);
+
+/* Waits for the stream, then reports a grid-barrier watchdog expiry recorded
+ * by an earlier GRID_BARRIER call on this device (DPAR_ERR_TIMEOUT, flag
+ * cleared) or a pending HIP error. */
+int dpar_check_status(hipStream_t stream);
+
+/* Text of the calling thread's last error ("" if none). */
+const char* dpar_last_error(void);
+
+/* Frees every library-owned device and pinned host buffer (device tables,
+ * counters, staging).  The library re-creates them lazily on the next call.
+ * The caller must make sure no enqueued call is still running. */
+int dpar_finalize(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DPAR_H */

@@ -1,0 +1,11 @@
+"""Doubly-pipelined, dual-root reduction-to-all (Traeff 2021) on one MI355X.
+
+The work happens in libdpar.so (include/dpar.h): host tree builder and round
+schedule in C++, the round program in HIP kernels for gfx950.  ``dpar`` is a
+thin ctypes binding with the same function names.
+"""
+
+from .dpar import (  # noqa: F401
+    DparError, allreduce, dpar_allreduce, dpar_allreduce_ex, dpar_block_bounds,
+    dpar_block_rule, dpar_check_status, dpar_finalize, dpar_last_error,
+    dpar_rounds, dpar_schedule_info, dpar_tree_info, lib, rows)

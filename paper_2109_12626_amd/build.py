@@ -1,0 +1,56 @@
+"""Builds libdpar.so in place: HIP kernels for gfx950 with hipcc, host C++
+with g++, linked by hipcc.  ``python -m paper_2109_12626_amd.build``."""
+
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+BUILD = os.path.join(ROOT, "_build")
+LIB = os.path.join(HERE, "libdpar.so")
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+ARCH = "gfx950"
+
+HIP_FLAGS = [
+    "-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
+    "-fno-fast-math", "-ffp-contract=off",
+    # keep fp32 arithmetic on the scalar (non-packed) VALU instructions
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-result",
+]
+HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-Wextra",
+              "-Wno-unused-parameter", "-D__HIP_PLATFORM_AMD__"]
+
+
+def _run(cmd):
+    print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+
+
+def build(verbose=True):
+    os.makedirs(BUILD, exist_ok=True)
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC,
+           "-I", os.path.join(ROCM, "include")]
+    hipcc = os.path.join(ROCM, "bin", "hipcc")
+    objs = []
+    for src in ("plan.cpp", "api.cpp"):
+        obj = os.path.join(BUILD, src + ".o")
+        _run(["g++"] + HOST_FLAGS + inc + ["-c", os.path.join(CSRC, src),
+                                           "-o", obj])
+        objs.append(obj)
+    obj = os.path.join(BUILD, "kernels.hip.o")
+    _run([hipcc] + HIP_FLAGS + inc + ["-c", os.path.join(CSRC, "kernels.hip"),
+                                      "-o", obj])
+    objs.append(obj)
+    tmp = LIB + ".tmp"
+    _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp]
+         + objs + ["-Wl,-soname,libdpar.so"])
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    build()
+    sys.exit(0)

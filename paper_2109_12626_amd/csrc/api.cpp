@@ -1,0 +1,481 @@
+// C ABI of libdpar: argument checks, plan cache, pointer-table staging and
+// executor dispatch (Traeff 2021, Section 1 problem statement; Algorithm 1).
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "dpar.h"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(DPAR_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int kCounterSlots = 64;      // concurrent calls before reuse
+constexpr int kCounterStride = 32;     // uint32 words: 128-byte lines
+constexpr int kStageSlots = 8;
+
+struct OpsTable {
+  uint32_t* dev = nullptr;
+  int height = 0;
+  int n_a = 0;
+};
+
+struct StageSlot {
+  std::vector<uint64_t> key;  // x pointers then y pointers
+  uint64_t* host = nullptr;   // pinned
+  uint64_t* dev = nullptr;
+  size_t cap = 0;             // entries
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+  unsigned long long last_use = 0;
+};
+
+struct DeviceState {
+  int device = -1;
+  int num_cus = 0;
+  unsigned* counters = nullptr;  // kCounterSlots lines + one error line
+  unsigned next_counter = 0;
+  std::map<int, OpsTable> ops;
+  StageSlot stage[kStageSlots];
+  unsigned long long tick = 0;
+};
+
+std::mutex g_mu;
+std::map<int, std::unique_ptr<DeviceState>> g_devices;
+
+int env_int(const char* name, int dflt) {
+  const char* v = std::getenv(name);
+  return v && *v ? std::atoi(v) : dflt;
+}
+
+unsigned long long spin_limit() {
+  const char* v = std::getenv("DPAR_SPIN_LIMIT");
+  return v && *v ? std::strtoull(v, nullptr, 10) : (1ull << 26);
+}
+
+int get_state(DeviceState** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  auto it = g_devices.find(dev);
+  if (it != g_devices.end()) {
+    *out = it->second.get();
+    return DPAR_SUCCESS;
+  }
+  auto st = std::make_unique<DeviceState>();
+  st->device = dev;
+  e = hipDeviceGetAttribute(&st->num_cus, hipDeviceAttributeMultiprocessorCount,
+                            dev);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+  const size_t words = (size_t)(kCounterSlots + 1) * kCounterStride;
+  e = hipMalloc(&st->counters, words * sizeof(unsigned));
+  if (e != hipSuccess) return fail(DPAR_ERR_NOMEM, "counters: %s",
+                                   hipGetErrorString(e));
+  e = hipMemset(st->counters, 0, words * sizeof(unsigned));
+  if (e != hipSuccess) return hip_fail(e, "hipMemset");
+  *out = st.get();
+  g_devices[dev] = std::move(st);
+  return DPAR_SUCCESS;
+}
+
+int get_ops(DeviceState* st, int p, const OpsTable** out) {
+  auto it = st->ops.find(p);
+  if (it != st->ops.end()) {
+    *out = &it->second;
+    return DPAR_SUCCESS;
+  }
+  const dpar::Tree t = dpar::build_tree(p);
+  const std::vector<uint32_t> ops = dpar::make_ops(t);
+  OpsTable tab;
+  tab.height = t.height;
+  tab.n_a = t.n_a;
+  std::vector<uint32_t> padded(ops);
+  padded.resize(ops.size() + dpar::kTablePad, 0u);  // kernels read ahead
+  hipError_t e = hipMalloc(&tab.dev, padded.size() * sizeof(uint32_t));
+  if (e != hipSuccess) return fail(DPAR_ERR_NOMEM, "opcode table: %s",
+                                   hipGetErrorString(e));
+  e = hipMemcpy(tab.dev, padded.data(), padded.size() * sizeof(uint32_t),
+                hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(tab.dev);
+    return hip_fail(e, "hipMemcpy opcodes");
+  }
+  st->ops[p] = tab;
+  *out = &st->ops[p];
+  return DPAR_SUCCESS;
+}
+
+// Copies the two pointer arrays into a device table, reusing a slot that
+// already holds the same arrays.  Returns the device address of [x..., y...].
+int stage_pointers(DeviceState* st, const void* const* x, void* const* y,
+                   int p, hipStream_t stream, StageSlot** used) {
+  std::vector<uint64_t> key(2 * (size_t)p);
+  for (int i = 0; i < p; ++i) {
+    key[i] = (uint64_t)(uintptr_t)x[i];
+    key[p + i] = (uint64_t)(uintptr_t)y[i];
+  }
+  ++st->tick;
+  for (auto& s : st->stage) {
+    if (s.dev && s.key == key) {
+      s.last_use = st->tick;
+      *used = &s;
+      return DPAR_SUCCESS;
+    }
+  }
+  StageSlot* s = &st->stage[0];
+  for (auto& c : st->stage)
+    if (c.last_use < s->last_use) s = &c;
+  hipError_t e;
+  if (s->pending) {  // the slot's previous table may still be read
+    e = hipEventSynchronize(s->ev);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    s->pending = false;
+  }
+  if (s->cap < key.size() + dpar::kTablePad) {
+    if (s->host) (void)hipHostFree(s->host);
+    if (s->dev) (void)hipFree(s->dev);
+    s->host = nullptr;
+    s->dev = nullptr;
+    s->cap = 0;
+    // the kernels read a few entries past the last pointer
+    const size_t cap = std::max<size_t>(key.size(), 256) + dpar::kTablePad;
+    e = hipHostMalloc(&s->host, cap * sizeof(uint64_t), hipHostMallocDefault);
+    if (e != hipSuccess) return fail(DPAR_ERR_NOMEM, "pinned staging: %s",
+                                     hipGetErrorString(e));
+    e = hipMalloc(&s->dev, cap * sizeof(uint64_t));
+    if (e != hipSuccess) return fail(DPAR_ERR_NOMEM, "pointer table: %s",
+                                     hipGetErrorString(e));
+    s->cap = cap;
+  }
+  if (!s->ev) {
+    e = hipEventCreateWithFlags(&s->ev, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+  }
+  std::memcpy(s->host, key.data(), key.size() * sizeof(uint64_t));
+  e = hipMemcpyAsync(s->dev, s->host, key.size() * sizeof(uint64_t),
+                     hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync pointer table");
+  s->key = std::move(key);
+  s->last_use = st->tick;
+  *used = s;
+  return DPAR_SUCCESS;
+}
+
+size_t elem_size(dpar_dtype_t dt) { return dt == DPAR_U32_MAT2X2 ? 16 : 4; }
+
+bool valid_pair(dpar_dtype_t dt, dpar_op_t op) {
+  return (dt == DPAR_INT32 && (op == DPAR_SUM || op == DPAR_MAX)) ||
+         (dt == DPAR_FLOAT32 && op == DPAR_SUM) ||
+         (dt == DPAR_U32_MAT2X2 && op == DPAR_MATMUL);
+}
+
+dpar::Kind kind_of(dpar_dtype_t dt, dpar_op_t op) {
+  if (dt == DPAR_U32_MAT2X2) return dpar::Kind::MAT;
+  if (dt == DPAR_FLOAT32) return dpar::Kind::F32_SUM;
+  return op == DPAR_MAX ? dpar::Kind::I32_MAX : dpar::Kind::I32_SUM;
+}
+
+// Output ranges must be pairwise disjoint; an output range may coincide
+// exactly with an input range (in place) but not overlap one partially.  All
+// 2p ranges have the same length, so two of them overlap exactly when their
+// start addresses differ by less than that length.
+bool aliasing_ok(const void* const* x, void* const* y, int p, size_t bytes) {
+  if (bytes == 0) return true;
+  std::vector<uint64_t> in(p), out(p);
+  for (int i = 0; i < p; ++i) {
+    in[i] = (uint64_t)(uintptr_t)x[i];
+    out[i] = (uint64_t)(uintptr_t)y[i];
+  }
+  std::sort(in.begin(), in.end());
+  std::sort(out.begin(), out.end());
+  for (int i = 1; i < p; ++i)
+    if (out[i] - out[i - 1] < bytes) return false;
+  for (uint64_t lo : out) {
+    const uint64_t from = lo >= bytes ? lo - bytes + 1 : 0;
+    auto first = std::lower_bound(in.begin(), in.end(), from);
+    auto last = std::lower_bound(in.begin(), in.end(), lo + bytes);
+    for (auto it = first; it != last; ++it)
+      if (*it != lo) return false;
+  }
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dpar_last_error(void) { return g_err.c_str(); }
+
+int dpar_tree_info(int p, int rank, dpar_node_t* out) {
+  g_err.clear();
+  if (p < 1 || rank < 0 || rank >= p || !out)
+    return fail(DPAR_ERR_INVALID_ARG, "dpar_tree_info: bad p/rank/out");
+  const dpar::Tree t = dpar::build_tree(p);
+  out->parent = t.parent[rank];
+  out->child0 = t.child0[rank];
+  out->child1 = t.child1[rank];
+  out->depth = t.depth[rank];
+  out->subtree_lo = t.lo[rank];
+  out->dual = t.dual[rank];
+  return DPAR_SUCCESS;
+}
+
+int dpar_block_rule(int p, size_t m, double alpha, double beta) {
+  g_err.clear();
+  if (p < 1) return fail(DPAR_ERR_INVALID_ARG, "dpar_block_rule: p < 1");
+  return (int)dpar::block_rule(p, m, alpha, beta);
+}
+
+int dpar_rounds(int p, int b, int rank) {
+  g_err.clear();
+  if (p < 1 || b < 1 || rank < -1 || rank >= p)
+    return fail(DPAR_ERR_INVALID_ARG, "dpar_rounds: bad p/b/rank");
+  return dpar::rank_rounds(dpar::build_tree(p), b, rank);
+}
+
+static int choose_schedule(int p, size_t m, dpar_dtype_t dtype, int b,
+                           bool aligned16, dpar::Schedule* s,
+                           dpar::Path* path) {
+  int g = 1;
+  *path = dpar::Path::SCALAR;
+  if (dtype == DPAR_U32_MAT2X2) {
+    if (aligned16) *path = dpar::Path::VEC16;
+  } else if (aligned16 && m / 4 >= (size_t)b) {
+    g = 4;
+    *path = dpar::Path::VEC16;
+  }
+  *s = dpar::make_schedule(m, b, g);
+  const dpar::Tree t = dpar::build_tree(p);  // height only
+  (void)t;
+  return DPAR_SUCCESS;
+}
+
+int dpar_schedule_info(int p, size_t m, dpar_dtype_t dtype, int b, int aligned,
+                       dpar_schedule_t* out) {
+  g_err.clear();
+  if (p < 1 || b < 0 || !out || m == 0)
+    return fail(DPAR_ERR_INVALID_ARG, "dpar_schedule_info: bad arguments");
+  if (dtype < DPAR_INT32 || dtype > DPAR_U32_MAT2X2)
+    return fail(DPAR_ERR_UNSUPPORTED, "dpar_schedule_info: dtype");
+  if (b == 0) b = (int)dpar::block_rule(p, m, 0.0, 0.0);
+  if ((size_t)b > m) return fail(DPAR_ERR_INVALID_ARG, "b > m");
+  dpar::Schedule s;
+  dpar::Path path;
+  choose_schedule(p, m, dtype, b, aligned != 0, &s, &path);
+  const dpar::Tree t = dpar::build_tree(p);
+  out->b = s.b;
+  out->granularity = s.g;
+  out->nquanta = s.Q;
+  out->tail_elems = s.tail;
+  out->chunks_per_block = s.C;
+  out->height = t.height;
+  out->waves_per_chunk = p >= 2 ? env_int("DPAR_WAVES", 2) == 1 ? 1 : 2 : 1;
+  return DPAR_SUCCESS;
+}
+
+int dpar_block_bounds(const dpar_schedule_t* s, size_t m, int j,
+                      size_t* start, size_t* end) {
+  g_err.clear();
+  if (!s || !start || !end || j < 0 || j >= s->b || s->b < 1)
+    return fail(DPAR_ERR_INVALID_ARG, "dpar_block_bounds: bad arguments");
+  dpar::Schedule sc;
+  sc.b = s->b;
+  sc.g = s->granularity;
+  sc.Q = s->nquanta;
+  uint64_t qs, qe;
+  dpar::block_quanta(sc, j, &qs, &qe);
+  *start = (size_t)(qs * (uint64_t)sc.g);
+  *end = (size_t)(qe * (uint64_t)sc.g);
+  if (j == s->b - 1) *end = m;  // the tail rides with the last block
+  return DPAR_SUCCESS;
+}
+
+int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
+                      dpar_dtype_t dtype, dpar_op_t op, int b,
+                      dpar_exec_t exec, hipStream_t stream) {
+  g_err.clear();
+  if (!x || !y) return fail(DPAR_ERR_INVALID_ARG, "null pointer array");
+  if (p < 1) return fail(DPAR_ERR_INVALID_ARG, "p must be >= 1");
+  if (b < 0) return fail(DPAR_ERR_INVALID_ARG, "b must be >= 0");
+  if (!valid_pair(dtype, op))
+    return fail(DPAR_ERR_UNSUPPORTED, "unsupported dtype/op pair (%d, %d)",
+                (int)dtype, (int)op);
+  if (exec < DPAR_EXEC_AUTO || exec > DPAR_EXEC_TICKET)
+    return fail(DPAR_ERR_INVALID_ARG, "unknown executor %d", (int)exec);
+  bool aligned16 = true;
+  for (int i = 0; i < p; ++i) {
+    if (!x[i] || !y[i])
+      return fail(DPAR_ERR_INVALID_ARG, "null buffer for rank %d", i);
+    const uintptr_t a = (uintptr_t)x[i], c = (uintptr_t)y[i];
+    if ((a | c) & 3)
+      return fail(DPAR_ERR_INVALID_ARG, "rank %d buffer not 4-byte aligned",
+                  i);
+    if ((a | c) & 15) aligned16 = false;
+    if (((a | c) >> 48) != 0)
+      return fail(DPAR_ERR_UNSUPPORTED, "rank %d address above 2^48", i);
+  }
+  if (m == 0) return DPAR_SUCCESS;
+  if (b == 0) b = (int)dpar::block_rule(p, m, 0.0, 0.0);
+  if ((size_t)b > m)
+    return fail(DPAR_ERR_INVALID_ARG, "b = %d exceeds m = %zu", b, m);
+  const size_t esz = elem_size(dtype);
+  if (m > (size_t)1 << 40)
+    return fail(DPAR_ERR_UNSUPPORTED, "m beyond 2^40 elements");
+  if (!aliasing_ok(x, y, p, m * esz))
+    return fail(DPAR_ERR_ALIAS, "output buffers overlap each other or "
+                                "partially overlap an input");
+
+  dpar::Schedule s;
+  dpar::Path path;
+  choose_schedule(p, m, dtype, b, aligned16, &s, &path);
+  if ((unsigned __int128)s.Q * (unsigned)(b + 1) >= ((unsigned __int128)1 << 63))
+    return fail(DPAR_ERR_UNSUPPORTED, "m * b beyond the index range");
+  if (s.units() >= (1ull << 31))
+    return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items");
+
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceState* st = nullptr;
+  int rc = get_state(&st);
+  if (rc) return rc;
+  const OpsTable* ops = nullptr;
+  rc = get_ops(st, p, &ops);
+  if (rc) return rc;
+
+  int waves = p >= 2 ? (env_int("DPAR_WAVES", 2) == 1 ? 1 : 2) : 1;
+  const int nslots = ops->height + 1;
+  const dpar::Kind kind = kind_of(dtype, op);
+  if (dpar::lds_bytes(path, kind, waves, nslots) > 65536 && waves == 2)
+    waves = 1;
+  if (dpar::lds_bytes(path, kind, waves, nslots) > 65536)
+    return fail(DPAR_ERR_UNSUPPORTED, "tree too deep for the LDS slots");
+
+  StageSlot* slot = nullptr;
+  rc = stage_pointers(st, x, y, p, stream, &slot);
+  if (rc) return rc;
+
+  const unsigned cslot = st->next_counter++ % kCounterSlots;
+  unsigned* line = st->counters + (size_t)cslot * kCounterStride;
+  dpar::Params prm{};
+  prm.p = p;
+  prm.n_a = ops->n_a;
+  prm.nslots = nslots;
+  prm.dual = p >= 2;
+  prm.Q = s.Q;
+  prm.qbase = 0;
+  prm.b = s.b;
+  prm.C = s.C;
+  prm.ticket = line + 0;
+  prm.done = line + 1;
+  prm.bar_count = line + 2;
+  prm.bar_gen = line + 3;
+  prm.err = st->counters + (size_t)kCounterSlots * kCounterStride;
+  prm.spin_limit = spin_limit();
+
+  dpar::Tables tab;
+  tab.xp = slot->dev;
+  tab.yp = slot->dev + p;
+  tab.ops = ops->dev;
+
+  const dpar::Exec ex = exec == DPAR_EXEC_AUTO ? dpar::Exec::TICKET
+                                               : (dpar::Exec)exec;
+  hipError_t e = dpar::launch(kind, path, waves, ex, tab, prm, stream,
+                              st->num_cus);
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  if (s.tail > 0) {
+    // the elements after the last whole 16-byte quantum: one more chunk of
+    // the last block, with one scalar per lane
+    dpar::Params tp = prm;
+    tp.Q = s.tail;
+    tp.qbase = s.Q * (uint64_t)s.g;
+    tp.b = 1;
+    tp.C = 1;
+    e = dpar::launch(kind, dpar::Path::SCALAR, waves,
+                     dpar::Exec::LAUNCH_PER_ROUND, tab, tp, stream,
+                     st->num_cus);
+    if (e != hipSuccess) return hip_fail(e, "tail launch");
+  }
+  e = hipEventRecord(slot->ev, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  slot->pending = true;
+  return DPAR_SUCCESS;
+}
+
+int dpar_allreduce(const void* const* x, void* const* y, int p, size_t m,
+                   dpar_dtype_t dtype, dpar_op_t op, int b,
+                   hipStream_t stream) {
+  return dpar_allreduce_ex(x, y, p, m, dtype, op, b, DPAR_EXEC_AUTO, stream);
+}
+
+int dpar_check_status(hipStream_t stream) {
+  g_err.clear();
+  hipError_t e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceState* st = nullptr;
+  int rc = get_state(&st);
+  if (rc) return rc;
+  unsigned* errw = st->counters + (size_t)kCounterSlots * kCounterStride;
+  unsigned flag = 0;
+  e = hipMemcpy(&flag, errw, sizeof flag, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
+  if (flag) {
+    // a barrier gave up: clear the flag and every barrier counter
+    const size_t words = (size_t)(kCounterSlots + 1) * kCounterStride;
+    e = hipMemset(st->counters, 0, words * sizeof(unsigned));
+    if (e != hipSuccess) return hip_fail(e, "hipMemset");
+    return fail(DPAR_ERR_TIMEOUT, "a grid-barrier wait exceeded its spin "
+                                  "limit; results of that call are unordered "
+                                  "but complete");
+  }
+  return DPAR_SUCCESS;
+}
+
+int dpar_finalize(void) {
+  g_err.clear();
+  std::lock_guard<std::mutex> lock(g_mu);
+  int prev = -1;
+  (void)hipGetDevice(&prev);
+  for (auto& kv : g_devices) {
+    DeviceState* st = kv.second.get();
+    (void)hipSetDevice(st->device);
+    (void)hipDeviceSynchronize();
+    for (auto& o : st->ops) (void)hipFree(o.second.dev);
+    for (auto& s : st->stage) {
+      if (s.ev) (void)hipEventDestroy(s.ev);
+      if (s.host) (void)hipHostFree(s.host);
+      if (s.dev) (void)hipFree(s.dev);
+    }
+    if (st->counters) (void)hipFree(st->counters);
+  }
+  g_devices.clear();
+  if (prev >= 0) (void)hipSetDevice(prev);
+  return DPAR_SUCCESS;
+}
+
+}  // extern "C"

@@ -1,0 +1,56 @@
+// Interface between the C ABI layer and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+
+namespace dpar {
+
+// Operator / lane-layout families compiled into the library.
+enum class Kind : int { I32_SUM = 0, I32_MAX = 1, F32_SUM = 2, MAT = 3 };
+// VEC16: 16-byte lanes (4 scalars or 1 matrix) on 16-byte aligned buffers.
+// SCALAR: one 4-byte scalar (or one matrix read as 4 dwords) per lane.
+enum class Path : int { VEC16 = 0, SCALAR = 1 };
+enum class Exec : int { LAUNCH_PER_ROUND = 1, GRID_BARRIER = 2, TICKET = 3 };
+
+// Scalars every kernel needs.  The tables (device pointers to the x and y
+// pointer arrays and the per-rank opcodes) are passed as separate restrict
+// parameters so the compiler reads them through the scalar cache.
+struct Params {
+  int p;            // ranks
+  int n_a;          // tree A = [0, n_a)
+  int nslots;       // LDS slots per wavefront = H + 1
+  int dual;         // 1 when there is a tree B (p >= 2)
+  uint64_t Q;       // quanta split into blocks
+  uint64_t qbase;   // first quantum index (the tail unit starts after Q)
+  int b;            // blocks = rounds
+  int C;            // chunks per block
+  unsigned* ticket;     // TICKET: next work item; reset by the last WG out
+  unsigned* done;       // TICKET: WGs finished
+  unsigned* bar_count;  // GRID_BARRIER: arrivals
+  unsigned* bar_gen;    // GRID_BARRIER: generation
+  unsigned* err;        // bit 0: a barrier wait gave up
+  unsigned long long spin_limit;
+};
+
+// Entries the host appends to the pointer and opcode tables so that the
+// kernels may read a fixed number of entries past the last rank.
+constexpr int kTablePad = 32;
+
+struct Tables {
+  const uint64_t* xp;   // [p] device addresses of x_i
+  const uint64_t* yp;   // [p] device addresses of y_i
+  const uint32_t* ops;  // [p] opcodes (plan.hpp)
+};
+
+// Enqueue one executor run over all b*C chunks of a schedule.
+// `waves` is 1 or 2 (2 needs p >= 2).  Returns the first HIP error.
+hipError_t launch(Kind kind, Path path, int waves, Exec exec,
+                  const Tables& tab, const Params& prm, hipStream_t stream,
+                  int num_cus);
+
+// Bytes of dynamic LDS a workgroup needs.
+size_t lds_bytes(Path path, Kind kind, int waves, int nslots);
+
+}  // namespace dpar

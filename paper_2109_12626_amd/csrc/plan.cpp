@@ -1,0 +1,138 @@
+// Host-side plan: trees, opcodes, round counts, block rule, decomposition.
+#include "plan.hpp"
+
+#include <algorithm>
+#include <cmath>
+#include <utility>
+
+namespace dpar {
+
+namespace {
+
+// One heap-shaped complete tree on n nodes (heap index h has children 2h and
+// 2h+1), numbered in post-order starting at `first`.  Iterative walk: a node
+// is numbered when it is popped the second time.
+void add_heap_tree(Tree& t, int first, int n) {
+  if (n <= 0) return;
+  std::vector<int> rank_of(n + 1, -1);
+  std::vector<std::pair<int, bool>> st;
+  st.reserve(64);
+  st.push_back({1, false});
+  int next = first;
+  while (!st.empty()) {
+    auto [h, expanded] = st.back();
+    st.pop_back();
+    if (expanded) {
+      rank_of[h] = next++;
+      continue;
+    }
+    st.push_back({h, true});
+    if (2 * h + 1 <= n) st.push_back({2 * h + 1, false});
+    if (2 * h <= n) st.push_back({2 * h, false});
+  }
+  for (int h = 1; h <= n; ++h) {
+    const int r = rank_of[h];
+    const int left = 2 * h, right = 2 * h + 1;
+    t.parent[r] = h > 1 ? rank_of[h / 2] : -1;
+    if (right <= n) {            // two children: the right one is r - 1
+      t.child0[r] = rank_of[right];
+      t.child1[r] = rank_of[left];
+    } else if (left <= n) {      // single child, also r - 1
+      t.child0[r] = rank_of[left];
+      t.child1[r] = -1;
+    } else {
+      t.child0[r] = t.child1[r] = -1;
+    }
+    int d = 0;
+    for (int x = h; x > 1; x >>= 1) ++d;
+    t.depth[r] = d;
+    int leftmost = h;
+    while (2 * leftmost <= n) leftmost *= 2;
+    t.lo[r] = rank_of[leftmost];
+  }
+}
+
+}  // namespace
+
+Tree build_tree(int p) {
+  Tree t;
+  t.p = p;
+  t.n_a = (p + 1) / 2;
+  t.parent.assign(p, -1);
+  t.child0.assign(p, -1);
+  t.child1.assign(p, -1);
+  t.depth.assign(p, 0);
+  t.lo.assign(p, 0);
+  t.dual.assign(p, -1);
+  add_heap_tree(t, 0, t.n_a);
+  add_heap_tree(t, t.n_a, p - t.n_a);
+  t.root_a = t.n_a - 1;
+  t.root_b = p > 1 ? p - 1 : -1;
+  if (t.root_b >= 0) {
+    t.dual[t.root_a] = t.root_b;
+    t.dual[t.root_b] = t.root_a;
+  }
+  t.height = 0;
+  for (int d : t.depth) t.height = std::max(t.height, d);
+  return t;
+}
+
+std::vector<uint32_t> make_ops(const Tree& t) {
+  std::vector<uint32_t> ops(t.p, 0);
+  for (int i = 0; i < t.p; ++i) {
+    uint32_t op = (uint32_t)t.depth[i] & OP_DEPTH_MASK;
+    if (t.child0[i] >= 0) op |= OP_C0;
+    if (t.child1[i] >= 0) op |= OP_C1;
+    const int par = t.parent[i];
+    // A second child's value waits for its sibling subtree; root A's value
+    // waits for tree B.  Everything else is consumed by the next rank.
+    if ((par >= 0 && t.child1[par] == i) || i == t.root_a) op |= OP_SAVE;
+    ops[i] = op;
+  }
+  return ops;
+}
+
+int rank_rounds(const Tree& t, int b, int rank) {
+  if (t.p == 1) return 0;
+  if (rank < 0) return b + t.height;
+  const bool leaf = t.child0[rank] < 0;
+  if (leaf && t.parent[rank] < 0) return b;
+  return leaf ? b + t.depth[rank] : b + t.depth[rank] + 1;
+}
+
+long long block_rule(int p, size_t m, double alpha, double beta) {
+  if (p < 1) return -1;
+  if (m == 0) return 0;
+  double b;
+  if (alpha > 0.0 && beta > 0.0) {
+    const double h = std::log2((double)p + 2.0);
+    b = std::floor(std::sqrt((4.0 * h - 6.0) * beta * (double)m /
+                             (3.0 * alpha)) + 0.5);
+  } else {
+    if (p == 1) return 1;
+    b = std::ceil(std::sqrt((double)m * std::log2((double)p)));
+  }
+  if (!(b >= 1.0)) b = 1.0;
+  if (b > (double)m) b = (double)m;
+  if (b > 2147483647.0) b = 2147483647.0;
+  return (long long)b;
+}
+
+Schedule make_schedule(uint64_t m, int b, int g) {
+  Schedule s;
+  s.b = b;
+  s.g = g;
+  s.Q = m / (uint64_t)g;
+  s.tail = m - s.Q * (uint64_t)g;
+  const uint64_t max_block = (s.Q + (uint64_t)b - 1) / (uint64_t)b;
+  s.C = (int)std::max<uint64_t>(1, (max_block + 63) / 64);
+  return s;
+}
+
+void block_quanta(const Schedule& s, int j, uint64_t* qs, uint64_t* qe) {
+  const unsigned __int128 Q = s.Q;
+  *qs = (uint64_t)(Q * (unsigned)j / (unsigned)s.b);
+  *qe = (uint64_t)(Q * (unsigned)(j + 1) / (unsigned)s.b);
+}
+
+}  // namespace dpar

@@ -1,0 +1,60 @@
+// Host-side plan: the two trees, the per-rank round program and the block
+// decomposition (Traeff 2021, Sections 1.1 and 1.2).  Pure C++, no HIP.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+namespace dpar {
+
+// Per-rank opcode consumed by the device round program.  One rank's step in
+// a round (Algorithm 1): Y <- x_i; if it has a first child, Y <- t (.) Y with
+// t = the first child's block; if it has a second child, again with the
+// second child's block; then the block goes up (to the parent, or to the
+// dual root).  On the device the value going up either stays in a register
+// ("current") or waits in a per-depth LDS slot until its parent runs.
+enum : uint32_t {
+  OP_DEPTH_MASK = 0x3f,   // d_i
+  OP_C0 = 1u << 6,        // has child0: v = current (.) v
+  OP_C1 = 1u << 7,        // has child1: v = slot[d+1] (.) v
+  OP_SAVE = 1u << 8,      // result waits in slot[d] (else it becomes current)
+};
+
+struct Tree {
+  int p = 0;
+  int n_a = 0;            // tree A = [0, n_a), tree B = [n_a, p)
+  int root_a = -1, root_b = -1;
+  int height = 0;         // largest depth over both trees
+  std::vector<int> parent, child0, child1, depth, lo, dual;
+};
+
+// Heap-shaped complete binary trees, post-order numbered (Section 1.1).
+Tree build_tree(int p);
+
+// Opcodes for ranks 0..p-1 (uint32 each).
+std::vector<uint32_t> make_ops(const Tree& t);
+
+// Rounds with a non-empty exchange for one rank (rank == -1: overall).
+int rank_rounds(const Tree& t, int b, int rank);
+
+// Block-count rule of Section 1.2 (see dpar_block_rule).
+long long block_rule(int p, size_t m, double alpha, double beta);
+
+struct Schedule {
+  int b = 0;
+  int g = 1;                // elements per quantum
+  uint64_t Q = 0;           // whole quanta split into blocks
+  uint64_t tail = 0;        // elements after g*Q (vector path only)
+  int C = 1;                // chunks per block (each <= 64 quanta)
+  int waves = 1;            // wavefronts per chunk
+  uint64_t units() const { return (uint64_t)b * (uint64_t)C; }
+};
+
+// The decomposition for (m, b) with granularity g in {1, 4}.
+Schedule make_schedule(uint64_t m, int b, int g);
+
+// Quanta [qs, qe) of block j.
+void block_quanta(const Schedule& s, int j, uint64_t* qs, uint64_t* qe);
+
+}  // namespace dpar

@@ -1,0 +1,214 @@
+"""Python binding of libdpar.so (include/dpar.h).
+
+Argument marshalling only: every step of the reduction runs in the library's
+HIP kernels.  The functions keep the C names.  torch is imported first so that
+the library binds to the HIP runtime torch already loaded (one runtime per
+process); torch serves only for device memory and streams.
+"""
+
+import ctypes
+import os
+
+import torch  # noqa: F401  (must precede loading libdpar: one HIP runtime)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdpar.so")
+
+DPAR_SUCCESS = 0
+DPAR_ERR_INVALID_ARG = -1
+DPAR_ERR_UNSUPPORTED = -2
+DPAR_ERR_ALIAS = -3
+DPAR_ERR_NOMEM = -4
+DPAR_ERR_HIP = -5
+DPAR_ERR_TIMEOUT = -6
+
+DPAR_INT32, DPAR_FLOAT32, DPAR_U32_MAT2X2 = 0, 1, 2
+DPAR_SUM, DPAR_MAX, DPAR_MATMUL = 0, 1, 2
+DPAR_EXEC_AUTO, DPAR_EXEC_LAUNCH_PER_ROUND, DPAR_EXEC_GRID_BARRIER, \
+    DPAR_EXEC_TICKET = 0, 1, 2, 3
+
+DTYPES = {"int32": DPAR_INT32, "float32": DPAR_FLOAT32,
+          "u32mat2x2": DPAR_U32_MAT2X2}
+OPS = {"sum": DPAR_SUM, "max": DPAR_MAX, "matmul": DPAR_MATMUL}
+EXECS = {"auto": DPAR_EXEC_AUTO, "launch": DPAR_EXEC_LAUNCH_PER_ROUND,
+         "barrier": DPAR_EXEC_GRID_BARRIER, "ticket": DPAR_EXEC_TICKET}
+
+
+class DparError(RuntimeError):
+    def __init__(self, code, msg):
+        self.code = code
+        super().__init__(f"dpar error {code}: {msg}")
+
+
+class dpar_node_t(ctypes.Structure):
+    _fields_ = [("parent", ctypes.c_int), ("child0", ctypes.c_int),
+                ("child1", ctypes.c_int), ("depth", ctypes.c_int),
+                ("subtree_lo", ctypes.c_int), ("dual", ctypes.c_int)]
+
+
+class dpar_schedule_t(ctypes.Structure):
+    _fields_ = [("b", ctypes.c_int), ("granularity", ctypes.c_int),
+                ("nquanta", ctypes.c_size_t), ("tail_elems", ctypes.c_size_t),
+                ("chunks_per_block", ctypes.c_int), ("height", ctypes.c_int),
+                ("waves_per_chunk", ctypes.c_int)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with "
+            "`python -c 'import __graft_entry__ as g; g.build()'`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, sz, i = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+    L.dpar_allreduce.argtypes = [vp, vp, i, sz, i, i, i, vp]
+    L.dpar_allreduce_ex.argtypes = [vp, vp, i, sz, i, i, i, i, vp]
+    L.dpar_tree_info.argtypes = [i, i, ctypes.POINTER(dpar_node_t)]
+    L.dpar_block_rule.argtypes = [i, sz, ctypes.c_double, ctypes.c_double]
+    L.dpar_rounds.argtypes = [i, i, i]
+    L.dpar_schedule_info.argtypes = [i, sz, i, i, i,
+                                     ctypes.POINTER(dpar_schedule_t)]
+    L.dpar_block_bounds.argtypes = [ctypes.POINTER(dpar_schedule_t), sz, i,
+                                    ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    L.dpar_check_status.argtypes = [vp]
+    L.dpar_last_error.restype = ctypes.c_char_p
+    L.dpar_last_error.argtypes = []
+    L.dpar_finalize.argtypes = []
+    for name in ("dpar_allreduce", "dpar_allreduce_ex", "dpar_tree_info",
+                 "dpar_block_rule", "dpar_rounds", "dpar_schedule_info",
+                 "dpar_block_bounds", "dpar_check_status", "dpar_finalize"):
+        getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(rc):
+    if rc < 0:
+        raise DparError(rc, lib().dpar_last_error().decode())
+    return rc
+
+
+def _addr(v):
+    if isinstance(v, torch.Tensor):
+        return v.data_ptr()
+    return int(v)
+
+
+def _ptr_array(seq):
+    arr = (ctypes.c_void_p * len(seq))()
+    for k, v in enumerate(seq):
+        arr[k] = _addr(v)
+    return arr
+
+
+def _stream(stream):
+    if stream is None:
+        return None
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _enum(table, v):
+    return table[v] if isinstance(v, str) else int(v)
+
+
+def rows(t):
+    """Device addresses of the rows of a [p, ...] tensor."""
+    if t.dim() < 1:
+        raise ValueError("need at least one dimension")
+    step = t.stride(0) * t.element_size()
+    base = t.data_ptr()
+    return [base + i * step for i in range(t.shape[0])]
+
+
+def dpar_allreduce(x, y, p, m, dtype, op, b=0, stream=None):
+    """x, y: sequences of p device addresses (ints or tensors)."""
+    return _check(lib().dpar_allreduce(
+        _ptr_array(x), _ptr_array(y), int(p), int(m), _enum(DTYPES, dtype),
+        _enum(OPS, op), int(b), _stream(stream)))
+
+
+def dpar_allreduce_ex(x, y, p, m, dtype, op, b=0, exec="auto", stream=None):
+    return _check(lib().dpar_allreduce_ex(
+        _ptr_array(x), _ptr_array(y), int(p), int(m), _enum(DTYPES, dtype),
+        _enum(OPS, op), int(b), _enum(EXECS, exec), _stream(stream)))
+
+
+def dpar_tree_info(p, rank):
+    out = dpar_node_t()
+    _check(lib().dpar_tree_info(int(p), int(rank), ctypes.byref(out)))
+    return {f: getattr(out, f) for f, _ in dpar_node_t._fields_}
+
+
+def dpar_block_rule(p, m, alpha=0.0, beta=0.0):
+    return _check(lib().dpar_block_rule(int(p), int(m), float(alpha),
+                                        float(beta)))
+
+
+def dpar_rounds(p, b, rank=-1):
+    return _check(lib().dpar_rounds(int(p), int(b), int(rank)))
+
+
+def dpar_schedule_info(p, m, dtype, b=0, aligned=True):
+    out = dpar_schedule_t()
+    _check(lib().dpar_schedule_info(int(p), int(m), _enum(DTYPES, dtype),
+                                    int(b), int(bool(aligned)),
+                                    ctypes.byref(out)))
+    return out
+
+
+def dpar_block_bounds(sched, m, j):
+    s, e = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().dpar_block_bounds(ctypes.byref(sched), int(m), int(j),
+                                   ctypes.byref(s), ctypes.byref(e)))
+    return s.value, e.value
+
+
+def dpar_check_status(stream=None):
+    return _check(lib().dpar_check_status(_stream(stream)))
+
+
+def dpar_last_error():
+    return lib().dpar_last_error().decode()
+
+
+def dpar_finalize():
+    return _check(lib().dpar_finalize())
+
+
+# ------------------------------------------------------------ convenience
+
+_ELEM = {"int32": 4, "float32": 4, "u32mat2x2": 16}
+
+
+def allreduce(x, y=None, dtype=None, op="sum", b=0, exec="auto", stream=None):
+    """Tensor front end: x is a [p, m] (or [p, m, 4] uint32 for matrices)
+    device tensor, or a list of p 1-D tensors; y likewise (default: a new
+    [p, ...] tensor).  Returns y.  Only marshals addresses."""
+    if isinstance(x, torch.Tensor):
+        p = x.shape[0]
+        xs = rows(x)
+        sample = x[0]
+    else:
+        p = len(x)
+        xs = [t.data_ptr() for t in x]
+        sample = x[0]
+    if dtype is None:
+        dtype = {torch.int32: "int32", torch.float32: "float32",
+                 torch.uint32: "u32mat2x2"}[sample.dtype]
+    m = sample.numel() * sample.element_size() // _ELEM[dtype]
+    if y is None:
+        y = torch.empty((p,) + tuple(sample.shape), dtype=sample.dtype,
+                        device=sample.device)
+    ys = rows(y) if isinstance(y, torch.Tensor) else [t.data_ptr() for t in y]
+    if stream is None:
+        stream = torch.cuda.current_stream(sample.device)
+    dpar_allreduce_ex(xs, ys, p, m, dtype, op, b, exec, stream)
+    return y

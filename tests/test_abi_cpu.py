@@ -1,0 +1,179 @@
+"""The C ABI on the CPU: the library loads, exports every function the header
+declares, and its host-side plan (trees, round counts, block rule, block
+decomposition) agrees with the independently written oracle.  Argument
+checks run before any device work, so their error codes are testable here.
+"""
+
+import math
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2109_12626_amd import dpar
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dpar.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dpar_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = _declared()
+    assert "dpar_allreduce" in names and len(names) >= 9
+    out = subprocess.run(["nm", "-D", "--defined-only", dpar.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r" T (dpar_\w+)", out))
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    L = dpar.lib()
+    for n in names:
+        assert hasattr(L, n)
+
+
+@pytest.mark.parametrize("p", list(range(1, 70)) + [127, 128, 576, 1151, 1152,
+                                                     4097])
+def test_tree_info_matches_oracle(p):
+    t = oracle.build_trees(p)
+    none = lambda v: -1 if v is None else v  # noqa: E731
+    for i in range(p):
+        got = dpar.dpar_tree_info(p, i)
+        assert got == {"parent": none(t.parent[i]), "child0": none(t.child0[i]),
+                       "child1": none(t.child1[i]), "depth": t.depth[i],
+                       "subtree_lo": t.lo[i], "dual": none(t.dual[i])}, i
+
+
+@pytest.mark.parametrize("p", [1, 2, 3, 5, 7, 9, 14, 36, 64, 100])
+@pytest.mark.parametrize("b", [1, 2, 4, 7])
+def test_round_counts_match_simulation(p, b):
+    x = np.zeros((p, 2 * b + 2), dtype=np.int32)
+    _, tr = oracle.simulate(x, "int32", "sum", b)
+    for i in range(p):
+        assert dpar.dpar_rounds(p, b, i) == tr.span(i), i
+    assert dpar.dpar_rounds(p, b, -1) == tr.global_rounds()
+
+
+def test_block_rule_matches_oracle():
+    for p in (1, 2, 7, 36, 64, 1152, 4095):
+        for m in (0, 1, 2, 16, 1000, 1024, 1 << 16, 1 << 20, 1 << 22,
+                  12345678):
+            assert dpar.dpar_block_rule(p, m) == oracle.block_rule_lit(p, m)
+            if m:
+                assert dpar.dpar_block_rule(p, m, 3e-6, 1e-9) == \
+                    oracle.block_rule_cal(p, m, 3e-6, 1e-9)
+    assert dpar.dpar_block_rule(1152, 1 << 22) == 6532
+
+
+@pytest.mark.parametrize("m,b,dtype,aligned", [
+    (1000, 4, "int32", True), (1 << 20, 2329, "int32", True),
+    (1 << 22, 6532, "float32", True), (1 << 18, 32, "u32mat2x2", True),
+    (1003, 7, "float32", True), (16, 13, "int32", True), (5, 5, "int32", True),
+    (1000, 4, "float32", False), (12345, 17, "u32mat2x2", False),
+    (1 << 16, 817, "int32", True)])
+def test_block_decomposition(m, b, dtype, aligned):
+    s = dpar.dpar_schedule_info(36, m, dtype, b, aligned)
+    assert s.b == b
+    vec = aligned and dtype != "u32mat2x2" and m // 4 >= b
+    assert s.granularity == (4 if vec else 1)
+    assert s.nquanta * s.granularity + s.tail_elems == m
+    bounds = [dpar.dpar_block_bounds(s, m, j) for j in range(b)]
+    assert bounds[0][0] == 0 and bounds[-1][1] == m
+    for (s0, e0), (s1, _) in zip(bounds, bounds[1:]):
+        assert e0 == s1
+    sizes = [e - s_ for s_, e in bounds]
+    sizes[-1] -= s.tail_elems
+    assert min(sizes) >= 1
+    assert max(sizes) - min(sizes) <= s.granularity
+    assert abs(sizes[0] - m / b) <= 2 * s.granularity
+    # chunks: at most 64 quanta each
+    assert math.ceil(max(sizes) / s.granularity / s.chunks_per_block) <= 64
+
+
+def test_scalar_path_matches_canonical_partition():
+    m, b = 1000, 7
+    s = dpar.dpar_schedule_info(9, m, "float32", b, aligned=False)
+    for j in range(b):
+        assert dpar.dpar_block_bounds(s, m, j) == oracle.block_bounds(m, b, j)
+
+
+# ------------------------------------------------------------ argument errors
+
+A = 1 << 30  # fake, never dereferenced: every case fails before device work
+
+
+def _err(fn, *args):
+    with pytest.raises(dpar.DparError) as e:
+        fn(*args)
+    return e.value.code
+
+
+def test_argument_errors():
+    xs = [A + i * 4096 for i in range(4)]
+    ys = [A + (1 << 20) + i * 4096 for i in range(4)]
+    ok = (xs, ys, 4, 1000, "int32", "sum", 4)
+    f = dpar.dpar_allreduce
+    assert _err(f, xs, ys, 0, 1000, "int32", "sum", 4) == dpar.DPAR_ERR_INVALID_ARG
+    assert _err(f, xs, ys, 4, 1000, "int32", "sum", -1) == dpar.DPAR_ERR_INVALID_ARG
+    assert _err(f, xs, ys, 4, 1000, "int32", "sum", 1001) == \
+        dpar.DPAR_ERR_INVALID_ARG
+    assert _err(f, xs, ys, 4, 1000, "float32", "max", 4) == \
+        dpar.DPAR_ERR_UNSUPPORTED
+    assert _err(f, xs, ys, 4, 1000, "int32", "matmul", 4) == \
+        dpar.DPAR_ERR_UNSUPPORTED
+    assert _err(f, xs[:3] + [0], ys, 4, 1000, "int32", "sum", 4) == \
+        dpar.DPAR_ERR_INVALID_ARG
+    assert _err(f, xs, ys[:3] + [A + 2], 4, 1000, "int32", "sum", 4) == \
+        dpar.DPAR_ERR_INVALID_ARG                    # not 4-byte aligned
+    assert _err(dpar.dpar_allreduce_ex, *ok, 9) == dpar.DPAR_ERR_INVALID_ARG
+    # m = 0 is a successful no-op (nothing is touched)
+    assert f(xs, ys, 4, 0, "int32", "sum", 0) == 0
+
+
+def test_alias_rules():
+    f = dpar.dpar_allreduce
+    n = 1000 * 4
+    xs = [A + i * 8192 for i in range(4)]
+    ys = [A + (1 << 20) + i * 8192 for i in range(4)]
+    # two outputs overlap
+    bad = list(ys)
+    bad[2] = ys[1] + 16
+    assert _err(f, xs, bad, 4, 1000, "int32", "sum", 4) == dpar.DPAR_ERR_ALIAS
+    # an output partially overlaps an input
+    bad = list(ys)
+    bad[0] = xs[3] + 64
+    assert _err(f, xs, bad, 4, 1000, "int32", "sum", 4) == dpar.DPAR_ERR_ALIAS
+    # inputs that overlap each other are allowed: the call gets as far as the
+    # device (none here) or succeeds on a GPU
+    shared = [A] * 4
+    assert n < 8192
+    code = _call_code(f, shared, ys, 4, 1000, "int32", "sum", 4)
+    assert code != dpar.DPAR_ERR_ALIAS
+
+
+def _call_code(fn, *args):
+    try:
+        fn(*args)
+        return 0
+    except dpar.DparError as e:
+        return e.code
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"), reason="a GPU is present")
+def test_valid_call_without_gpu_fails_loudly():
+    xs = [A + i * 8192 for i in range(4)]
+    code = _call_code(dpar.dpar_allreduce, xs, xs, 4, 1000, "int32", "sum", 4)
+    assert code == dpar.DPAR_ERR_HIP
+
+
+def test_info_argument_errors():
+    assert _err(dpar.dpar_tree_info, 0, 0) == dpar.DPAR_ERR_INVALID_ARG
+    assert _err(dpar.dpar_tree_info, 5, 5) == dpar.DPAR_ERR_INVALID_ARG
+    assert _err(dpar.dpar_rounds, 5, 0, 1) == dpar.DPAR_ERR_INVALID_ARG
+    assert _err(dpar.dpar_block_rule, 0, 10) == dpar.DPAR_ERR_INVALID_ARG

@@ -1,0 +1,107 @@
+"""Full-size workloads at p = 1152, m = 2^22 (19.3 GB in, 19.3 GB out), run
+in the launch configuration the benchmark times (block count from the
+sqrt(m log2 p) rule, ticketed persistent executor).
+
+* Sampled columns (the first and last chunks, every column around a few
+  block boundaries, and random ones) are compared with the CPU oracle for
+  every rank, bit for bit.
+* Every column of every rank is checked against properties that hold at any
+  size: all p outputs are identical; int32 SUM and MAX equal the exact
+  column sum (wrapped) and maximum; fp32 SUM lies within the recursive
+  summation bound of the exact sum.
+"""
+
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import configs
+from tests._gpu import need_gpu, poisoned_like, to_dev, workload_input
+
+pytestmark = pytest.mark.gpu
+
+
+def _sample_cols(m, b, rng):
+    cols = set(range(64)) | set(range(m - 67, m))
+    for j in (1, 2, b // 2, b - 1):
+        s, _ = oracle.block_bounds(m, b, j)
+        cols |= set(range(max(0, s - 5), min(m, s + 5)))
+    cols |= set(rng.choice(m, 2048, replace=False).tolist())
+    return np.array(sorted(cols))
+
+
+def _run_full(w, op):
+    from paper_2109_12626_amd import dpar
+    x = workload_input(w)
+    b = oracle.block_rule_lit(w.p, w.m)
+    xd = to_dev(x)
+    yd = poisoned_like(xd)
+    s = torch.cuda.current_stream()
+    dpar.dpar_allreduce(dpar.rows(xd), dpar.rows(yd), w.p, w.m, w.dtype, op,
+                        b, s)
+    dpar.dpar_check_status(s)
+    return x, xd, yd, b
+
+
+def _check_sampled(x, yd, b, dtype, op, seed):
+    cols = _sample_cols(x.shape[1], b, np.random.default_rng(seed))
+    want = oracle.allreduce_tree(x[:, cols], dtype, op)
+    got = yd[:, torch.from_numpy(cols).cuda()].cpu().numpy()
+    for i in range(x.shape[0]):
+        assert np.array_equal(got[i], want), f"rank {i}"
+
+
+def _check_rows_identical(yd):
+    for i in range(1, yd.shape[0]):
+        assert torch.equal(yd[i], yd[0]), f"rank {i} differs from rank 0"
+
+
+@pytest.fixture(autouse=True)
+def _cleanup():
+    need_gpu()
+    yield
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def test_p1152_fp32_sum_full_size():
+    w = configs.P1152_F32
+    x, xd, yd, b = _run_full(w, "sum")
+    _check_sampled(x, yd, b, "float32", "sum", 1)
+    _check_rows_identical(yd)
+    # every column within the recursive-summation bound of the exact sum:
+    # at most 2 (H + 1) + 1 additions on any input's path, H = 9
+    L = 2 * (9 + 1) + 1
+    u = 2.0 ** -24
+    gamma = L * u / (1 - L * u)
+    y0 = yd[0].double()
+    step = 1 << 18
+    for c in range(0, w.m, step):
+        blk = xd[:, c:c + step].double()
+        exact = blk.sum(0)
+        mag = blk.abs().sum(0)
+        err = (y0[c:c + step] - exact).abs()
+        # fp64 summation of 1152 terms is exact to ~1e-13 relative, far
+        # below the fp32 bound
+        assert bool((err <= gamma * mag + 1e-30).all()), f"columns from {c}"
+
+
+@pytest.mark.parametrize("op", ["sum", "max"])
+def test_p1152_int32_full_size(op):
+    w = next(v for v in configs.P1152_SWEEP if v.m == 1 << 22)
+    x, xd, yd, b = _run_full(w, op)
+    _check_sampled(x, yd, b, "int32", op, 2)
+    _check_rows_identical(yd)
+    step = 1 << 18
+    y0 = yd[0]
+    for c in range(0, w.m, step):
+        blk = xd[:, c:c + step]
+        if op == "sum":
+            want = blk.to(torch.int64).sum(0)
+            want = ((want + 2 ** 31) % 2 ** 32 - 2 ** 31).to(torch.int32)
+        else:
+            want = blk.max(0).values
+        assert torch.equal(y0[c:c + step], want), f"columns from {c}"

@@ -1,0 +1,234 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, element
+by element, on seeded inputs.  Integer and matrix results must be bit-exact;
+fp32 SUM must also be bit-exact, because the kernels apply the additions in
+exactly the tree order the oracle follows (Algorithm 1's association).
+
+Small and mid-size cases compare every element of every rank's output.
+Full-size workloads compare sampled columns with the oracle and check
+properties that hold at any size for every column.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from synth import configs
+from tests._gpu import (POISON, assert_all_ranks_equal, env_waves, from_dev,
+                        need_gpu, poisoned_like, resolve_b, run, to_dev,
+                        workload_input)
+
+pytestmark = pytest.mark.gpu
+
+EXECS = ["launch", "barrier", "ticket"]
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    need_gpu()
+    yield
+    torch.cuda.synchronize()
+
+
+def _want(x, dtype, op):
+    return oracle.allreduce_tree(x, dtype, op)
+
+
+# ------------------------------------------------------------ p = 7, m = 1000
+
+@pytest.mark.parametrize("exec", EXECS)
+@pytest.mark.parametrize("b", [4, 1, 2, 7, 249, 250, 251, 1000])
+def test_p7_int32_sum_every_executor_and_b(exec, b):
+    w = configs.P7_SMALL
+    x = workload_input(w)
+    out = run(x, "int32", "sum", b, exec)
+    assert_all_ranks_equal(out, _want(x, "int32", "sum"), f"b={b} {exec}")
+
+
+@pytest.mark.parametrize("waves", [1, 2])
+@pytest.mark.parametrize("dtype,op", [("int32", "sum"), ("int32", "max"),
+                                      ("float32", "sum")])
+def test_p7_all_ops_both_wave_layouts(waves, dtype, op):
+    w = configs.P7_SMALL
+    x = workload_input(w)
+    if dtype == "float32":
+        x = synth.generate("normal_f32", 7, w.p, w.m)
+    with env_waves(waves):
+        out = run(x, dtype, op, 4)
+    assert_all_ranks_equal(out, _want(x, dtype, op))
+
+
+def test_fp32_worked_examples_on_device():
+    # the hand-derived association examples, repeated over 300 columns
+    path = "tests/golden/fp32_worked_examples.txt"
+    for line in open(path):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        name, shape, xs, tree_v, _ = (c.strip() for c in line.split("|"))
+        if shape != "heap":
+            continue
+        col = np.array([float(v) for v in xs.split()], dtype=np.float32)
+        x = np.repeat(col[:, None], 300, axis=1)
+        out = run(x, "float32", "sum", 3)
+        assert (out == np.float32(float(tree_v))).all(), name
+
+
+# ------------------------------------------------------------ edge cases
+
+@pytest.mark.parametrize("p", [1, 2, 3, 4, 5, 8, 9, 15, 16, 17, 31, 33, 100])
+@pytest.mark.parametrize("m", [1, 3, 4, 5, 64, 255, 256, 257, 1027])
+def test_small_p_and_m(p, m):
+    x = synth.generate("normal_f32", 100 + p, p, m)
+    b = min(m, 3)
+    out = run(x, "float32", "sum", b)
+    assert_all_ranks_equal(out, _want(x, "float32", "sum"), f"p={p} m={m}")
+
+
+@pytest.mark.parametrize("exec", EXECS)
+def test_m_zero_is_a_noop(exec):
+    from paper_2109_12626_amd import dpar
+    xd = torch.zeros((5, 8), dtype=torch.int32, device="cuda")
+    yd = poisoned_like(xd)
+    dpar.dpar_allreduce_ex(dpar.rows(xd), dpar.rows(yd), 5, 0, "int32", "sum",
+                           0, exec, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    assert (yd == POISON).all()
+
+
+@pytest.mark.parametrize("m,b", [(16, 13), (16, 16), (10, 10), (7, 7),
+                                 (1024, 1024), (1003, 300)])
+def test_b_large_uses_scalar_lanes(m, b):
+    x = synth.generate("uniform_int", 3, 1152, m, lo=0, hi=65535)
+    for op in ("sum", "max"):
+        out = run(x, "int32", op, b)
+        assert_all_ranks_equal(out, _want(x, "int32", op), f"{op} m={m} b={b}")
+
+
+@pytest.mark.parametrize("offset", [4, 8, 12])
+def test_unaligned_pointers(offset):
+    # rows start 4/8/12 bytes past a 16-byte boundary: scalar lanes
+    p, m = 37, 1001
+    x = synth.generate("normal_f32", 5, p, m)
+    big = torch.zeros((p, m + 8), dtype=torch.float32, device="cuda")
+    k = offset // 4
+    big[:, k:k + m] = torch.from_numpy(x).cuda()
+    yb = torch.full((p, m + 8), float("nan"), device="cuda")
+    from paper_2109_12626_amd import dpar
+    xs = [a + offset for a in dpar.rows(big)]
+    ys = [a + offset for a in dpar.rows(yb)]
+    dpar.dpar_allreduce(xs, ys, p, m, "float32", "sum", 5,
+                        torch.cuda.current_stream())
+    dpar.dpar_check_status(torch.cuda.current_stream())
+    out = yb[:, k:k + m].cpu().numpy()
+    assert_all_ranks_equal(out, _want(x, "float32", "sum"))
+    # bytes outside the rows are untouched
+    assert torch.isnan(yb[:, :k]).all() and torch.isnan(yb[:, k + m:]).all()
+
+
+def test_in_place():
+    p, m = 64, 4099
+    x = synth.generate("normal_f32", 9, p, m)
+    want = _want(x, "float32", "sum")
+    xd = to_dev(x)
+    from paper_2109_12626_amd import dpar
+    dpar.dpar_allreduce(dpar.rows(xd), dpar.rows(xd), p, m, "float32", "sum",
+                        0, torch.cuda.current_stream())
+    dpar.dpar_check_status(torch.cuda.current_stream())
+    assert_all_ranks_equal(xd.cpu().numpy(), want)
+
+
+def test_separate_allocations_and_permuted_pointer_order():
+    # buffers from separate allocations, handed over in an arbitrary order:
+    # the rank order is the order of the pointer array
+    p, m = 29, 777
+    x = synth.generate("odd_det_u32_mat", 4, p, m)
+    perm = np.random.default_rng(0).permutation(p)
+    xs_t = [to_dev(x[i]) for i in range(p)]
+    ys_t = [poisoned_like(t) for t in xs_t]
+    from paper_2109_12626_amd import dpar
+    xs = [xs_t[i].data_ptr() for i in perm]
+    ys = [ys_t[i].data_ptr() for i in perm]
+    dpar.dpar_allreduce(xs, ys, p, m, "u32mat2x2", "matmul", 5,
+                        torch.cuda.current_stream())
+    dpar.dpar_check_status(torch.cuda.current_stream())
+    want = _want(x[perm], "u32mat2x2", "matmul")
+    for i in range(p):
+        got = from_dev(ys_t[i], x)
+        assert np.array_equal(got, want), i
+
+
+def test_int32_wraps_on_device():
+    x = np.full((33, 100), 2 ** 31 - 1, dtype=np.int32)
+    out = run(x, "int32", "sum", 2)
+    assert_all_ranks_equal(out, _want(x, "int32", "sum"))
+
+
+def test_repeat_runs_are_identical():
+    p, m = 300, 1 << 14
+    x = synth.generate("normal_f32", 77, p, m)
+    outs = [run(x, "float32", "sum", b, e) for b, e in
+            ((0, "ticket"), (1, "launch"), (64, "barrier"), (0, "ticket"))]
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+    assert_all_ranks_equal(outs[0], _want(x, "float32", "sum"))
+
+
+def test_single_rank_and_two_ranks():
+    for p in (1, 2):
+        x = synth.generate("odd_det_u32_mat", 12, p, 300)
+        out = run(x, "u32mat2x2", "matmul", 7)
+        assert_all_ranks_equal(out, _want(x, "u32mat2x2", "matmul"), f"p={p}")
+
+
+def test_one_library_hip_runtime_loaded():
+    # torch's HIP runtime and the library's must be the same object
+    import paper_2109_12626_amd  # noqa: F401
+    torch.zeros(1, device="cuda")
+    maps = open("/proc/self/maps").read()
+    libs = {ln.split()[-1] for ln in maps.splitlines()
+            if "libamdhip64" in ln}
+    assert len(libs) == 1, libs
+    assert any("libdpar.so" in ln for ln in maps.splitlines())
+
+
+# ------------------------------------------------------------ workloads
+
+@pytest.mark.parametrize("b", list(configs.P36_INT.bs))
+@pytest.mark.parametrize("exec", EXECS)
+def test_p36_int32_sum_full(b, exec):
+    w = configs.P36_INT
+    x = workload_input(w)
+    bb = resolve_b(b, w.p, w.m)
+    out = run(x, "int32", "sum", bb, exec)
+    assert_all_ranks_equal(out, _want(x, "int32", "sum"), f"b={bb} {exec}")
+
+
+@pytest.mark.parametrize("dist", ["uniform_u32_mat", "odd_det_u32_mat"])
+def test_p64_matmul_full(dist):
+    w = configs.P64_MAT
+    x = synth.generate(dist, w.seed, w.p, w.m)
+    out = run(x, "u32mat2x2", "matmul", w.bs[0])
+    assert_all_ranks_equal(out, _want(x, "u32mat2x2", "matmul"))
+
+
+@pytest.mark.parametrize("k", [4, 10, 16])
+@pytest.mark.parametrize("op", ["max", "sum"])
+@pytest.mark.parametrize("b", [1, "rule"])
+def test_p1152_int32_sweep_full(k, op, b):
+    w = next(v for v in configs.P1152_SWEEP if v.m == 1 << k)
+    x = workload_input(w)
+    bb = resolve_b(b, w.p, w.m)
+    out = run(x, "int32", op, bb)
+    assert_all_ranks_equal(out, _want(x, "int32", op), f"m=2^{k} b={bb}")
+
+
+def test_p1152_fp32_reduced_size_every_element():
+    # the headline shape with fewer columns (several chunks and a ragged tail)
+    w = configs.P1152_F32
+    m = 3 * 4096 + 7
+    x = workload_input(w, m=m)
+    for exec in EXECS:
+        out = run(x, "float32", "sum", resolve_b("rule", w.p, m), exec)
+        assert_all_ranks_equal(out, _want(x, "float32", "sum"), exec)
