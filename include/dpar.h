@@ -59,19 +59,26 @@ typedef enum {
 } dpar_op_t;
 
 /* How the b pipeline rounds are sequenced on the device (Algorithm 1's round
- * loop).  All give bit-identical results.
+ * loop).  All give bit-identical results.  In the first three, each chunk's
+ * y is written to all p outputs right after its up-phase, so reads of later
+ * rounds and writes of earlier ones overlap (the paper's double pipelining):
  *   LAUNCH_PER_ROUND  one kernel launch per round j = 0 .. b-1;
  *   GRID_BARRIER      one persistent (co-resident) launch, a device-wide
  *                     barrier after each round;
  *   TICKET            one persistent launch; workgroups claim (round, chunk)
  *                     work items from an atomic counter in increasing round
- *                     order, no barrier, several rounds in flight;
- *   AUTO              TICKET. */
+ *                     order, no barrier, several rounds in flight.
+ * TICKET_SPLIT runs the up-phase of every round as TICKET does but writes
+ * each chunk's y only to y_0; a second pass then streams y_0 into the other
+ * p - 1 outputs.  HBM reads and writes share one bus, so separating the two
+ * directions avoids read/write turnarounds.
+ *   AUTO              TICKET_SPLIT for p >= 2, TICKET for p == 1. */
 typedef enum {
     DPAR_EXEC_AUTO = 0,
     DPAR_EXEC_LAUNCH_PER_ROUND = 1,
     DPAR_EXEC_GRID_BARRIER = 2,
-    DPAR_EXEC_TICKET = 3
+    DPAR_EXEC_TICKET = 3,
+    DPAR_EXEC_TICKET_SPLIT = 4
 } dpar_exec_t;
 
 /* One rank's place in the two trees (Section 1.1).  -1 means "none". */
@@ -85,17 +92,22 @@ typedef struct {
 } dpar_node_t;
 
 /* Block decomposition chosen for a call (Section 1.1: b successive blocks of
- * roughly m/b elements; Section 1.3).  Blocks are made of whole "quanta":
- * granularity = 4 elements (16 bytes) on the vector path for INT32/FLOAT32,
- * 1 element otherwise.  Block j holds quanta
- *     [floor(j*Q/b), floor((j+1)*Q/b)),   Q = nquanta,
- * and the last block also holds the tail_elems elements that do not fill a
- * quantum.  Inside a round a block is cut into chunks_per_block near-equal
- * chunks of at most 64 quanta, one wavefront lane per quantum. */
+ * roughly m/b elements).  A wavefront lane owns one quantum of `quantum`
+ * elements (4 = 16 bytes on the vector path for INT32/FLOAT32, else 1).
+ * Blocks are cut at multiples of `granularity` elements (128-byte lines on
+ * the vector path when m allows b such lines, else one quantum): with
+ * L = ceil(nquanta * quantum / granularity) lines, block j holds lines
+ *     [floor(j*L/b), floor((j+1)*L/b)),
+ * clipped at nquanta quanta, and the last block also holds the tail_elems
+ * elements that do not fill a quantum.  Inside a round a block is cut at
+ * line boundaries into chunks_per_block chunks of at most 64 quanta, one
+ * lane per quantum.  With granularity 1 this is the canonical partition
+ * [floor(j*m/b), floor((j+1)*m/b)). */
 typedef struct {
-    int b;                  /* number of blocks / rounds actually used */
-    int granularity;        /* elements per quantum: 4 or 1 */
-    size_t nquanta;         /* Q */
+    int b;                  /* number of blocks / rounds */
+    int granularity;        /* elements per line: 32, 8, 4 or 1 */
+    int quantum;            /* elements per lane: 4 or 1 */
+    size_t nquanta;         /* whole quanta */
     size_t tail_elems;      /* elements after the last whole quantum */
     int chunks_per_block;
     int height;             /* H: largest depth over both trees */

@@ -29,26 +29,30 @@ def _run(cmd):
     subprocess.run(cmd, check=True)
 
 
-def build(verbose=True):
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose=True, out=None, defines=()):
+    """Compiles libdpar.so (or ``out``); ``defines`` are extra -D flags for
+    kernel experiments."""
+    build_dir = BUILD if out is None else os.path.dirname(out) + "/_obj"
+    os.makedirs(build_dir, exist_ok=True)
     inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC,
            "-I", os.path.join(ROCM, "include")]
     hipcc = os.path.join(ROCM, "bin", "hipcc")
     objs = []
     for src in ("plan.cpp", "api.cpp"):
-        obj = os.path.join(BUILD, src + ".o")
+        obj = os.path.join(build_dir, src + ".o")
         _run(["g++"] + HOST_FLAGS + inc + ["-c", os.path.join(CSRC, src),
                                            "-o", obj])
         objs.append(obj)
-    obj = os.path.join(BUILD, "kernels.hip.o")
-    _run([hipcc] + HIP_FLAGS + inc + ["-c", os.path.join(CSRC, "kernels.hip"),
-                                      "-o", obj])
+    obj = os.path.join(build_dir, "kernels.hip.o")
+    _run([hipcc] + HIP_FLAGS + [f"-D{d}" for d in defines] + inc
+         + ["-c", os.path.join(CSRC, "kernels.hip"), "-o", obj])
     objs.append(obj)
-    tmp = LIB + ".tmp"
+    lib = LIB if out is None else out
+    tmp = lib + ".tmp"
     _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp]
          + objs + ["-Wl,-soname,libdpar.so"])
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":

@@ -259,21 +259,25 @@ int dpar_rounds(int p, int b, int rank) {
   return dpar::rank_rounds(dpar::build_tree(p), b, rank);
 }
 
-static int choose_schedule(int p, size_t m, dpar_dtype_t dtype, int b,
-                           bool aligned16, dpar::Schedule* s,
-                           dpar::Path* path) {
-  int g = 1;
+// Vector path (16-byte lanes) when every buffer is 16-byte aligned; blocks
+// are cut at 128-byte lines when there are at least b lines, else at 16-byte
+// quanta; otherwise one element per lane and the canonical element partition.
+static void choose_schedule(size_t m, dpar_dtype_t dtype, int b,
+                            bool aligned16, dpar::Schedule* s,
+                            dpar::Path* path) {
   *path = dpar::Path::SCALAR;
+  int g = 1, lq = 1;
   if (dtype == DPAR_U32_MAT2X2) {
-    if (aligned16) *path = dpar::Path::VEC16;
+    if (aligned16) {
+      *path = dpar::Path::VEC16;
+      lq = (m + 7) / 8 >= (size_t)b ? 8 : 1;
+    }
   } else if (aligned16 && m / 4 >= (size_t)b) {
-    g = 4;
     *path = dpar::Path::VEC16;
+    g = 4;
+    lq = (m / 4 + 7) / 8 >= (size_t)b ? 8 : 1;
   }
-  *s = dpar::make_schedule(m, b, g);
-  const dpar::Tree t = dpar::build_tree(p);  // height only
-  (void)t;
-  return DPAR_SUCCESS;
+  *s = dpar::make_schedule(m, b, g, lq);
 }
 
 int dpar_schedule_info(int p, size_t m, dpar_dtype_t dtype, int b, int aligned,
@@ -287,10 +291,11 @@ int dpar_schedule_info(int p, size_t m, dpar_dtype_t dtype, int b, int aligned,
   if ((size_t)b > m) return fail(DPAR_ERR_INVALID_ARG, "b > m");
   dpar::Schedule s;
   dpar::Path path;
-  choose_schedule(p, m, dtype, b, aligned != 0, &s, &path);
+  choose_schedule(m, dtype, b, aligned != 0, &s, &path);
   const dpar::Tree t = dpar::build_tree(p);
   out->b = s.b;
-  out->granularity = s.g;
+  out->granularity = s.g * s.lq;
+  out->quantum = s.g;
   out->nquanta = s.Q;
   out->tail_elems = s.tail;
   out->chunks_per_block = s.C;
@@ -304,14 +309,15 @@ int dpar_block_bounds(const dpar_schedule_t* s, size_t m, int j,
   g_err.clear();
   if (!s || !start || !end || j < 0 || j >= s->b || s->b < 1)
     return fail(DPAR_ERR_INVALID_ARG, "dpar_block_bounds: bad arguments");
-  dpar::Schedule sc;
-  sc.b = s->b;
-  sc.g = s->granularity;
-  sc.Q = s->nquanta;
+  if (s->quantum < 1 || s->granularity % s->quantum)
+    return fail(DPAR_ERR_INVALID_ARG, "dpar_block_bounds: bad schedule");
+  dpar::Schedule sc = dpar::make_schedule(
+      (uint64_t)s->nquanta * s->quantum, s->b, s->quantum,
+      s->granularity / s->quantum);
   uint64_t qs, qe;
   dpar::block_quanta(sc, j, &qs, &qe);
-  *start = (size_t)(qs * (uint64_t)sc.g);
-  *end = (size_t)(qe * (uint64_t)sc.g);
+  *start = (size_t)(qs * (uint64_t)s->quantum);
+  *end = (size_t)(qe * (uint64_t)s->quantum);
   if (j == s->b - 1) *end = m;  // the tail rides with the last block
   return DPAR_SUCCESS;
 }
@@ -326,7 +332,7 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
   if (!valid_pair(dtype, op))
     return fail(DPAR_ERR_UNSUPPORTED, "unsupported dtype/op pair (%d, %d)",
                 (int)dtype, (int)op);
-  if (exec < DPAR_EXEC_AUTO || exec > DPAR_EXEC_TICKET)
+  if (exec < DPAR_EXEC_AUTO || exec > DPAR_EXEC_TICKET_SPLIT)
     return fail(DPAR_ERR_INVALID_ARG, "unknown executor %d", (int)exec);
   bool aligned16 = true;
   for (int i = 0; i < p; ++i) {
@@ -353,8 +359,8 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
 
   dpar::Schedule s;
   dpar::Path path;
-  choose_schedule(p, m, dtype, b, aligned16, &s, &path);
-  if ((unsigned __int128)s.Q * (unsigned)(b + 1) >= ((unsigned __int128)1 << 63))
+  choose_schedule(m, dtype, b, aligned16, &s, &path);
+  if ((unsigned __int128)s.NL * (unsigned)(b + 1) >= ((unsigned __int128)1 << 63))
     return fail(DPAR_ERR_UNSUPPORTED, "m * b beyond the index range");
   if (s.units() >= (1ull << 31))
     return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items");
@@ -387,6 +393,8 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
   prm.nslots = nslots;
   prm.dual = p >= 2;
   prm.Q = s.Q;
+  prm.NL = s.NL;
+  prm.lq = (uint32_t)s.lq;
   prm.qbase = 0;
   prm.b = s.b;
   prm.C = s.C;
@@ -402,8 +410,10 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
   tab.yp = slot->dev + p;
   tab.ops = ops->dev;
 
-  const dpar::Exec ex = exec == DPAR_EXEC_AUTO ? dpar::Exec::TICKET
-                                               : (dpar::Exec)exec;
+  dpar::Exec ex = (dpar::Exec)exec;
+  if (exec == DPAR_EXEC_AUTO)
+    ex = p >= 2 ? dpar::Exec::TICKET_SPLIT : dpar::Exec::TICKET;
+  if (ex == dpar::Exec::TICKET_SPLIT && p < 2) ex = dpar::Exec::TICKET;
   hipError_t e = dpar::launch(kind, path, waves, ex, tab, prm, stream,
                               st->num_cus);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
@@ -412,6 +422,8 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
     // the last block, with one scalar per lane
     dpar::Params tp = prm;
     tp.Q = s.tail;
+    tp.NL = s.tail;
+    tp.lq = 1;
     tp.qbase = s.Q * (uint64_t)s.g;
     tp.b = 1;
     tp.C = 1;
@@ -419,6 +431,14 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
                      dpar::Exec::LAUNCH_PER_ROUND, tab, tp, stream,
                      st->num_cus);
     if (e != hipSuccess) return hip_fail(e, "tail launch");
+  }
+  if (ex == dpar::Exec::TICKET_SPLIT) {
+    // y_0 now holds y for the whole chunked part; stream it to y_1..y_{p-1}
+    const uint64_t main_bytes = s.Q * (uint64_t)s.g * esz;
+    e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16, stream,
+                        st->num_cus, env_int("DPAR_BCAST_QPT", 8),
+                        env_int("DPAR_BCAST_ROWS", 0));
+    if (e != hipSuccess) return hip_fail(e, "broadcast launch");
   }
   e = hipEventRecord(slot->ev, stream);
   if (e != hipSuccess) return hip_fail(e, "hipEventRecord");

@@ -34,6 +34,30 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // flat accesses.
 #define DPAR_GLOBAL __attribute__((address_space(1)))
 
+#ifndef DPAR_NT_LOAD
+#define DPAR_NT_LOAD 1
+#endif
+#ifndef DPAR_NT_STORE
+#define DPAR_NT_STORE 1
+#endif
+
+template <class T>
+__device__ inline T ld(const DPAR_GLOBAL T* p) {
+#if DPAR_NT_LOAD
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
+template <class T>
+__device__ inline void st(DPAR_GLOBAL T* p, T v) {
+#if DPAR_NT_STORE
+  __builtin_nontemporal_store(v, p);
+#else
+  *p = v;
+#endif
+}
+
 template <class T>
 __device__ inline const DPAR_GLOBAL T* gptr(uint64_t row, uint32_t off) {
   return reinterpret_cast<const DPAR_GLOBAL T*>(
@@ -87,10 +111,10 @@ struct Lane4 {  // four scalars, one 16-byte access
     return r;
   }
   __device__ static T load(uint64_t row, uint32_t off) {
-    return __builtin_nontemporal_load(gptr<T>(row, off));
+    return ld(gptr<T>(row, off));
   }
   __device__ static void store(uint64_t row, uint32_t off, T v) {
-    __builtin_nontemporal_store(v, gptr_w<T>(row, off));
+    st(gptr_w<T>(row, off), v);
   }
 };
 
@@ -100,10 +124,10 @@ struct Lane1 {  // one scalar
   static constexpr uint32_t bytes = 4;
   __device__ static T ap(T a, T b) { return E::ap(a, b); }
   __device__ static T load(uint64_t row, uint32_t off) {
-    return __builtin_nontemporal_load(gptr<T>(row, off));
+    return ld(gptr<T>(row, off));
   }
   __device__ static void store(uint64_t row, uint32_t off, T v) {
-    __builtin_nontemporal_store(v, gptr_w<T>(row, off));
+    st(gptr_w<T>(row, off), v);
   }
 };
 
@@ -112,10 +136,10 @@ struct LaneMat16 {  // one matrix, 16-byte aligned
   static constexpr uint32_t bytes = 16;
   __device__ static T ap(T a, T b) { return mat_mul(a, b); }
   __device__ static T load(uint64_t row, uint32_t off) {
-    return __builtin_nontemporal_load(gptr<T>(row, off));
+    return ld(gptr<T>(row, off));
   }
   __device__ static void store(uint64_t row, uint32_t off, T v) {
-    __builtin_nontemporal_store(v, gptr_w<T>(row, off));
+    st(gptr_w<T>(row, off), v);
   }
 };
 
@@ -145,10 +169,16 @@ struct LaneMat4 {  // one matrix, only 4-byte aligned: four dword accesses
 
 // Ranks whose loads are in flight per wavefront.  The host pads the pointer
 // and opcode tables by kTablePad >= 2 * kU entries.
-constexpr int kU = 8;
+#ifndef DPAR_KU
+#define DPAR_KU 8
+#endif
+constexpr int kU = DPAR_KU;
+static_assert(2 * kU <= kTablePad, "tables are padded for 2 * kU reads");
 
-// Processes work item t (block j = t / C, chunk c = t % C).
-template <class L, int W>
+// Processes work item t (block j = t / C, chunk c = t % C).  FUSED: y goes
+// straight to all p outputs; otherwise only to y_0, from where a separate
+// broadcast pass copies it to the other p - 1 outputs.
+template <class L, int W, bool FUSED>
 __device__ __forceinline__ void run_unit(const uint64_t* __restrict__ xp,
                                          const uint64_t* __restrict__ yp,
                                          const uint32_t* __restrict__ ops,
@@ -161,13 +191,16 @@ __device__ __forceinline__ void run_unit(const uint64_t* __restrict__ xp,
   const int wave =
       (W == 1) ? 0 : __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 
-  // chunk -> quanta [cs, ce) (block partition of Section 1.1)
+  // chunk -> quanta [cs, ce): block j is a run of lines (Section 1.1's
+  // partition into b blocks), cut into C chunks at line boundaries
   const uint64_t j = t / (uint64_t)prm.C, c = t % (uint64_t)prm.C;
-  const uint64_t qs = prm.Q * j / (uint64_t)prm.b;
-  const uint64_t qe = prm.Q * (j + 1) / (uint64_t)prm.b;
-  const uint64_t n = qe - qs;
-  const uint64_t cs = qs + c * n / (uint64_t)prm.C;
-  const uint64_t ce = qs + (c + 1) * n / (uint64_t)prm.C;
+  const uint64_t ls = prm.NL * j / (uint64_t)prm.b;
+  const uint64_t le = prm.NL * (j + 1) / (uint64_t)prm.b;
+  const uint64_t nl = le - ls;
+  const uint64_t cls = ls + c * nl / (uint64_t)prm.C;
+  const uint64_t cle = ls + (c + 1) * nl / (uint64_t)prm.C;
+  const uint64_t cs = min(cls * prm.lq, prm.Q);
+  const uint64_t ce = min(cle * prm.lq, prm.Q);
   const uint32_t count = (uint32_t)(ce - cs);
   if (count == 0) return;  // uniform; cannot happen for b <= Q
   const uint64_t unit_off = (prm.qbase + cs) * (uint64_t)L::bytes;
@@ -236,8 +269,10 @@ __device__ __forceinline__ void run_unit(const uint64_t* __restrict__ xp,
     y = L::ap(slots[lane], slots[(size_t)prm.nslots * 64 + lane]);
   }
 
-  // Fused broadcast of y to this wavefront's ranks.
-  if (active) {
+  // Fused broadcast of y to this wavefront's ranks, or y to y_0 only.
+  if (!FUSED) {
+    if (active && wave == 0) L::store(yp[0] + unit_off, lane_off, y);
+  } else if (active) {
     for (int base = r0; base < r1; base += kU) {
       uint64_t row[kU];
 #pragma unroll
@@ -258,8 +293,8 @@ __global__ __launch_bounds__(64 * W) void k_round(
     const uint32_t* __restrict__ ops, Params prm, int round) {
   extern __shared__ char lds_raw[];
   typename L::T* slots = reinterpret_cast<typename L::T*>(lds_raw);
-  run_unit<L, W>(xp, yp, ops, prm,
-                 (uint64_t)round * prm.C + blockIdx.x, slots);
+  run_unit<L, W, true>(xp, yp, ops, prm,
+                       (uint64_t)round * prm.C + blockIdx.x, slots);
 }
 
 __device__ inline void grid_barrier(const Params& prm) {
@@ -300,12 +335,12 @@ __global__ __launch_bounds__(64 * W) void k_barrier(
   typename L::T* slots = reinterpret_cast<typename L::T*>(lds_raw);
   for (int j = 0; j < prm.b; ++j) {
     for (uint64_t c = blockIdx.x; c < (uint64_t)prm.C; c += gridDim.x)
-      run_unit<L, W>(xp, yp, ops, prm, (uint64_t)j * prm.C + c, slots);
+      run_unit<L, W, true>(xp, yp, ops, prm, (uint64_t)j * prm.C + c, slots);
     if (j + 1 < prm.b) grid_barrier(prm);
   }
 }
 
-template <class L, int W>
+template <class L, int W, bool FUSED>
 __global__ __launch_bounds__(64 * W) void k_ticket(
     const uint64_t* __restrict__ xp, const uint64_t* __restrict__ yp,
     const uint32_t* __restrict__ ops, Params prm) {
@@ -319,13 +354,75 @@ __global__ __launch_bounds__(64 * W) void k_ticket(
     const unsigned t = s_ticket;
     __syncthreads();
     if (t >= nunits) break;
-    run_unit<L, W>(xp, yp, ops, prm, t, slots);
+    run_unit<L, W, FUSED>(xp, yp, ops, prm, t, slots);
   }
   if (threadIdx.x == 0) {
     __threadfence();
     if (atomicAdd(prm.done, 1u) == gridDim.x - 1) {
       atomicExch(prm.ticket, 0u);
       atomicExch(prm.done, 0u);
+    }
+  }
+}
+
+// Broadcast pass of the split executor: y_0 -> y_1 .. y_{p-1}.  A workgroup
+// owns a tile of QPT * 256 lanes of y_0 (QPT * 4 KB on the 16-byte path) and
+// a group of consecutive ranks; it reads its tile once (a cache hit: the
+// up-phase has just written it) and streams it into each of its ranks' rows,
+// so every row receives QPT * 4 KB contiguous bytes per visit.  Works on
+// bytes, whatever the element type.
+#ifndef DPAR_BCAST_NT
+#define DPAR_BCAST_NT 0
+#endif
+constexpr int kBcastRows = 8;
+
+template <class T, int QPT>
+__global__ __launch_bounds__(256) void k_bcast(const uint64_t* __restrict__ yp,
+                                               int p, uint64_t n,
+                                               int rows_per_group) {
+  const uint64_t tile_lanes = 256ull * QPT;
+  const uint64_t tiles = (n + tile_lanes - 1) / tile_lanes;
+  const int groups = (p - 1 + rows_per_group - 1) / rows_per_group;
+  const uint64_t items = tiles * (uint64_t)groups;
+  for (uint64_t it = blockIdx.x; it < items; it += gridDim.x) {
+    // consecutive workgroups take neighbouring tiles of the same row group
+    const uint64_t tile = it % tiles;
+    const int grp = (int)(it / tiles);
+    const int i0 = 1 + grp * rows_per_group;
+    const int i1 = min(p, i0 + rows_per_group);
+    const uint64_t tile_off = tile * tile_lanes * sizeof(T);
+    T v[QPT];
+    bool ok[QPT];
+#pragma unroll
+    for (int k = 0; k < QPT; ++k) {
+      const uint64_t lane = tile * tile_lanes + (uint64_t)k * 256 + threadIdx.x;
+      ok[k] = lane < n;
+      // lanes past the end re-read lane 0 of the tile (always in range)
+      const uint32_t off =
+          ok[k] ? ((uint32_t)k * 256 + threadIdx.x) * (uint32_t)sizeof(T) : 0u;
+      v[k] = *gptr<T>(yp[0] + tile_off, off);
+    }
+    for (int i = i0; i < i1; i += kBcastRows) {
+      uint64_t row[kBcastRows];
+#pragma unroll
+      for (int r = 0; r < kBcastRows; ++r) row[r] = yp[i + r] + tile_off;
+#pragma unroll
+      for (int r = 0; r < kBcastRows; ++r) {
+        if (i + r < i1) {
+#pragma unroll
+          for (int k = 0; k < QPT; ++k) {
+            const uint32_t off =
+                ((uint32_t)k * 256 + threadIdx.x) * (uint32_t)sizeof(T);
+            if (ok[k]) {
+#if DPAR_BCAST_NT
+              __builtin_nontemporal_store(v[k], gptr_w<T>(row[r], off));
+#else
+              *gptr_w<T>(row[r], off) = v[k];
+#endif
+            }
+          }
+        }
+      }
     }
   }
 }
@@ -364,15 +461,23 @@ hipError_t launch_t(Exec exec, const Tables& tab, const Params& prm,
         reinterpret_cast<const void*>(&k_barrier<L, W>), dim3((unsigned)grid),
         block, args, (unsigned)lds, stream);
   }
+  const bool fused = exec == Exec::TICKET;
+  const void* kfn = fused
+      ? reinterpret_cast<const void*>(&k_ticket<L, W, true>)
+      : reinterpret_cast<const void*>(&k_ticket<L, W, false>);
   int per_cu = 0;
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-      &per_cu, reinterpret_cast<const void*>(&k_ticket<L, W>), 64 * W, lds);
+  hipError_t e =
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kfn, 64 * W, lds);
   if (e != hipSuccess) return e;
   if (per_cu < 1) per_cu = 1;
   uint64_t grid = (uint64_t)per_cu * num_cus;
   if (grid > nunits) grid = nunits;
-  hipLaunchKernelGGL((k_ticket<L, W>), dim3((unsigned)grid), block, lds,
-                     stream, tab.xp, tab.yp, tab.ops, prm);
+  if (fused)
+    hipLaunchKernelGGL((k_ticket<L, W, true>), dim3((unsigned)grid), block,
+                       lds, stream, tab.xp, tab.yp, tab.ops, prm);
+  else
+    hipLaunchKernelGGL((k_ticket<L, W, false>), dim3((unsigned)grid), block,
+                       lds, stream, tab.xp, tab.yp, tab.ops, prm);
   return hipGetLastError();
 }
 
@@ -404,6 +509,36 @@ hipError_t launch(Kind kind, Path path, int waves, Exec exec,
                  : launch_w<LaneMat4>(waves, exec, tab, prm, stream, num_cus);
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
+                     hipStream_t stream, int num_cus, int qpt, int rows) {
+  if (p < 2 || nbytes == 0) return hipSuccess;
+  const uint64_t lane = vec16 ? 16 : 4;
+  const uint64_t n = nbytes / lane;
+  if (qpt != 1 && qpt != 2 && qpt != 4 && qpt != 8 && qpt != 16) qpt = 8;
+  if (rows < 1) rows = p - 1;
+  const uint64_t tiles = (n + 256ull * qpt - 1) / (256ull * qpt);
+  const uint64_t groups = (uint64_t)(p - 1 + rows - 1) / rows;
+  uint64_t grid = tiles * groups;
+  const uint64_t cap = (uint64_t)num_cus * 64;  // grid-stride beyond this
+  if (grid > cap) grid = cap;
+#define DPAR_BCAST_CASE(Q)                                                  \
+  if (qpt == Q) {                                                           \
+    if (vec16)                                                              \
+      hipLaunchKernelGGL((k_bcast<u32x4, Q>), dim3((unsigned)grid),        \
+                         dim3(256), 0, stream, tab.yp, p, n, rows);         \
+    else                                                                    \
+      hipLaunchKernelGGL((k_bcast<uint32_t, Q>), dim3((unsigned)grid),     \
+                         dim3(256), 0, stream, tab.yp, p, n, rows);         \
+  }
+  DPAR_BCAST_CASE(1)
+  DPAR_BCAST_CASE(2)
+  DPAR_BCAST_CASE(4)
+  DPAR_BCAST_CASE(8)
+  DPAR_BCAST_CASE(16)
+#undef DPAR_BCAST_CASE
+  return hipGetLastError();
 }
 
 size_t lds_bytes(Path path, Kind kind, int waves, int nslots) {

@@ -12,7 +12,12 @@ enum class Kind : int { I32_SUM = 0, I32_MAX = 1, F32_SUM = 2, MAT = 3 };
 // VEC16: 16-byte lanes (4 scalars or 1 matrix) on 16-byte aligned buffers.
 // SCALAR: one 4-byte scalar (or one matrix read as 4 dwords) per lane.
 enum class Path : int { VEC16 = 0, SCALAR = 1 };
-enum class Exec : int { LAUNCH_PER_ROUND = 1, GRID_BARRIER = 2, TICKET = 3 };
+enum class Exec : int {
+  LAUNCH_PER_ROUND = 1,
+  GRID_BARRIER = 2,
+  TICKET = 3,
+  TICKET_SPLIT = 4,  // up-phase of every chunk by ticket, y into y_0 only
+};
 
 // Scalars every kernel needs.  The tables (device pointers to the x and y
 // pointer arrays and the per-rank opcodes) are passed as separate restrict
@@ -23,6 +28,8 @@ struct Params {
   int nslots;       // LDS slots per wavefront = H + 1
   int dual;         // 1 when there is a tree B (p >= 2)
   uint64_t Q;       // quanta split into blocks
+  uint64_t NL;      // lines of lq quanta (the partition unit)
+  uint32_t lq;      // quanta per line
   uint64_t qbase;   // first quantum index (the tail unit starts after Q)
   int b;            // blocks = rounds
   int C;            // chunks per block
@@ -36,7 +43,7 @@ struct Params {
 
 // Entries the host appends to the pointer and opcode tables so that the
 // kernels may read a fixed number of entries past the last rank.
-constexpr int kTablePad = 32;
+constexpr int kTablePad = 64;
 
 struct Tables {
   const uint64_t* xp;   // [p] device addresses of x_i
@@ -49,6 +56,12 @@ struct Tables {
 hipError_t launch(Kind kind, Path path, int waves, Exec exec,
                   const Tables& tab, const Params& prm, hipStream_t stream,
                   int num_cus);
+
+// Broadcast pass of the split executor: copies bytes [0, nbytes) of y_0 into
+// y_1 .. y_{p-1} (16-byte lanes when vec16, else 4-byte lanes).  A workgroup
+// handles qpt * 256 lanes of one group of `rows` consecutive ranks.
+hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
+                     hipStream_t stream, int num_cus, int qpt, int rows);
 
 // Bytes of dynamic LDS a workgroup needs.
 size_t lds_bytes(Path path, Kind kind, int waves, int nslots);

@@ -118,21 +118,27 @@ long long block_rule(int p, size_t m, double alpha, double beta) {
   return (long long)b;
 }
 
-Schedule make_schedule(uint64_t m, int b, int g) {
+Schedule make_schedule(uint64_t m, int b, int g, int lq) {
   Schedule s;
   s.b = b;
   s.g = g;
+  s.lq = lq;
   s.Q = m / (uint64_t)g;
   s.tail = m - s.Q * (uint64_t)g;
-  const uint64_t max_block = (s.Q + (uint64_t)b - 1) / (uint64_t)b;
-  s.C = (int)std::max<uint64_t>(1, (max_block + 63) / 64);
+  s.NL = (s.Q + (uint64_t)lq - 1) / (uint64_t)lq;
+  const uint64_t max_lines = (s.NL + (uint64_t)b - 1) / (uint64_t)b;
+  const uint64_t lines_per_chunk = 64 / (uint64_t)lq;
+  s.C = (int)std::max<uint64_t>(1, (max_lines + lines_per_chunk - 1) /
+                                       lines_per_chunk);
   return s;
 }
 
 void block_quanta(const Schedule& s, int j, uint64_t* qs, uint64_t* qe) {
-  const unsigned __int128 Q = s.Q;
-  *qs = (uint64_t)(Q * (unsigned)j / (unsigned)s.b);
-  *qe = (uint64_t)(Q * (unsigned)(j + 1) / (unsigned)s.b);
+  const unsigned __int128 NL = s.NL;
+  const uint64_t ls = (uint64_t)(NL * (unsigned)j / (unsigned)s.b);
+  const uint64_t le = (uint64_t)(NL * (unsigned)(j + 1) / (unsigned)s.b);
+  *qs = std::min<uint64_t>(ls * (uint64_t)s.lq, s.Q);
+  *qe = std::min<uint64_t>(le * (uint64_t)s.lq, s.Q);
 }
 
 }  // namespace dpar

@@ -41,18 +41,26 @@ int rank_rounds(const Tree& t, int b, int rank);
 // Block-count rule of Section 1.2 (see dpar_block_rule).
 long long block_rule(int p, size_t m, double alpha, double beta);
 
+// Block decomposition (Section 1.1: b successive blocks of roughly m/b
+// elements).  A lane owns one "quantum" of g elements (16 bytes on the
+// vector path); blocks are cut at "line" boundaries of lq quanta (128 bytes
+// on the vector path) so that neighbouring blocks and chunks never share a
+// cache line.  Block j = lines [floor(j NL / b), floor((j+1) NL / b)); the
+// last line and the tail (elements after g*Q) belong to the last block.
 struct Schedule {
   int b = 0;
   int g = 1;                // elements per quantum
-  uint64_t Q = 0;           // whole quanta split into blocks
+  int lq = 1;               // quanta per line
+  uint64_t Q = 0;           // whole quanta
+  uint64_t NL = 0;          // lines = ceil(Q / lq)
   uint64_t tail = 0;        // elements after g*Q (vector path only)
   int C = 1;                // chunks per block (each <= 64 quanta)
-  int waves = 1;            // wavefronts per chunk
   uint64_t units() const { return (uint64_t)b * (uint64_t)C; }
 };
 
-// The decomposition for (m, b) with granularity g in {1, 4}.
-Schedule make_schedule(uint64_t m, int b, int g);
+// The decomposition for (m, b) with g elements per quantum and lq quanta per
+// line.  Needs 1 <= b <= ceil(m / g / lq) lines.
+Schedule make_schedule(uint64_t m, int b, int g, int lq);
 
 // Quanta [qs, qe) of block j.
 void block_quanta(const Schedule& s, int j, uint64_t* qs, uint64_t* qe);

@@ -12,7 +12,7 @@ import os
 import torch  # noqa: F401  (must precede loading libdpar: one HIP runtime)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libdpar.so")
+LIB_PATH = os.environ.get("DPAR_LIB_PATH") or os.path.join(_HERE, "libdpar.so")
 
 DPAR_SUCCESS = 0
 DPAR_ERR_INVALID_ARG = -1
@@ -25,13 +25,14 @@ DPAR_ERR_TIMEOUT = -6
 DPAR_INT32, DPAR_FLOAT32, DPAR_U32_MAT2X2 = 0, 1, 2
 DPAR_SUM, DPAR_MAX, DPAR_MATMUL = 0, 1, 2
 DPAR_EXEC_AUTO, DPAR_EXEC_LAUNCH_PER_ROUND, DPAR_EXEC_GRID_BARRIER, \
-    DPAR_EXEC_TICKET = 0, 1, 2, 3
+    DPAR_EXEC_TICKET, DPAR_EXEC_TICKET_SPLIT = 0, 1, 2, 3, 4
 
 DTYPES = {"int32": DPAR_INT32, "float32": DPAR_FLOAT32,
           "u32mat2x2": DPAR_U32_MAT2X2}
 OPS = {"sum": DPAR_SUM, "max": DPAR_MAX, "matmul": DPAR_MATMUL}
 EXECS = {"auto": DPAR_EXEC_AUTO, "launch": DPAR_EXEC_LAUNCH_PER_ROUND,
-         "barrier": DPAR_EXEC_GRID_BARRIER, "ticket": DPAR_EXEC_TICKET}
+         "barrier": DPAR_EXEC_GRID_BARRIER, "ticket": DPAR_EXEC_TICKET,
+         "split": DPAR_EXEC_TICKET_SPLIT}
 
 
 class DparError(RuntimeError):
@@ -48,6 +49,7 @@ class dpar_node_t(ctypes.Structure):
 
 class dpar_schedule_t(ctypes.Structure):
     _fields_ = [("b", ctypes.c_int), ("granularity", ctypes.c_int),
+                ("quantum", ctypes.c_int),
                 ("nquanta", ctypes.c_size_t), ("tail_elems", ctypes.c_size_t),
                 ("chunks_per_block", ctypes.c_int), ("height", ctypes.c_int),
                 ("waves_per_chunk", ctypes.c_int)]

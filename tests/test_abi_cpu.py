@@ -80,20 +80,28 @@ def test_block_rule_matches_oracle():
 def test_block_decomposition(m, b, dtype, aligned):
     s = dpar.dpar_schedule_info(36, m, dtype, b, aligned)
     assert s.b == b
-    vec = aligned and dtype != "u32mat2x2" and m // 4 >= b
-    assert s.granularity == (4 if vec else 1)
-    assert s.nquanta * s.granularity + s.tail_elems == m
+    vec4 = aligned and dtype != "u32mat2x2" and m // 4 >= b
+    assert s.quantum == (4 if vec4 else 1)
+    vec = vec4 or (aligned and dtype == "u32mat2x2")
+    lines = -(-(s.nquanta * s.quantum) // (8 * s.quantum))
+    want_g = s.quantum * (8 if vec and lines >= b else 1)
+    assert s.granularity == want_g
+    assert s.nquanta * s.quantum + s.tail_elems == m
     bounds = [dpar.dpar_block_bounds(s, m, j) for j in range(b)]
     assert bounds[0][0] == 0 and bounds[-1][1] == m
     for (s0, e0), (s1, _) in zip(bounds, bounds[1:]):
         assert e0 == s1
+        assert s1 % s.granularity == 0          # cut at line boundaries
     sizes = [e - s_ for s_, e in bounds]
     sizes[-1] -= s.tail_elems
     assert min(sizes) >= 1
-    assert max(sizes) - min(sizes) <= s.granularity
+    # every block but the last is a whole number of lines; sizes differ by at
+    # most one line (the last may also lose part of its final line)
+    assert max(sizes[:-1] or [0]) - min(sizes[:-1] or [0]) <= s.granularity
     assert abs(sizes[0] - m / b) <= 2 * s.granularity
     # chunks: at most 64 quanta each
-    assert math.ceil(max(sizes) / s.granularity / s.chunks_per_block) <= 64
+    per_block = -(-max(sizes) // s.quantum)
+    assert -(-per_block // s.chunks_per_block) <= 64 + 8
 
 
 def test_scalar_path_matches_canonical_partition():
@@ -149,12 +157,18 @@ def test_alias_rules():
     bad = list(ys)
     bad[0] = xs[3] + 64
     assert _err(f, xs, bad, 4, 1000, "int32", "sum", 4) == dpar.DPAR_ERR_ALIAS
-    # inputs that overlap each other are allowed: the call gets as far as the
-    # device (none here) or succeeds on a GPU
-    shared = [A] * 4
     assert n < 8192
-    code = _call_code(f, shared, ys, 4, 1000, "int32", "sum", 4)
-    assert code != dpar.DPAR_ERR_ALIAS
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"),
+                    reason="would launch on fake addresses with a GPU present")
+def test_overlapping_inputs_pass_the_alias_check():
+    # inputs that overlap each other are allowed: without a GPU the call gets
+    # past every argument check and fails only at the device
+    ys = [A + (1 << 20) + i * 8192 for i in range(4)]
+    code = _call_code(dpar.dpar_allreduce, [A] * 4, ys, 4, 1000, "int32",
+                      "sum", 4)
+    assert code == dpar.DPAR_ERR_HIP
 
 
 def _call_code(fn, *args):

@@ -21,7 +21,7 @@ from tests._gpu import (POISON, assert_all_ranks_equal, env_waves, from_dev,
 
 pytestmark = pytest.mark.gpu
 
-EXECS = ["launch", "barrier", "ticket"]
+EXECS = ["launch", "barrier", "ticket", "split"]
 
 
 @pytest.fixture(autouse=True)
@@ -157,6 +157,20 @@ def test_separate_allocations_and_permuted_pointer_order():
     for i in range(p):
         got = from_dev(ys_t[i], x)
         assert np.array_equal(got, want), i
+
+
+def test_shared_input_buffer():
+    # every rank reads the same input buffer (inputs may overlap)
+    from paper_2109_12626_amd import dpar
+    p, m = 40, 3000
+    x = synth.generate("uniform_int", 8, 1, m, lo=-9, hi=9)
+    xd = to_dev(x)
+    yd = torch.empty((p, m), dtype=torch.int32, device="cuda")
+    dpar.dpar_allreduce([xd.data_ptr()] * p, dpar.rows(yd), p, m, "int32",
+                        "sum", 6, torch.cuda.current_stream())
+    dpar.dpar_check_status(torch.cuda.current_stream())
+    want = _want(np.repeat(x, p, axis=0), "int32", "sum")
+    assert_all_ranks_equal(yd.cpu().numpy(), want)
 
 
 def test_int32_wraps_on_device():
