@@ -44,40 +44,47 @@ def kernel_sha():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def traffic_per_launch():
-    """HBM bytes per launch from committed rocprofv3 counter runs, scaled by
-    the same counters on a plain copy of known size; None when the kernel
-    source changed since the counters were taken."""
+def traffic_per_launch(phase):
+    """HBM bytes per launch of the phase's kernel from committed rocprofv3
+    counter runs (FETCH_SIZE, WRITE_SIZE in KiB per dispatch), each scaled by
+    what the same counter reads for a plain device copy of known size; None
+    when the kernel source changed since the counters were taken."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_sha") != kernel_sha():
+    if t.get("kernel_sha") != kernel_sha() or phase not in t.get("kernels", {}):
         return None
-    fetch = t["fetch_kib_per_dispatch"] * 1024 * t["fetch_scale"]
-    write = t["write_kib_per_dispatch"] * 1024 * t["write_scale"]
-    return fetch + write
+    k = t["kernels"][phase]
+    fetch = k["fetch_kib_per_dispatch"] * 1024 * t["fetch_scale"]
+    write = k["write_kib_per_dispatch"] * 1024 * t["write_scale"]
+    return int(fetch + write)
 
 
 def cpu_baseline(x_host, b):
-    """The CPU oracle, as it stands, on a bounded sample: all 1152 ranks,
-    the first 2^20 of the 2^22 columns, tree-order reduce plus the copy of y
-    into 1152 outputs.  numpy runs it on one thread."""
+    """The CPU oracle, as it stands, on the whole workload: tree-order reduce
+    of all 1152 ranks over all 2^22 columns plus the copy of y into 1152
+    outputs, repeated until at least 10 s have passed.  numpy runs it on one
+    thread."""
     import numpy as np
     import oracle
-    cols = 1 << 20
-    xs = x_host[:, :cols]
-    out = np.empty((P, cols), dtype=np.float32)
-    t0 = time.perf_counter()
-    oracle.allreduce_all([xs[i] for i in range(P)], "float32", "sum", out=out)
-    dt = time.perf_counter() - t0
-    gbs = 2.0 * P * cols * ELEM / dt / 1e9
+    out = np.empty((P, M), dtype=np.float32)
+    rows = [x_host[i] for i in range(P)]
+    runs, t0 = 0, time.perf_counter()
+    while True:
+        oracle.allreduce_all(rows, "float32", "sum", out=out)
+        runs += 1
+        dt = time.perf_counter() - t0
+        if dt >= 10.0 or runs >= 8:
+            break
+    per_run = dt / runs
+    gbs = 2.0 * P * M * ELEM / per_run / 1e9
     return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1,
             "kind": "oracle",
-            "sample": f"p={P}, first {cols} of {M} columns (1/4 of the "
-                      f"workload), tree-order reduce + copy to {P} outputs, "
-                      f"{dt:.2f} s"}
+            "sample": f"the whole workload (p={P}, m={M}): tree-order reduce "
+                      f"+ copy to {P} outputs, {runs} runs in {dt:.1f} s, "
+                      f"{per_run:.2f} s per run"}
 
 
 def calib_copy():
@@ -135,27 +142,59 @@ def main():
         step()
     dpar.dpar_check_status(stream)
 
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    split = args.exec in ("auto", "split")
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    starts = [ev() for _ in range(args.steps)]
+    mids = [ev() for _ in range(args.steps)]
+    ends = [ev() for _ in range(args.steps)]
+    for e in mids:          # create the events before handing them over
+        e.record(stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
         starts[k].record(stream)
+        if split:
+            dpar.dpar_set_phase_event(mids[k])
         step()
         ends[k].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     dpar.dpar_check_status(stream)
-    per_launch_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
-    avg_ms = sum(per_launch_ms) / len(per_launch_ms)
+    call_ms = [s_.elapsed_time(e) for s_, e in zip(starts, ends)]
+    avg_ms = sum(call_ms) / len(call_ms)
     ms_per_step = wall * 1e3 / args.steps
-
     nbytes = 2.0 * P * M * ELEM
     value = nbytes / (ms_per_step * 1e-3) / 1e9
-    achieved = nbytes / (avg_ms * 1e-3) / 1e9
-    log(f"b={b} exec={args.exec}: wall {ms_per_step:.3f} ms/step, event "
-        f"avg {avg_ms:.3f} ms (min {min(per_launch_ms):.3f}), "
-        f"{value:.1f} GB/s = {value / HBM_PEAK_GBS:.1%} of peak")
+
+    def rate(nb, ms):
+        return round(nb / (ms * 1e-3) / 1e9, 2)
+
+    phases = {"call": {"avg_ms": round(avg_ms, 4),
+                       "algorithmic_bytes": int(nbytes),
+                       "GB/s": rate(nbytes, avg_ms)}}
+    if split:
+        up_ms = sum(s_.elapsed_time(m) for s_, m in zip(starts, mids)) / args.steps
+        bc_ms = sum(m.elapsed_time(e) for m, e in zip(mids, ends)) / args.steps
+        up_bytes = P * M * ELEM + M * ELEM           # read all x, write y_0
+        bc_bytes = (P - 1) * M * ELEM                # write y_1 .. y_{p-1}
+        phases["up"] = {"kernel": "k_ticket (up-phase, y into y_0)",
+                        "avg_ms": round(up_ms, 4), "algorithmic_bytes": up_bytes,
+                        "GB/s": rate(up_bytes, up_ms)}
+        phases["broadcast"] = {"kernel": "k_bcast (y_0 to the other ranks)",
+                               "avg_ms": round(bc_ms, 4),
+                               "algorithmic_bytes": bc_bytes,
+                               "GB/s": rate(bc_bytes, bc_ms)}
+        dom = max(("up", "broadcast"), key=lambda k: phases[k]["avg_ms"])
+    else:
+        phases["fused"] = {"kernel": "k_ticket/k_round/k_barrier (fused)",
+                           "avg_ms": round(avg_ms, 4),
+                           "algorithmic_bytes": int(nbytes),
+                           "GB/s": rate(nbytes, avg_ms)}
+        dom = "fused"
+    dk = phases[dom]
+    log(f"b={b} exec={args.exec}: wall {ms_per_step:.3f} ms/step, call avg "
+        f"{avg_ms:.3f} ms (min {min(call_ms):.3f}), {value:.1f} GB/s = "
+        f"{value / HBM_PEAK_GBS:.1%} of peak; phases {json.dumps(phases)}")
 
     # spot check: a few columns against the oracle (outside the timed region)
     import oracle
@@ -189,10 +228,14 @@ def main():
                    "b": b, "block_rule": "ceil(sqrt(m log2 p))",
                    "executor": "split" if args.exec == "auto" else args.exec,
                    "bytes_per_step": int(nbytes)},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 2),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic_per_launch()},
+        "roofline": {"bound": "hbm", "kernel": dk["kernel"],
+                     "achieved": dk["GB/s"], "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s",
+                     "frac": round(dk["GB/s"] / HBM_PEAK_GBS, 4),
+                     "traffic": traffic_per_launch(dom),
+                     "per_launch_bytes": dk["algorithmic_bytes"],
+                     "avg_launch_ms": dk["avg_ms"]},
+        "phases": phases,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

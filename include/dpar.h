@@ -177,6 +177,13 @@ int dpar_block_bounds(const dpar_schedule_t* s, size_t m, int j, size_t* start,
  * cleared) or a pending HIP error. */
 int dpar_check_status(hipStream_t stream);
 
+/* Profiling aid: records `ev` on the call's stream between the up-phase and
+ * the broadcast pass of the calling thread's next call that runs the
+ * TICKET_SPLIT executor, so that each pass can be timed with HIP events.
+ * The setting is consumed by that call; NULL clears it.  It never changes
+ * what a call computes.  No device work. */
+int dpar_set_phase_event(hipEvent_t ev);
+
 /* Text of the calling thread's last error ("" if none). */
 const char* dpar_last_error(void);
 

@@ -20,6 +20,7 @@
 namespace {
 
 thread_local std::string g_err;
+thread_local hipEvent_t g_phase_event = nullptr;
 
 int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 int fail(int code, const char* fmt, ...) {
@@ -232,6 +233,12 @@ extern "C" {
 
 const char* dpar_last_error(void) { return g_err.c_str(); }
 
+int dpar_set_phase_event(hipEvent_t ev) {
+  g_err.clear();
+  g_phase_event = ev;
+  return DPAR_SUCCESS;
+}
+
 int dpar_tree_info(int p, int rank, dpar_node_t* out) {
   g_err.clear();
   if (p < 1 || rank < 0 || rank >= p || !out)
@@ -433,6 +440,11 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
     if (e != hipSuccess) return hip_fail(e, "tail launch");
   }
   if (ex == dpar::Exec::TICKET_SPLIT) {
+    if (g_phase_event) {
+      e = hipEventRecord(g_phase_event, stream);
+      g_phase_event = nullptr;
+      if (e != hipSuccess) return hip_fail(e, "hipEventRecord phase event");
+    }
     // y_0 now holds y for the whole chunked part; stream it to y_1..y_{p-1}
     const uint64_t main_bytes = s.Q * (uint64_t)s.g * esz;
     e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16, stream,

@@ -79,12 +79,14 @@ def lib():
     L.dpar_block_bounds.argtypes = [ctypes.POINTER(dpar_schedule_t), sz, i,
                                     ctypes.POINTER(sz), ctypes.POINTER(sz)]
     L.dpar_check_status.argtypes = [vp]
+    L.dpar_set_phase_event.argtypes = [vp]
     L.dpar_last_error.restype = ctypes.c_char_p
     L.dpar_last_error.argtypes = []
     L.dpar_finalize.argtypes = []
     for name in ("dpar_allreduce", "dpar_allreduce_ex", "dpar_tree_info",
                  "dpar_block_rule", "dpar_rounds", "dpar_schedule_info",
-                 "dpar_block_bounds", "dpar_check_status", "dpar_finalize"):
+                 "dpar_block_bounds", "dpar_check_status", "dpar_finalize",
+                 "dpar_set_phase_event"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -175,6 +177,18 @@ def dpar_block_bounds(sched, m, j):
 
 def dpar_check_status(stream=None):
     return _check(lib().dpar_check_status(_stream(stream)))
+
+
+def dpar_set_phase_event(event):
+    """event: a torch.cuda.Event that has been recorded once (so that it
+    exists), a raw hipEvent_t handle, or None."""
+    if event is None:
+        h = None
+    elif isinstance(event, torch.cuda.Event):
+        h = ctypes.c_void_p(event.cuda_event)
+    else:
+        h = ctypes.c_void_p(int(event))
+    return _check(lib().dpar_set_phase_event(h))
 
 
 def dpar_last_error():
