@@ -15,6 +15,7 @@ Prints ONE JSON line.  Extra lines go to stderr.
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
   python bench.py --calib-copy      # a plain 4 GiB device copy, for the
                                     # rocprofv3 FETCH/WRITE calibration
+  python bench.py --sweep OUT.jsonl # every workload, executor, block count
 """
 
 import argparse
@@ -98,6 +99,93 @@ def calib_copy():
     print(json.dumps({"calib_copy_bytes": n * 4, "dispatches": 3}))
 
 
+def sweep(out_path, only=()):
+    """Every workload x executor x block count, cold caches (a 512 MiB
+    scratch write between calls), min and median of several calls.  Writes
+    JSON lines to out_path and a table to stderr."""
+    import numpy as np
+    import torch
+
+    import synth
+    from synth import configs
+    from paper_2109_12626_amd import dpar
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    scratch = torch.empty(1 << 27, dtype=torch.float32, device=dev)
+    execs = ["split", "ticket", "launch", "barrier"]
+    out = open(out_path, "w")
+
+    def timed(fn, reps):
+        ts = []
+        for _ in range(reps):
+            scratch.fill_(1.0)                      # evict L2 and MALL
+            a = torch.cuda.Event(enable_timing=True)
+            z = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            z.record(stream)
+            z.synchronize()
+            ts.append(a.elapsed_time(z))
+        return min(ts), float(np.median(ts))
+
+    def alpha_beta(xs, ys, w, op):
+        # per-round executor cost (launch per round) and per-column cost
+        f = lambda b: (lambda: dpar.dpar_allreduce_ex(  # noqa: E731
+            xs, ys, w.p, w.m, w.dtype, op, b, "launch", stream))
+        t1 = timed(f(1), 3)[0]
+        bb = min(256, w.m)
+        tb = timed(f(bb), 3)[0]
+        alpha = max((tb - t1) / max(bb - 1, 1), 1e-4) * 1e-3   # s per round
+        beta = t1 * 1e-3 / w.m                                   # s per column
+        return alpha, beta
+
+    for w in configs.ALL:
+        if only and not any(o in w.name for o in only):
+            continue
+        x = synth.generate(w.dist, w.seed, w.p, w.m, **w.dist_kw)
+        xd = torch.from_numpy(x.view(np.int32) if x.dtype == np.uint32
+                              else x).to(dev)
+        yd = torch.empty_like(xd)
+        xs, ys = dpar.pointers(dpar.rows(xd)), dpar.pointers(dpar.rows(yd))
+        nbytes = 2.0 * w.p * w.m * (16 if w.dtype == "u32mat2x2" else 4)
+        for op in w.ops:
+            alpha, beta = alpha_beta(xs, ys, w, op)
+            bcal = dpar.dpar_block_rule(w.p, w.m, alpha, beta)
+            blist = []
+            for b in list(w.bs) + [1, "cal"]:
+                bb = (dpar.dpar_block_rule(w.p, w.m) if b == "rule" else
+                      bcal if b == "cal" else b)
+                tag = b if isinstance(b, str) else "given"
+                if bb not in [v for v, _ in blist]:
+                    blist.append((bb, tag))
+            for bb, tag in blist:
+                for ex in execs:
+                    slow = ex in ("launch", "barrier") and bb > 512
+                    reps = 2 if slow else 7
+                    fn = lambda: dpar.dpar_allreduce_ex(  # noqa: E731
+                        xs, ys, w.p, w.m, w.dtype, op, bb, ex, stream)
+                    fn()
+                    dpar.dpar_check_status(stream)
+                    tmin, tmed = timed(fn, reps)
+                    rec = {"workload": w.name, "op": op, "b": bb, "b_kind": tag,
+                           "exec": ex, "ms_min": round(tmin, 4),
+                           "ms_median": round(tmed, 4),
+                           "GB/s": round(nbytes / (tmin * 1e-3) / 1e9, 2),
+                           "pct_peak": round(100 * nbytes / (tmin * 1e-3) / 1e9
+                                             / HBM_PEAK_GBS, 2),
+                           "alpha_us": round(alpha * 1e6, 3),
+                           "beta_ns": round(beta * 1e9, 4)}
+                    out.write(json.dumps(rec) + "\n")
+                    out.flush()
+                    log(f"{w.name:34s} {op:4s} b={bb:<6d} ({tag:5s}) {ex:8s} "
+                        f"min {tmin:9.4f} ms  med {tmed:9.4f} ms  "
+                        f"{rec['GB/s']:9.1f} GB/s  {rec['pct_peak']:5.1f}%")
+        del xd, yd, x
+        torch.cuda.empty_cache()
+    out.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -105,6 +193,16 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true")
+    ap.add_argument("--sweep", metavar="OUT_JSONL",
+                    help="measure every workload, executor and block count")
+    ap.add_argument("--only", default="",
+                    help="with --sweep: comma-separated workload-name parts")
+    ap.add_argument("--workload", default=WORKLOAD,
+                    help="time another workload (name from synth.configs) "
+                         "with the same protocol; the default is the headline")
+    ap.add_argument("--op", default=None, help="with --workload")
+    ap.add_argument("--b", type=int, default=None,
+                    help="block count (default: the sqrt(m log2 p) rule)")
     ap.add_argument("--exec", default="auto",
                     choices=["auto", "launch", "barrier", "ticket", "split"])
     args = ap.parse_args()
@@ -116,6 +214,9 @@ def main():
     if args.calib_copy:
         calib_copy()
         return
+    if args.sweep:
+        sweep(args.sweep, [v for v in args.only.split(",") if v])
+        return
 
     import numpy as np
     import torch
@@ -123,19 +224,25 @@ def main():
     import synth
     from paper_2109_12626_amd import dpar
 
+    from synth import configs
+    w = next(v for v in configs.ALL if v.name == args.workload)
+    op = args.op or w.ops[0]
+    p_, m_, esz = w.p, w.m, (16 if w.dtype == "u32mat2x2" else 4)
+    headline = w.name == WORKLOAD and op == "sum" and args.b is None
     dev = torch.device("cuda:0")
     t0 = time.perf_counter()
-    x_host = synth.generate("normal_f32", SEED, P, M)
+    x_host = synth.generate(w.dist, w.seed, p_, m_, **w.dist_kw)
     log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
-    xd = torch.from_numpy(x_host).to(dev)
+    xd = torch.from_numpy(x_host.view(np.int32) if x_host.dtype == np.uint32
+                          else x_host).to(dev)
     yd = torch.empty_like(xd)
     torch.cuda.synchronize()
-    xs, ys = dpar.rows(xd), dpar.rows(yd)
-    b = dpar.dpar_block_rule(P, M)
+    xs, ys = dpar.pointers(dpar.rows(xd)), dpar.pointers(dpar.rows(yd))
+    b = args.b if args.b is not None else dpar.dpar_block_rule(p_, m_)
     stream = torch.cuda.current_stream(dev)
 
     def step():
-        dpar.dpar_allreduce_ex(xs, ys, P, M, "float32", "sum", b, args.exec,
+        dpar.dpar_allreduce_ex(xs, ys, p_, m_, w.dtype, op, b, args.exec,
                                stream)
 
     for _ in range(args.warmup):
@@ -163,7 +270,7 @@ def main():
     call_ms = [s_.elapsed_time(e) for s_, e in zip(starts, ends)]
     avg_ms = sum(call_ms) / len(call_ms)
     ms_per_step = wall * 1e3 / args.steps
-    nbytes = 2.0 * P * M * ELEM
+    nbytes = 2.0 * p_ * m_ * esz
     value = nbytes / (ms_per_step * 1e-3) / 1e9
 
     def rate(nb, ms):
@@ -175,9 +282,9 @@ def main():
     if split:
         up_ms = sum(s_.elapsed_time(m) for s_, m in zip(starts, mids)) / args.steps
         bc_ms = sum(m.elapsed_time(e) for m, e in zip(mids, ends)) / args.steps
-        up_bytes = P * M * ELEM + M * ELEM           # read all x, write y_0
-        bc_bytes = (P - 1) * M * ELEM                # write y_1 .. y_{p-1}
-        phases["up"] = {"kernel": "k_ticket (up-phase, y into y_0)",
+        up_bytes = p_ * m_ * esz + m_ * esz          # read all x, write y_0
+        bc_bytes = (p_ - 1) * m_ * esz               # write y_1 .. y_{p-1}
+        phases["up"] = {"kernel": "k_round (up-phase of every round, y into y_0)",
                         "avg_ms": round(up_ms, 4), "algorithmic_bytes": up_bytes,
                         "GB/s": rate(up_bytes, up_ms)}
         phases["broadcast"] = {"kernel": "k_bcast (y_0 to the other ranks)",
@@ -198,14 +305,17 @@ def main():
 
     # spot check: a few columns against the oracle (outside the timed region)
     import oracle
-    cols = np.array([0, 1, 2, 3, 1000, M // 2, M - 1])
-    want = oracle.allreduce_tree(x_host[:, cols], "float32", "sum")
+    cols = np.unique(np.array([0, 1, 2, 3, 1000, m_ // 2, m_ - 1]) % m_)
+    want = oracle.allreduce_tree(x_host[:, cols], w.dtype, op)
     got = yd[:, torch.from_numpy(cols).to(dev)].cpu().numpy()
-    if not all(np.array_equal(got[i], want) for i in range(P)):
+    if x_host.dtype == np.uint32:
+        got = got.view(np.uint32)
+    if not all(np.array_equal(got[i], want) for i in range(p_)):
         log("bench: spot check against the oracle FAILED")
         sys.exit(1)
 
-    cpu = None if args.no_cpu_baseline else cpu_baseline(x_host, b)
+    cpu = None if (args.no_cpu_baseline or not headline) else \
+        cpu_baseline(x_host, b)
     if cpu:
         log(f"cpu oracle: {cpu['value']} GB/s ({cpu['sample']})")
 
@@ -224,15 +334,16 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
-        "config": {"workload": WORKLOAD, "p": P, "m": M, "op": "sum",
-                   "b": b, "block_rule": "ceil(sqrt(m log2 p))",
+        "config": {"workload": w.name, "p": p_, "m": m_, "op": op,
+                   "b": b, "block_rule": ("ceil(sqrt(m log2 p))"
+                                          if args.b is None else "given"),
                    "executor": "split" if args.exec == "auto" else args.exec,
                    "bytes_per_step": int(nbytes)},
         "roofline": {"bound": "hbm", "kernel": dk["kernel"],
                      "achieved": dk["GB/s"], "peak": HBM_PEAK_GBS,
                      "unit": "GB/s",
                      "frac": round(dk["GB/s"] / HBM_PEAK_GBS, 4),
-                     "traffic": traffic_per_launch(dom),
+                     "traffic": traffic_per_launch(dom) if headline else None,
                      "per_launch_bytes": dk["algorithmic_bytes"],
                      "avg_launch_ms": dk["avg_ms"]},
         "phases": phases,

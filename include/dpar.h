@@ -66,19 +66,21 @@ typedef enum {
  *   GRID_BARRIER      one persistent (co-resident) launch, a device-wide
  *                     barrier after each round;
  *   TICKET            one persistent launch; workgroups claim (round, chunk)
- *                     work items from an atomic counter in increasing round
+ *                     work items from atomic counters in increasing round
  *                     order, no barrier, several rounds in flight.
- * TICKET_SPLIT runs the up-phase of every round as TICKET does but writes
- * each chunk's y only to y_0; a second pass then streams y_0 into the other
- * p - 1 outputs.  HBM reads and writes share one bus, so separating the two
- * directions avoids read/write turnarounds.
- *   AUTO              TICKET_SPLIT for p >= 2, TICKET for p == 1. */
+ *   SPLIT             the up-phase of every round runs first, one workgroup
+ *                     per chunk handed out by the hardware in round order,
+ *                     writing each chunk's y only to y_0; a second pass then
+ *                     streams y_0 into the other p - 1 outputs.  HBM reads
+ *                     and writes share one bus, so separating the two
+ *                     directions avoids read/write turnarounds.
+ *   AUTO              SPLIT. */
 typedef enum {
     DPAR_EXEC_AUTO = 0,
     DPAR_EXEC_LAUNCH_PER_ROUND = 1,
     DPAR_EXEC_GRID_BARRIER = 2,
     DPAR_EXEC_TICKET = 3,
-    DPAR_EXEC_TICKET_SPLIT = 4
+    DPAR_EXEC_SPLIT = 4
 } dpar_exec_t;
 
 /* One rank's place in the two trees (Section 1.1).  -1 means "none". */
@@ -178,8 +180,8 @@ int dpar_block_bounds(const dpar_schedule_t* s, size_t m, int j, size_t* start,
 int dpar_check_status(hipStream_t stream);
 
 /* Profiling aid: records `ev` on the call's stream between the up-phase and
- * the broadcast pass of the calling thread's next call that runs the
- * TICKET_SPLIT executor, so that each pass can be timed with HIP events.
+ * the broadcast pass of the calling thread's next call that runs the SPLIT
+ * executor, so that each pass can be timed with HIP events.
  * The setting is consumed by that call; NULL clears it.  It never changes
  * what a call computes.  No device work. */
 int dpar_set_phase_event(hipEvent_t ev);

@@ -9,4 +9,4 @@ from .dpar import (  # noqa: F401
     DparError, allreduce, dpar_allreduce, dpar_allreduce_ex, dpar_block_bounds,
     dpar_block_rule, dpar_check_status, dpar_finalize, dpar_last_error,
     dpar_rounds, dpar_schedule_info, dpar_set_phase_event, dpar_tree_info, lib,
-    rows)
+    pointers, rows)

@@ -38,11 +38,15 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 constexpr int kCounterSlots = 64;      // concurrent calls before reuse
-constexpr int kCounterStride = 32;     // uint32 words: 128-byte lines
+using dpar::kCounterStride;            // uint32 words: 128-byte lines
+// per call slot: kTicketCounters ticket lines, as many done-counter lines,
+// then one line for the grid-barrier words
+constexpr int kLinesPerSlot = 2 * dpar::kTicketCounters + 1;
 constexpr int kStageSlots = 8;
 
 struct OpsTable {
-  uint32_t* dev = nullptr;
+  uint32_t* dev = nullptr;   // opcodes, padded
+  uint32_t* lvl = nullptr;   // level-ordered entries + boundaries (p <= 65534)
   int height = 0;
   int n_a = 0;
 };
@@ -60,7 +64,8 @@ struct StageSlot {
 struct DeviceState {
   int device = -1;
   int num_cus = 0;
-  unsigned* counters = nullptr;  // kCounterSlots lines + one error line
+  int lds_limit = 65536;         // dynamic LDS bytes per workgroup
+  unsigned* counters = nullptr;  // kCounterSlots slots + one error line
   unsigned next_counter = 0;
   std::map<int, OpsTable> ops;
   StageSlot stage[kStageSlots];
@@ -94,7 +99,11 @@ int get_state(DeviceState** out) {
   e = hipDeviceGetAttribute(&st->num_cus, hipDeviceAttributeMultiprocessorCount,
                             dev);
   if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
-  const size_t words = (size_t)(kCounterSlots + 1) * kCounterStride;
+  e = hipDeviceGetAttribute(&st->lds_limit,
+                            hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+  const size_t words =
+      ((size_t)kCounterSlots * kLinesPerSlot + 1) * kCounterStride;
   e = hipMalloc(&st->counters, words * sizeof(unsigned));
   if (e != hipSuccess) return fail(DPAR_ERR_NOMEM, "counters: %s",
                                    hipGetErrorString(e));
@@ -127,13 +136,78 @@ int get_ops(DeviceState* st, int p, const OpsTable** out) {
     (void)hipFree(tab.dev);
     return hip_fail(e, "hipMemcpy opcodes");
   }
+  if (p <= 65534) {
+    const std::vector<uint32_t> lv = dpar::make_levels(t);
+    e = hipMalloc(&tab.lvl, lv.size() * sizeof(uint32_t));
+    if (e != hipSuccess) {
+      (void)hipFree(tab.dev);
+      return fail(DPAR_ERR_NOMEM, "level table: %s", hipGetErrorString(e));
+    }
+    e = hipMemcpy(tab.lvl, lv.data(), lv.size() * sizeof(uint32_t),
+                  hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      (void)hipFree(tab.dev);
+      (void)hipFree(tab.lvl);
+      return hip_fail(e, "hipMemcpy level table");
+    }
+  }
   st->ops[p] = tab;
   *out = &st->ops[p];
   return DPAR_SUCCESS;
 }
 
-// Copies the two pointer arrays into a device table, reusing a slot that
-// already holds the same arrays.  Returns the device address of [x..., y...].
+// Pointer sets (x then y) that passed the aliasing rules, with their row
+// length in bytes; a few recent ones, most recent first.
+struct AliasOk {
+  std::vector<uint64_t> key;
+  size_t bytes;
+};
+std::vector<AliasOk> g_alias_ok;
+
+bool same_key(const std::vector<uint64_t>& k, const void* const* x,
+              void* const* y, int p) {
+  if (k.size() != 2 * (size_t)p) return false;
+  for (int i = 0; i < p; ++i)
+    if (k[i] != (uint64_t)(uintptr_t)x[i] ||
+        k[p + i] != (uint64_t)(uintptr_t)y[i])
+      return false;
+  return true;
+}
+
+bool alias_cached(const void* const* x, void* const* y, int p, size_t bytes) {
+  for (const AliasOk& a : g_alias_ok)
+    if (a.bytes == bytes && same_key(a.key, x, y, p)) return true;
+  return false;
+}
+
+void alias_remember(const void* const* x, void* const* y, int p,
+                    size_t bytes) {
+  AliasOk a;
+  a.bytes = bytes;
+  a.key.resize(2 * (size_t)p);
+  for (int i = 0; i < p; ++i) {
+    a.key[i] = (uint64_t)(uintptr_t)x[i];
+    a.key[p + i] = (uint64_t)(uintptr_t)y[i];
+  }
+  g_alias_ok.insert(g_alias_ok.begin(), std::move(a));
+  if (g_alias_ok.size() > 8) g_alias_ok.pop_back();
+}
+
+// A staging slot that already holds exactly these pointer arrays, if any.
+bool find_staged(DeviceState* st, const void* const* x, void* const* y, int p,
+                 StageSlot** out) {
+  for (auto& s : st->stage) {
+    if (s.dev && same_key(s.key, x, y, p)) {
+      s.last_use = ++st->tick;
+      *out = &s;
+      return true;
+    }
+  }
+  return false;
+}
+
+// Copies the two pointer arrays into the least recently used staging slot
+// (callers look for a slot holding the same arrays first).
 int stage_pointers(DeviceState* st, const void* const* x, void* const* y,
                    int p, hipStream_t stream, StageSlot** used) {
   std::vector<uint64_t> key(2 * (size_t)p);
@@ -142,13 +216,6 @@ int stage_pointers(DeviceState* st, const void* const* x, void* const* y,
     key[p + i] = (uint64_t)(uintptr_t)y[i];
   }
   ++st->tick;
-  for (auto& s : st->stage) {
-    if (s.dev && s.key == key) {
-      s.last_use = st->tick;
-      *used = &s;
-      return DPAR_SUCCESS;
-    }
-  }
   StageSlot* s = &st->stage[0];
   for (auto& c : st->stage)
     if (c.last_use < s->last_use) s = &c;
@@ -339,7 +406,7 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
   if (!valid_pair(dtype, op))
     return fail(DPAR_ERR_UNSUPPORTED, "unsupported dtype/op pair (%d, %d)",
                 (int)dtype, (int)op);
-  if (exec < DPAR_EXEC_AUTO || exec > DPAR_EXEC_TICKET_SPLIT)
+  if (exec < DPAR_EXEC_AUTO || exec > DPAR_EXEC_SPLIT)
     return fail(DPAR_ERR_INVALID_ARG, "unknown executor %d", (int)exec);
   bool aligned16 = true;
   for (int i = 0; i < p; ++i) {
@@ -360,9 +427,6 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
   const size_t esz = elem_size(dtype);
   if (m > (size_t)1 << 40)
     return fail(DPAR_ERR_UNSUPPORTED, "m beyond 2^40 elements");
-  if (!aliasing_ok(x, y, p, m * esz))
-    return fail(DPAR_ERR_ALIAS, "output buffers overlap each other or "
-                                "partially overlap an input");
 
   dpar::Schedule s;
   dpar::Path path;
@@ -373,6 +437,14 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
     return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items");
 
   std::lock_guard<std::mutex> lock(g_mu);
+  // aliasing rules: checked before any device work; a pointer set that
+  // passed for this row length is not sorted again
+  if (!alias_cached(x, y, p, m * esz)) {
+    if (!aliasing_ok(x, y, p, m * esz))
+      return fail(DPAR_ERR_ALIAS, "output buffers overlap each other or "
+                                  "partially overlap an input");
+    alias_remember(x, y, p, m * esz);
+  }
   DeviceState* st = nullptr;
   int rc = get_state(&st);
   if (rc) return rc;
@@ -389,11 +461,16 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
     return fail(DPAR_ERR_UNSUPPORTED, "tree too deep for the LDS slots");
 
   StageSlot* slot = nullptr;
-  rc = stage_pointers(st, x, y, p, stream, &slot);
-  if (rc) return rc;
+  if (!find_staged(st, x, y, p, &slot)) {
+    rc = stage_pointers(st, x, y, p, stream, &slot);
+    if (rc) return rc;
+  }
 
   const unsigned cslot = st->next_counter++ % kCounterSlots;
-  unsigned* line = st->counters + (size_t)cslot * kCounterStride;
+  unsigned* slot_base =
+      st->counters + (size_t)cslot * kLinesPerSlot * kCounterStride;
+  unsigned* line =
+      slot_base + (size_t)2 * dpar::kTicketCounters * kCounterStride;
   dpar::Params prm{};
   prm.p = p;
   prm.n_a = ops->n_a;
@@ -405,23 +482,93 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
   prm.qbase = 0;
   prm.b = s.b;
   prm.C = s.C;
-  prm.ticket = line + 0;
-  prm.done = line + 1;
-  prm.bar_count = line + 2;
-  prm.bar_gen = line + 3;
-  prm.err = st->counters + (size_t)kCounterSlots * kCounterStride;
+  // short work items (few ranks) are claimed several at a time, so that the
+  // ticket counter is not the bottleneck; at most 1/2 of a fair share
+  {
+    const uint64_t units = s.units();
+    uint64_t k = (512 + (uint64_t)p - 1) / (uint64_t)p;
+    const uint64_t fair = units / (2ull * 4 * (uint64_t)st->num_cus);
+    if (k > fair) k = fair;
+    if (k < 1) k = 1;
+    prm.batch = (unsigned)env_int("DPAR_TICKET_BATCH", (int)k);
+    if (prm.batch < 1) prm.batch = 1;
+  }
+  prm.ticket = slot_base;
+  prm.done = slot_base + (size_t)dpar::kTicketCounters * kCounterStride;
+  prm.bar_count = line + 0;
+  prm.bar_gen = line + 1;
+  prm.err = st->counters + (size_t)kCounterSlots * kLinesPerSlot *
+                               kCounterStride;
   prm.spin_limit = spin_limit();
 
   dpar::Tables tab;
   tab.xp = slot->dev;
   tab.yp = slot->dev + p;
   tab.ops = ops->dev;
+  tab.lvl = ops->lvl;
 
   dpar::Exec ex = (dpar::Exec)exec;
-  if (exec == DPAR_EXEC_AUTO)
-    ex = p >= 2 ? dpar::Exec::TICKET_SPLIT : dpar::Exec::TICKET;
-  if (ex == dpar::Exec::TICKET_SPLIT && p < 2) ex = dpar::Exec::TICKET;
-  hipError_t e = dpar::launch(kind, path, waves, ex, tab, prm, stream,
+  if (exec == DPAR_EXEC_AUTO) ex = dpar::Exec::SPLIT;
+  if (ex == dpar::Exec::SPLIT && p < 2) ex = dpar::Exec::DISPATCH;
+
+  // Work-item evaluation: a post-order walk per wavefront (SEQ) unless the
+  // chunks of a round (launch per round, grid barrier) or of the whole call
+  // (ticket) are too few to keep the CUs busy, in which case each chunk is
+  // staged in LDS and evaluated level by level (LEVEL), if it fits.
+  dpar::Unit unit = dpar::Unit::SEQ;
+  int lv_log2t = 0;
+  int lv_C = 1;
+  prm.nlev = ops->height + 1;
+  if (ops->lvl) {
+    int tmax = -1;
+    for (int lg = 6; lg >= 0; --lg) {
+      if (dpar::level_lds_bytes(path, kind, p, lg, prm.nlev) <=
+          (size_t)st->lds_limit) {
+        tmax = lg;
+        break;
+      }
+    }
+    // measured crossover: per round (launch per round) level items win below
+    // ~2 chunks per CU; over a whole ticketed call below ~1/2 chunk per CU
+    const bool per_round = ex == dpar::Exec::LAUNCH_PER_ROUND ||
+                           ex == dpar::Exec::GRID_BARRIER;
+    bool want = per_round ? (uint64_t)s.C < 2ull * (uint64_t)st->num_cus
+                          : s.units() < (uint64_t)st->num_cus / 2;
+    const char* u = std::getenv("DPAR_UNIT");
+    if (u && !std::strcmp(u, "seq")) want = false;
+    if (u && !std::strcmp(u, "level")) want = true;
+    // The grid-barrier executor keeps the post-order unit: with 1024-thread
+    // level work items its co-resident grid stalled in a barrier wait (seen
+    // once, at two workgroups per CU; the watchdog ended it) for a reason not
+    // yet established, so that combination stays switched off.
+    if (ex == dpar::Exec::GRID_BARRIER) want = false;
+    if (want && tmax >= 0) {
+      // largest block in quanta; chunk capacity T = a power of two
+      const uint64_t maxq = ((s.NL + s.b - 1) / s.b) * (uint64_t)s.lq;
+      int lg = 0;
+      while (lg < tmax && (1ull << lg) < maxq) ++lg;
+      lv_log2t = lg;
+      lv_C = (int)((maxq + (1ull << lg) - 1) >> lg);
+      unit = dpar::Unit::LEVEL;
+    }
+  }
+  if (unit == dpar::Unit::LEVEL) {
+    prm.C = lv_C;
+    prm.lv_log2t = lv_log2t;
+    prm.batch = 1;
+    if ((uint64_t)prm.b * (uint64_t)prm.C >= (1ull << 31))
+      return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items");
+  }
+
+  // the up-phase of the split executor: one workgroup per work item handed
+  // out by the hardware in round order (persistent ticketed workgroups on
+  // request, for comparison)
+  dpar::Exec up = ex;
+  if (ex == dpar::Exec::SPLIT) {
+    const char* v = std::getenv("DPAR_SPLIT_UP");
+    if (v && !std::strcmp(v, "ticket")) up = dpar::Exec::TICKET_SPLIT;
+  }
+  hipError_t e = dpar::launch(kind, path, unit, waves, up, tab, prm, stream,
                               st->num_cus);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   if (s.tail > 0) {
@@ -434,12 +581,13 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
     tp.qbase = s.Q * (uint64_t)s.g;
     tp.b = 1;
     tp.C = 1;
-    e = dpar::launch(kind, dpar::Path::SCALAR, waves,
+    tp.batch = 1;
+    e = dpar::launch(kind, dpar::Path::SCALAR, dpar::Unit::SEQ, waves,
                      dpar::Exec::LAUNCH_PER_ROUND, tab, tp, stream,
                      st->num_cus);
     if (e != hipSuccess) return hip_fail(e, "tail launch");
   }
-  if (ex == dpar::Exec::TICKET_SPLIT) {
+  if (ex == dpar::Exec::SPLIT) {
     if (g_phase_event) {
       e = hipEventRecord(g_phase_event, stream);
       g_phase_event = nullptr;
@@ -448,7 +596,7 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
     // y_0 now holds y for the whole chunked part; stream it to y_1..y_{p-1}
     const uint64_t main_bytes = s.Q * (uint64_t)s.g * esz;
     e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16, stream,
-                        st->num_cus, env_int("DPAR_BCAST_QPT", 8),
+                        st->num_cus, env_int("DPAR_BCAST_QPT", 0),
                         env_int("DPAR_BCAST_ROWS", 0));
     if (e != hipSuccess) return hip_fail(e, "broadcast launch");
   }
@@ -472,13 +620,15 @@ int dpar_check_status(hipStream_t stream) {
   DeviceState* st = nullptr;
   int rc = get_state(&st);
   if (rc) return rc;
-  unsigned* errw = st->counters + (size_t)kCounterSlots * kCounterStride;
+  unsigned* errw = st->counters + (size_t)kCounterSlots * kLinesPerSlot *
+                                      kCounterStride;
   unsigned flag = 0;
   e = hipMemcpy(&flag, errw, sizeof flag, hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
   if (flag) {
     // a barrier gave up: clear the flag and every barrier counter
-    const size_t words = (size_t)(kCounterSlots + 1) * kCounterStride;
+    const size_t words =
+        ((size_t)kCounterSlots * kLinesPerSlot + 1) * kCounterStride;
     e = hipMemset(st->counters, 0, words * sizeof(unsigned));
     if (e != hipSuccess) return hip_fail(e, "hipMemset");
     return fail(DPAR_ERR_TIMEOUT, "a grid-barrier wait exceeded its spin "
@@ -497,7 +647,10 @@ int dpar_finalize(void) {
     DeviceState* st = kv.second.get();
     (void)hipSetDevice(st->device);
     (void)hipDeviceSynchronize();
-    for (auto& o : st->ops) (void)hipFree(o.second.dev);
+    for (auto& o : st->ops) {
+      (void)hipFree(o.second.dev);
+      if (o.second.lvl) (void)hipFree(o.second.lvl);
+    }
     for (auto& s : st->stage) {
       if (s.ev) (void)hipEventDestroy(s.ev);
       if (s.host) (void)hipHostFree(s.host);
@@ -506,6 +659,7 @@ int dpar_finalize(void) {
     if (st->counters) (void)hipFree(st->counters);
   }
   g_devices.clear();
+  g_alias_ok.clear();
   if (prev >= 0) (void)hipSetDevice(prev);
   return DPAR_SUCCESS;
 }

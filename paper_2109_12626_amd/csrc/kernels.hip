@@ -21,6 +21,8 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <map>
+#include <utility>
 
 #include "kernels.hpp"
 #include "plan.hpp"
@@ -285,16 +287,178 @@ __device__ __forceinline__ void run_unit(const uint64_t* __restrict__ xp,
   if (W == 2) __syncthreads();  // slots are reused by the next work item
 }
 
+// ------------------------------------------------------------ level units
+// Level-synchronous work item, for chunks too small to keep a GPU busy with
+// one post-order walk per chunk.  1024 threads load every rank's quanta of a
+// chunk of at most T quanta into LDS at once, then evaluate the two trees one
+// depth level at a time from the deepest up: every (node, quantum) pair of a
+// level computes S(i) = S(child1) (.) (S(child0) (.) x_i) from children
+// finished in the previous level, then a barrier.  Same association as the
+// post-order walk; the dependent chain is H + 1 levels instead of p loads.
+//
+// LDS: S [p][T] lane values | Y [T] | ptr [p] row addresses | lvl [p]
+// level-ordered entries | off [H + 2] level boundaries.
+constexpr int kLvThreads = 1024;
+constexpr int kLvBatch = 8;  // loads in flight per thread
+
+__host__ __device__ inline size_t align16(size_t v) { return (v + 15) & ~(size_t)15; }
+
+template <class L>
+struct LvLayout {
+  size_t s, y, ptr, lvl, off, total;
+  __host__ __device__ LvLayout(int p, int T, int nlev) {
+    s = 0;
+    y = align16(s + (size_t)p * T * sizeof(typename L::T));
+    ptr = align16(y + (size_t)T * sizeof(typename L::T));
+    lvl = align16(ptr + (size_t)p * 8);
+    off = align16(lvl + (size_t)p * 4);
+    total = align16(off + (size_t)(nlev + 1) * 4);
+  }
+};
+
+template <class L, bool FUSED>
+__device__ __forceinline__ void run_unit_lv(const uint64_t* __restrict__ xp,
+                                            const uint64_t* __restrict__ yp,
+                                            const uint32_t* __restrict__ lvl_g,
+                                            const Params& prm, uint64_t t,
+                                            char* lds) {
+  using T = typename L::T;
+  const int tid = threadIdx.x;
+  const int p = prm.p, sh = prm.lv_log2t, TQ = 1 << sh, nlev = prm.nlev;
+  const LvLayout<L> lay(p, TQ, nlev);
+  T* S = reinterpret_cast<T*>(lds + lay.s);
+  T* Y = reinterpret_cast<T*>(lds + lay.y);
+  uint64_t* ptr = reinterpret_cast<uint64_t*>(lds + lay.ptr);
+  uint32_t* lvl = reinterpret_cast<uint32_t*>(lds + lay.lvl);
+  uint32_t* off = reinterpret_cast<uint32_t*>(lds + lay.off);
+
+  // chunk -> quanta [cs, ce): block j is cut at lines, the chunk at quanta
+  const uint64_t j = t / (uint64_t)prm.C, c = t % (uint64_t)prm.C;
+  const uint64_t ls = prm.NL * j / (uint64_t)prm.b;
+  const uint64_t le = prm.NL * (j + 1) / (uint64_t)prm.b;
+  const uint64_t qs = min(ls * prm.lq, prm.Q);
+  const uint64_t qe = min(le * prm.lq, prm.Q);
+  const uint64_t n = qe - qs;
+  const uint64_t cs = qs + c * n / (uint64_t)prm.C;
+  const uint64_t ce = qs + (c + 1) * n / (uint64_t)prm.C;
+  const int count = (int)(ce - cs);
+  if (count == 0) return;  // uniform
+  const uint64_t unit_off = (prm.qbase + cs) * (uint64_t)L::bytes;
+
+  for (int i = tid; i < p; i += kLvThreads) {
+    ptr[i] = xp[i] + unit_off;
+    lvl[i] = lvl_g[i];
+  }
+  for (int i = tid; i <= nlev; i += kLvThreads) off[i] = lvl_g[p + i];
+  __syncthreads();
+
+  // all loads of the chunk, kLvBatch per thread in flight
+  const int total = p << sh;
+  for (int base = 0; base < total; base += kLvThreads * kLvBatch) {
+    T v[kLvBatch];
+#pragma unroll
+    for (int k = 0; k < kLvBatch; ++k) {
+      const int idx = base + k * kLvThreads + tid;
+      const bool ok = idx < total && (idx & (TQ - 1)) < count;
+      // items past the chunk re-read quantum 0 of rank 0 (always in range)
+      const int i = ok ? (idx >> sh) : 0;
+      const uint32_t q = ok ? (uint32_t)(idx & (TQ - 1)) : 0u;
+      v[k] = L::load(ptr[i], q * L::bytes);
+    }
+#pragma unroll
+    for (int k = 0; k < kLvBatch; ++k) {
+      const int idx = base + k * kLvThreads + tid;
+      if (idx < total && (idx & (TQ - 1)) < count) S[idx] = v[k];
+    }
+  }
+  __syncthreads();
+
+  // levels, deepest first; entry = node << 16 | code, code 0xFFFF: leaf,
+  // 0xFFFE: first child only (node - 1), else the second child's rank
+  for (int lv = 0; lv < nlev; ++lv) {
+    const int o0 = (int)off[lv];
+    const int items = ((int)off[lv + 1] - o0) << sh;
+    for (int idx = tid; idx < items; idx += kLvThreads) {
+      const int q = idx & (TQ - 1);
+      if (q >= count) continue;
+      const uint32_t e = lvl[o0 + (idx >> sh)];
+      const int node = (int)(e >> 16);
+      const uint32_t code = e & 0xFFFFu;
+      T v = S[(node << sh) + q];
+      if (code != 0xFFFFu) v = L::ap(S[((node - 1) << sh) + q], v);
+      if (code < 0xFFFEu) v = L::ap(S[((int)code << sh) + q], v);
+      S[(node << sh) + q] = v;
+    }
+    __syncthreads();
+  }
+
+  // dual-root step, then the write-out
+  if (tid < count) {
+    const int ra = prm.n_a - 1;
+    Y[tid] = prm.dual ? L::ap(S[(ra << sh) + tid], S[((p - 1) << sh) + tid])
+                      : S[(ra << sh) + tid];
+  }
+  if (FUSED)
+    for (int i = tid; i < p; i += kLvThreads) ptr[i] = yp[i] + unit_off;
+  __syncthreads();
+  if (FUSED) {
+    for (int idx = tid; idx < total; idx += kLvThreads) {
+      const int q = idx & (TQ - 1);
+      if (q < count) L::store(ptr[idx >> sh], (uint32_t)q * L::bytes, Y[q]);
+    }
+  } else if (tid < count) {
+    L::store(yp[0] + unit_off, (uint32_t)tid * L::bytes, Y[tid]);
+  }
+  __syncthreads();  // LDS is reused by the next work item
+}
+
+// ------------------------------------------------------------ unit policies
+
+template <class L, int W, bool FUSED>
+struct SeqUnit {
+  static constexpr int kThreads = 64 * W;
+  __device__ static void run(const uint64_t* __restrict__ xp,
+                             const uint64_t* __restrict__ yp,
+                             const uint32_t* __restrict__ ops,
+                             const uint32_t* __restrict__ lvl,
+                             const Params& prm, uint64_t t, char* lds) {
+    (void)lvl;
+    run_unit<L, W, FUSED>(xp, yp, ops, prm, t,
+                          reinterpret_cast<typename L::T*>(lds));
+  }
+  static size_t lds(const Params& prm) {
+    return (size_t)W * prm.nslots * 64 * sizeof(typename L::T);
+  }
+};
+
+template <class L, bool FUSED>
+struct LvUnit {
+  static constexpr int kThreads = kLvThreads;
+  __device__ static void run(const uint64_t* __restrict__ xp,
+                             const uint64_t* __restrict__ yp,
+                             const uint32_t* __restrict__ ops,
+                             const uint32_t* __restrict__ lvl,
+                             const Params& prm, uint64_t t, char* lds) {
+    (void)ops;
+    run_unit_lv<L, FUSED>(xp, yp, lvl, prm, t, lds);
+  }
+  static size_t lds(const Params& prm) {
+    return LvLayout<L>(prm.p, 1 << prm.lv_log2t, prm.nlev).total;
+  }
+};
+
 // ------------------------------------------------------------ executors
 
-template <class L, int W>
-__global__ __launch_bounds__(64 * W) void k_round(
-    const uint64_t* __restrict__ xp, const uint64_t* __restrict__ yp,
-    const uint32_t* __restrict__ ops, Params prm, int round) {
+#define DPAR_KARGS                                                     \
+  const uint64_t *__restrict__ xp, const uint64_t *__restrict__ yp,   \
+      const uint32_t *__restrict__ ops, const uint32_t *__restrict__ lvl, \
+      Params prm
+
+template <class U>
+__global__ __launch_bounds__(U::kThreads) void k_round(DPAR_KARGS, int round) {
   extern __shared__ char lds_raw[];
-  typename L::T* slots = reinterpret_cast<typename L::T*>(lds_raw);
-  run_unit<L, W, true>(xp, yp, ops, prm,
-                       (uint64_t)round * prm.C + blockIdx.x, slots);
+  U::run(xp, yp, ops, lvl, prm, (uint64_t)round * prm.C + blockIdx.x,
+         lds_raw);
 }
 
 __device__ inline void grid_barrier(const Params& prm) {
@@ -327,40 +491,54 @@ __device__ inline void grid_barrier(const Params& prm) {
   __syncthreads();
 }
 
-template <class L, int W>
-__global__ __launch_bounds__(64 * W) void k_barrier(
-    const uint64_t* __restrict__ xp, const uint64_t* __restrict__ yp,
-    const uint32_t* __restrict__ ops, Params prm) {
+template <class U>
+__global__ __launch_bounds__(U::kThreads) void k_barrier(DPAR_KARGS) {
   extern __shared__ char lds_raw[];
-  typename L::T* slots = reinterpret_cast<typename L::T*>(lds_raw);
   for (int j = 0; j < prm.b; ++j) {
     for (uint64_t c = blockIdx.x; c < (uint64_t)prm.C; c += gridDim.x)
-      run_unit<L, W, true>(xp, yp, ops, prm, (uint64_t)j * prm.C + c, slots);
+      U::run(xp, yp, ops, lvl, prm, (uint64_t)j * prm.C + c, lds_raw);
     if (j + 1 < prm.b) grid_barrier(prm);
   }
 }
 
-template <class L, int W, bool FUSED>
-__global__ __launch_bounds__(64 * W) void k_ticket(
-    const uint64_t* __restrict__ xp, const uint64_t* __restrict__ yp,
-    const uint32_t* __restrict__ ops, Params prm) {
+template <class U>
+__global__ __launch_bounds__(U::kThreads) void k_ticket(DPAR_KARGS) {
   extern __shared__ char lds_raw[];
-  typename L::T* slots = reinterpret_cast<typename L::T*>(lds_raw);
   __shared__ unsigned s_ticket;
   const uint64_t nunits = (uint64_t)prm.b * prm.C;
+  const uint64_t K = prm.batch;
+  // Batch k (work items [k K, k K + K)) belongs to counter k % NC.  A
+  // workgroup serves one counter: its first batch is its own index, later
+  // ones come from that counter in increasing order, so every counter hands
+  // out its batches in round order and the atomics are spread NC ways.
+  const unsigned NC = min((unsigned)kTicketCounters, gridDim.x);
+  const unsigned c = blockIdx.x % NC;
+  const unsigned served = (gridDim.x - c + NC - 1) / NC;  // WGs on counter c
+  unsigned* ctr = prm.ticket + (size_t)c * kCounterStride;
+  uint64_t batch = blockIdx.x;
+  // the next batch is claimed before the current one is processed, so the
+  // atomic's round trip overlaps the work
+  unsigned next = 0;
+  if (threadIdx.x == 0 && batch * K < nunits) next = atomicAdd(ctr, 1u);
   for (;;) {
-    if (threadIdx.x == 0) s_ticket = atomicAdd(prm.ticket, 1u);
+    const uint64_t first = batch * K;
+    if (first >= nunits) break;
+    const uint64_t last = min(first + K, nunits);
+    for (uint64_t t = first; t < last; ++t)
+      U::run(xp, yp, ops, lvl, prm, t, lds_raw);
+    if (threadIdx.x == 0) s_ticket = next;
     __syncthreads();
-    const unsigned t = s_ticket;
+    batch = ((uint64_t)served + s_ticket) * NC + c;
     __syncthreads();
-    if (t >= nunits) break;
-    run_unit<L, W, FUSED>(xp, yp, ops, prm, t, slots);
+    if (threadIdx.x == 0 && batch * K < nunits) next = atomicAdd(ctr, 1u);
   }
+  // the last workgroup of each counter resets it for the next call
   if (threadIdx.x == 0) {
+    unsigned* dn = prm.done + (size_t)c * kCounterStride;
     __threadfence();
-    if (atomicAdd(prm.done, 1u) == gridDim.x - 1) {
-      atomicExch(prm.ticket, 0u);
-      atomicExch(prm.done, 0u);
+    if (atomicAdd(dn, 1u) == served - 1) {
+      atomicExch(ctr, 0u);
+      atomicExch(dn, 0u);
     }
   }
 }
@@ -431,84 +609,120 @@ __global__ __launch_bounds__(256) void k_bcast(const uint64_t* __restrict__ yp,
 
 namespace {
 
-template <class L, int W>
-hipError_t launch_t(Exec exec, const Tables& tab, const Params& prm,
+// Workgroups per CU for (kernel, LDS bytes), cached: the query costs more than
+// a launch.  Callers hold the library lock.
+hipError_t occupancy(const void* kfn, int threads, size_t lds, int* out) {
+  static std::map<std::pair<const void*, size_t>, int> cache;
+  const auto key = std::make_pair(kfn, lds);
+  auto it = cache.find(key);
+  if (it != cache.end()) {
+    *out = it->second;
+    return hipSuccess;
+  }
+  hipError_t e =
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(out, kfn, threads, lds);
+  if (e == hipSuccess) cache[key] = *out;
+  return e;
+}
+
+template <class U>
+hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
                     hipStream_t stream, int num_cus) {
-  const size_t lds = (size_t)W * prm.nslots * 64 * sizeof(typename L::T);
-  const dim3 block(64 * W);
+  const size_t lds = U::lds(prm);
+  const dim3 block(U::kThreads);
   const uint64_t nunits = (uint64_t)prm.b * prm.C;
-  if (exec == Exec::LAUNCH_PER_ROUND) {
-    for (int j = 0; j < prm.b; ++j) {
-      hipLaunchKernelGGL((k_round<L, W>), dim3(prm.C), block, lds, stream,
-                         tab.xp, tab.yp, tab.ops, prm, j);
-    }
+  if (exec == Exec::DISPATCH) {  // work item t = blockIdx.x, all rounds
+    hipLaunchKernelGGL((k_round<U>), dim3((unsigned)nunits), block, lds,
+                       stream, tab.xp, tab.yp, tab.ops, tab.lvl, prm, 0);
     return hipGetLastError();
   }
+  if (exec == Exec::LAUNCH_PER_ROUND) {
+    for (int j = 0; j < prm.b; ++j)
+      hipLaunchKernelGGL((k_round<U>), dim3(prm.C), block, lds, stream,
+                         tab.xp, tab.yp, tab.ops, tab.lvl, prm, j);
+    return hipGetLastError();
+  }
+  const void* kfn = exec == Exec::GRID_BARRIER
+                        ? reinterpret_cast<const void*>(&k_barrier<U>)
+                        : reinterpret_cast<const void*>(&k_ticket<U>);
+  int per_cu = 0;
+  hipError_t e = occupancy(kfn, U::kThreads, lds, &per_cu);
+  if (e != hipSuccess) return e;
   if (exec == Exec::GRID_BARRIER) {
-    int per_cu = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        &per_cu, reinterpret_cast<const void*>(&k_barrier<L, W>), 64 * W, lds);
-    if (e != hipSuccess) return e;
     if (per_cu < 1) return hipErrorInvalidConfiguration;
+    // every workgroup must be resident at once; leave one slot per CU free
+    // rather than fill the machine to the last slot
+    if (per_cu > 1) --per_cu;
     uint64_t grid = (uint64_t)per_cu * num_cus;
     if (grid > (uint64_t)prm.C) grid = prm.C;  // more would only wait
     const uint64_t* xp = tab.xp;
     const uint64_t* yp = tab.yp;
     const uint32_t* ops = tab.ops;
+    const uint32_t* lvl = tab.lvl;
     Params p2 = prm;
-    void* args[] = {&xp, &yp, &ops, &p2};
-    return hipLaunchCooperativeKernel(
-        reinterpret_cast<const void*>(&k_barrier<L, W>), dim3((unsigned)grid),
-        block, args, (unsigned)lds, stream);
+    void* args[] = {&xp, &yp, &ops, &lvl, &p2};
+    return hipLaunchCooperativeKernel(kfn, dim3((unsigned)grid), block, args,
+                                      (unsigned)lds, stream);
   }
-  const bool fused = exec == Exec::TICKET;
-  const void* kfn = fused
-      ? reinterpret_cast<const void*>(&k_ticket<L, W, true>)
-      : reinterpret_cast<const void*>(&k_ticket<L, W, false>);
-  int per_cu = 0;
-  hipError_t e =
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kfn, 64 * W, lds);
-  if (e != hipSuccess) return e;
   if (per_cu < 1) per_cu = 1;
   uint64_t grid = (uint64_t)per_cu * num_cus;
-  if (grid > nunits) grid = nunits;
-  if (fused)
-    hipLaunchKernelGGL((k_ticket<L, W, true>), dim3((unsigned)grid), block,
-                       lds, stream, tab.xp, tab.yp, tab.ops, prm);
-  else
-    hipLaunchKernelGGL((k_ticket<L, W, false>), dim3((unsigned)grid), block,
-                       lds, stream, tab.xp, tab.yp, tab.ops, prm);
+  const uint64_t batches = (nunits + prm.batch - 1) / prm.batch;
+  if (grid > batches) grid = batches;
+  hipLaunchKernelGGL((k_ticket<U>), dim3((unsigned)grid), block, lds, stream,
+                     tab.xp, tab.yp, tab.ops, tab.lvl, prm);
   return hipGetLastError();
 }
 
 template <class L>
-hipError_t launch_w(int waves, Exec exec, const Tables& tab,
+hipError_t launch_l(Unit unit, int waves, Exec exec, const Tables& tab,
                     const Params& prm, hipStream_t stream, int num_cus) {
-  return waves == 2 ? launch_t<L, 2>(exec, tab, prm, stream, num_cus)
-                    : launch_t<L, 1>(exec, tab, prm, stream, num_cus);
+  const bool fused = exec != Exec::TICKET_SPLIT && exec != Exec::SPLIT;
+  const Exec ex = exec == Exec::TICKET_SPLIT ? Exec::TICKET
+                  : exec == Exec::SPLIT      ? Exec::DISPATCH
+                                             : exec;
+  if (unit == Unit::LEVEL)
+    return fused ? launch_u<LvUnit<L, true>>(ex, tab, prm, stream, num_cus)
+                 : launch_u<LvUnit<L, false>>(ex, tab, prm, stream, num_cus);
+  if (waves == 2)
+    return fused
+               ? launch_u<SeqUnit<L, 2, true>>(ex, tab, prm, stream, num_cus)
+               : launch_u<SeqUnit<L, 2, false>>(ex, tab, prm, stream, num_cus);
+  return fused ? launch_u<SeqUnit<L, 1, true>>(ex, tab, prm, stream, num_cus)
+               : launch_u<SeqUnit<L, 1, false>>(ex, tab, prm, stream, num_cus);
 }
 
 }  // namespace
 
-hipError_t launch(Kind kind, Path path, int waves, Exec exec,
+hipError_t launch(Kind kind, Path path, Unit unit, int waves, Exec exec,
                   const Tables& tab, const Params& prm, hipStream_t stream,
                   int num_cus) {
   const bool vec = path == Path::VEC16;
   switch (kind) {
     case Kind::I32_SUM:
-      return vec ? launch_w<Lane4<I32Sum>>(waves, exec, tab, prm, stream, num_cus)
-                 : launch_w<Lane1<I32Sum>>(waves, exec, tab, prm, stream, num_cus);
+      return vec ? launch_l<Lane4<I32Sum>>(unit, waves, exec, tab, prm, stream, num_cus)
+                 : launch_l<Lane1<I32Sum>>(unit, waves, exec, tab, prm, stream, num_cus);
     case Kind::I32_MAX:
-      return vec ? launch_w<Lane4<I32Max>>(waves, exec, tab, prm, stream, num_cus)
-                 : launch_w<Lane1<I32Max>>(waves, exec, tab, prm, stream, num_cus);
+      return vec ? launch_l<Lane4<I32Max>>(unit, waves, exec, tab, prm, stream, num_cus)
+                 : launch_l<Lane1<I32Max>>(unit, waves, exec, tab, prm, stream, num_cus);
     case Kind::F32_SUM:
-      return vec ? launch_w<Lane4<F32Sum>>(waves, exec, tab, prm, stream, num_cus)
-                 : launch_w<Lane1<F32Sum>>(waves, exec, tab, prm, stream, num_cus);
+      return vec ? launch_l<Lane4<F32Sum>>(unit, waves, exec, tab, prm, stream, num_cus)
+                 : launch_l<Lane1<F32Sum>>(unit, waves, exec, tab, prm, stream, num_cus);
     case Kind::MAT:
-      return vec ? launch_w<LaneMat16>(waves, exec, tab, prm, stream, num_cus)
-                 : launch_w<LaneMat4>(waves, exec, tab, prm, stream, num_cus);
+      return vec ? launch_l<LaneMat16>(unit, waves, exec, tab, prm, stream, num_cus)
+                 : launch_l<LaneMat4>(unit, waves, exec, tab, prm, stream, num_cus);
   }
   return hipErrorInvalidValue;
+}
+
+size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev) {
+  const size_t lane = (path == Path::VEC16 || kind == Kind::MAT) ? 16 : 4;
+  const size_t T = (size_t)1 << log2t;
+  const size_t s = 0;
+  const size_t y = align16(s + (size_t)p * T * lane);
+  const size_t ptr = align16(y + T * lane);
+  const size_t lvl = align16(ptr + (size_t)p * 8);
+  const size_t off = align16(lvl + (size_t)p * 4);
+  return align16(off + (size_t)(nlev + 1) * 4);
 }
 
 hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
@@ -516,9 +730,21 @@ hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
   if (p < 2 || nbytes == 0) return hipSuccess;
   const uint64_t lane = vec16 ? 16 : 4;
   const uint64_t n = nbytes / lane;
+  // Default shape: 32 KB per row visit over all ranks, narrowed (fewer
+  // bytes per visit, then row groups) until there are >= 2 workgroups per CU.
+  const uint64_t want = 2ull * (uint64_t)num_cus;
+  const bool auto_shape = qpt <= 0;
+  if (auto_shape) qpt = 8;
   if (qpt != 1 && qpt != 2 && qpt != 4 && qpt != 8 && qpt != 16) qpt = 8;
   if (rows < 1) rows = p - 1;
-  const uint64_t tiles = (n + 256ull * qpt - 1) / (256ull * qpt);
+  auto tiles_of = [&](int q) { return (n + 256ull * q - 1) / (256ull * q); };
+  if (auto_shape) {
+    while (qpt > 1 && tiles_of(qpt) < want) qpt /= 2;
+    while (rows > 1 && tiles_of(qpt) * (uint64_t)((p - 1 + rows - 1) / rows) <
+                           want)
+      rows = (rows + 1) / 2;
+  }
+  const uint64_t tiles = tiles_of(qpt);
   const uint64_t groups = (uint64_t)(p - 1 + rows - 1) / rows;
   uint64_t grid = tiles * groups;
   const uint64_t cap = (uint64_t)num_cus * 64;  // grid-stride beyond this

@@ -12,11 +12,19 @@ enum class Kind : int { I32_SUM = 0, I32_MAX = 1, F32_SUM = 2, MAT = 3 };
 // VEC16: 16-byte lanes (4 scalars or 1 matrix) on 16-byte aligned buffers.
 // SCALAR: one 4-byte scalar (or one matrix read as 4 dwords) per lane.
 enum class Path : int { VEC16 = 0, SCALAR = 1 };
+// How one work item (a chunk of a block) is evaluated: a post-order walk per
+// wavefront over 16-byte lanes (SEQ) or level by level with the whole chunk
+// staged in LDS (LEVEL; short chunks, latency-bound cases).
+enum class Unit : int { SEQ = 0, LEVEL = 1 };
 enum class Exec : int {
   LAUNCH_PER_ROUND = 1,
   GRID_BARRIER = 2,
   TICKET = 3,
-  TICKET_SPLIT = 4,  // up-phase of every chunk by ticket, y into y_0 only
+  SPLIT = 4,         // up-phase of every chunk (DISPATCH order), y into y_0
+                     // only, then the broadcast pass
+  DISPATCH = 5,      // one launch, one workgroup per work item in round
+                     // order (the hardware dispatcher hands them out)
+  TICKET_SPLIT = 6,  // as SPLIT with a ticketed up-phase (experiments)
 };
 
 // Scalars every kernel needs.  The tables (device pointers to the x and y
@@ -33,13 +41,23 @@ struct Params {
   uint64_t qbase;   // first quantum index (the tail unit starts after Q)
   int b;            // blocks = rounds
   int C;            // chunks per block
-  unsigned* ticket;     // TICKET: next work item; reset by the last WG out
-  unsigned* done;       // TICKET: WGs finished
+  unsigned batch;   // TICKET: consecutive work items claimed per ticket
+  int lv_log2t;     // LEVEL: log2 of the chunk capacity T in quanta
+  int nlev;         // LEVEL: H + 1 depth levels
+  unsigned* ticket;     // TICKET: kTicketCounters counters, kCounterStride
+                        // words apart; each reset by the last WG it served
+  unsigned* done;       // TICKET: per-counter count of WGs finished, same
+                        // layout as `ticket`
   unsigned* bar_count;  // GRID_BARRIER: arrivals
   unsigned* bar_gen;    // GRID_BARRIER: generation
   unsigned* err;        // bit 0: a barrier wait gave up
   unsigned long long spin_limit;
 };
+
+// Ticket counters per call (each on its own 128-byte line): work-item batch
+// k belongs to counter k % kTicketCounters, which spreads the atomics.
+constexpr int kTicketCounters = 16;
+constexpr int kCounterStride = 32;  // uint32 words = 128 bytes
 
 // Entries the host appends to the pointer and opcode tables so that the
 // kernels may read a fixed number of entries past the last rank.
@@ -49,13 +67,17 @@ struct Tables {
   const uint64_t* xp;   // [p] device addresses of x_i
   const uint64_t* yp;   // [p] device addresses of y_i
   const uint32_t* ops;  // [p] opcodes (plan.hpp)
+  const uint32_t* lvl;  // [p] level-ordered entries, then H + 2 offsets
 };
 
 // Enqueue one executor run over all b*C chunks of a schedule.
 // `waves` is 1 or 2 (2 needs p >= 2).  Returns the first HIP error.
-hipError_t launch(Kind kind, Path path, int waves, Exec exec,
+hipError_t launch(Kind kind, Path path, Unit unit, int waves, Exec exec,
                   const Tables& tab, const Params& prm, hipStream_t stream,
                   int num_cus);
+
+// Bytes of dynamic LDS a LEVEL work item needs.
+size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev);
 
 // Broadcast pass of the split executor: copies bytes [0, nbytes) of y_0 into
 // y_1 .. y_{p-1} (16-byte lanes when vec16, else 4-byte lanes).  A workgroup

@@ -92,6 +92,27 @@ std::vector<uint32_t> make_ops(const Tree& t) {
   return ops;
 }
 
+std::vector<uint32_t> make_levels(const Tree& t) {
+  std::vector<uint32_t> out;
+  out.reserve((size_t)t.p + t.height + 2);
+  std::vector<uint32_t> bounds;
+  for (int d = t.height; d >= 0; --d) {
+    bounds.push_back((uint32_t)out.size());
+    for (int i = 0; i < t.p; ++i) {
+      if (t.depth[i] != d) continue;
+      uint32_t code = 0xFFFFu;
+      if (t.child1[i] >= 0)
+        code = (uint32_t)t.child1[i];
+      else if (t.child0[i] >= 0)
+        code = 0xFFFEu;
+      out.push_back(((uint32_t)i << 16) | code);
+    }
+  }
+  bounds.push_back((uint32_t)out.size());
+  out.insert(out.end(), bounds.begin(), bounds.end());
+  return out;
+}
+
 int rank_rounds(const Tree& t, int b, int rank) {
   if (t.p == 1) return 0;
   if (rank < 0) return b + t.height;

@@ -35,6 +35,13 @@ Tree build_tree(int p);
 // Opcodes for ranks 0..p-1 (uint32 each).
 std::vector<uint32_t> make_ops(const Tree& t);
 
+// Ranks in level order for level-synchronous evaluation: deepest level
+// first, ranks ascending within a level; entry = rank << 16 | code with code
+// 0xFFFF for a leaf, 0xFFFE for a rank whose only child is rank - 1, else the
+// second child's rank (the first is rank - 1).  The p entries are followed by
+// H + 2 level boundaries.  Needs p <= 65534.
+std::vector<uint32_t> make_levels(const Tree& t);
+
 // Rounds with a non-empty exchange for one rank (rank == -1: overall).
 int rank_rounds(const Tree& t, int b, int rank);
 

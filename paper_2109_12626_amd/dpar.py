@@ -25,14 +25,14 @@ DPAR_ERR_TIMEOUT = -6
 DPAR_INT32, DPAR_FLOAT32, DPAR_U32_MAT2X2 = 0, 1, 2
 DPAR_SUM, DPAR_MAX, DPAR_MATMUL = 0, 1, 2
 DPAR_EXEC_AUTO, DPAR_EXEC_LAUNCH_PER_ROUND, DPAR_EXEC_GRID_BARRIER, \
-    DPAR_EXEC_TICKET, DPAR_EXEC_TICKET_SPLIT = 0, 1, 2, 3, 4
+    DPAR_EXEC_TICKET, DPAR_EXEC_SPLIT = 0, 1, 2, 3, 4
 
 DTYPES = {"int32": DPAR_INT32, "float32": DPAR_FLOAT32,
           "u32mat2x2": DPAR_U32_MAT2X2}
 OPS = {"sum": DPAR_SUM, "max": DPAR_MAX, "matmul": DPAR_MATMUL}
 EXECS = {"auto": DPAR_EXEC_AUTO, "launch": DPAR_EXEC_LAUNCH_PER_ROUND,
          "barrier": DPAR_EXEC_GRID_BARRIER, "ticket": DPAR_EXEC_TICKET,
-         "split": DPAR_EXEC_TICKET_SPLIT}
+         "split": DPAR_EXEC_SPLIT}
 
 
 class DparError(RuntimeError):
@@ -104,11 +104,15 @@ def _addr(v):
     return int(v)
 
 
-def _ptr_array(seq):
-    arr = (ctypes.c_void_p * len(seq))()
-    for k, v in enumerate(seq):
-        arr[k] = _addr(v)
-    return arr
+def pointers(seq):
+    """A reusable C array of device addresses (ints or tensors); passing it
+    instead of a list saves the conversion on every call."""
+    if isinstance(seq, ctypes.Array):
+        return seq
+    return (ctypes.c_void_p * len(seq))(*[_addr(v) for v in seq])
+
+
+_ptr_array = pointers
 
 
 def _stream(stream):

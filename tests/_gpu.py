@@ -91,16 +91,31 @@ def gib(nbytes):
     return nbytes / 2 ** 30
 
 
-def env_waves(n):
-    """Context manager: library knob for wavefronts per chunk."""
-    class _Ctx:
-        def __enter__(self):
-            self.old = os.environ.get("DPAR_WAVES")
-            os.environ["DPAR_WAVES"] = str(n)
+class _Env:
+    """Context manager setting one library knob (environment variable)."""
 
-        def __exit__(self, *a):
-            if self.old is None:
-                os.environ.pop("DPAR_WAVES", None)
-            else:
-                os.environ["DPAR_WAVES"] = self.old
-    return _Ctx()
+    def __init__(self, name, value):
+        self.name, self.value = name, value
+
+    def __enter__(self):
+        self.old = os.environ.get(self.name)
+        if self.value is None:
+            os.environ.pop(self.name, None)
+        else:
+            os.environ[self.name] = str(self.value)
+
+    def __exit__(self, *a):
+        if self.old is None:
+            os.environ.pop(self.name, None)
+        else:
+            os.environ[self.name] = self.old
+
+
+def env_waves(n):
+    """Wavefronts per chunk of the post-order (SEQ) work item: 1 or 2."""
+    return _Env("DPAR_WAVES", n)
+
+
+def env_unit(u):
+    """Work-item evaluation: "seq", "level" or None (the library chooses)."""
+    return _Env("DPAR_UNIT", u)

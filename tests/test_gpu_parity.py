@@ -15,13 +15,14 @@ import torch
 import oracle
 import synth
 from synth import configs
-from tests._gpu import (POISON, assert_all_ranks_equal, env_waves, from_dev,
-                        need_gpu, poisoned_like, resolve_b, run, to_dev,
-                        workload_input)
+from tests._gpu import (POISON, assert_all_ranks_equal, env_unit, env_waves,
+                        from_dev, need_gpu, poisoned_like, resolve_b, run,
+                        to_dev, workload_input)
 
 pytestmark = pytest.mark.gpu
 
 EXECS = ["launch", "barrier", "ticket", "split"]
+UNITS = ["seq", "level"]
 
 
 @pytest.fixture(autouse=True)
@@ -37,12 +38,20 @@ def _want(x, dtype, op):
 
 # ------------------------------------------------------------ p = 7, m = 1000
 
+LEVEL_BARRIER_OFF = ("the grid-barrier executor does not use level work items "
+                     "(switched off after a barrier stall at 2 workgroups/CU)")
+
+
+@pytest.mark.parametrize("unit", UNITS)
 @pytest.mark.parametrize("exec", EXECS)
 @pytest.mark.parametrize("b", [4, 1, 2, 7, 249, 250, 251, 1000])
-def test_p7_int32_sum_every_executor_and_b(exec, b):
+def test_p7_int32_sum_every_executor_and_b(exec, b, unit):
+    if unit == "level" and exec == "barrier":
+        pytest.skip(LEVEL_BARRIER_OFF)
     w = configs.P7_SMALL
     x = workload_input(w)
-    out = run(x, "int32", "sum", b, exec)
+    with env_unit(unit):
+        out = run(x, "int32", "sum", b, exec)
     assert_all_ranks_equal(out, _want(x, "int32", "sum"), f"b={b} {exec}")
 
 
@@ -77,13 +86,31 @@ def test_fp32_worked_examples_on_device():
 
 # ------------------------------------------------------------ edge cases
 
+@pytest.mark.parametrize("unit", UNITS)
 @pytest.mark.parametrize("p", [1, 2, 3, 4, 5, 8, 9, 15, 16, 17, 31, 33, 100])
 @pytest.mark.parametrize("m", [1, 3, 4, 5, 64, 255, 256, 257, 1027])
-def test_small_p_and_m(p, m):
+def test_small_p_and_m(p, m, unit):
     x = synth.generate("normal_f32", 100 + p, p, m)
     b = min(m, 3)
-    out = run(x, "float32", "sum", b)
+    with env_unit(unit):
+        out = run(x, "float32", "sum", b)
     assert_all_ranks_equal(out, _want(x, "float32", "sum"), f"p={p} m={m}")
+
+
+@pytest.mark.parametrize("exec", EXECS)
+@pytest.mark.parametrize("dtype,op,dist", [
+    ("int32", "max", "uniform_int"), ("float32", "sum", "normal_f32"),
+    ("u32mat2x2", "matmul", "odd_det_u32_mat")])
+def test_level_unit_all_dtypes_and_executors(exec, dtype, op, dist):
+    if exec == "barrier":
+        pytest.skip(LEVEL_BARRIER_OFF)
+    p, m = 300, 1000
+    kw = {"lo": -99, "hi": 99} if dist == "uniform_int" else {}
+    x = synth.generate(dist, 61, p, m, **kw)
+    for b in (1, 7, 40):
+        with env_unit("level"):
+            out = run(x, dtype, op, b, exec)
+        assert_all_ranks_equal(out, _want(x, dtype, op), f"b={b}")
 
 
 @pytest.mark.parametrize("exec", EXECS)
@@ -227,22 +254,26 @@ def test_p64_matmul_full(dist):
     assert_all_ranks_equal(out, _want(x, "u32mat2x2", "matmul"))
 
 
+@pytest.mark.parametrize("unit", UNITS + [None])
 @pytest.mark.parametrize("k", [4, 10, 16])
 @pytest.mark.parametrize("op", ["max", "sum"])
 @pytest.mark.parametrize("b", [1, "rule"])
-def test_p1152_int32_sweep_full(k, op, b):
+def test_p1152_int32_sweep_full(k, op, b, unit):
     w = next(v for v in configs.P1152_SWEEP if v.m == 1 << k)
     x = workload_input(w)
     bb = resolve_b(b, w.p, w.m)
-    out = run(x, "int32", op, bb)
+    with env_unit(unit):
+        out = run(x, "int32", op, bb)
     assert_all_ranks_equal(out, _want(x, "int32", op), f"m=2^{k} b={bb}")
 
 
-def test_p1152_fp32_reduced_size_every_element():
+@pytest.mark.parametrize("unit", UNITS)
+def test_p1152_fp32_reduced_size_every_element(unit):
     # the headline shape with fewer columns (several chunks and a ragged tail)
     w = configs.P1152_F32
     m = 3 * 4096 + 7
     x = workload_input(w, m=m)
     for exec in EXECS:
-        out = run(x, "float32", "sum", resolve_b("rule", w.p, m), exec)
+        with env_unit(unit):
+            out = run(x, "float32", "sum", resolve_b("rule", w.p, m), exec)
         assert_all_ranks_equal(out, _want(x, "float32", "sum"), exec)
