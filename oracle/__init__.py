@@ -21,7 +21,13 @@ independent columns):
 * ``algorithm1``  -- a literal round-by-round rendezvous simulation of
                      Algorithm 1 with blocking, virtual empty blocks and the
                      telephone-model exchanges, used to pin the tree
-                     evaluation and the round counts.
+                     evaluation, the round counts and the round in which
+                     every rank's every block becomes final.  On one tree
+                     (``build_trees(p, layout="single")``) it is the
+                     single doubly-pipelined tree of Section 1.2.
+* ``reduce_bcast`` -- a rendezvous simulation of the pipelined reduction to
+                     the root of one tree followed by the pipelined
+                     broadcast (Section 2's User-Allreduce1).
 * ``blocks``      -- the block partition and the block-count rule of
                      Section 1.2.
 
@@ -36,12 +42,13 @@ from .trees import Trees, build_trees, heap_postorder_tree
 from .ops import DTYPES, OPS, combine, valid_pair, element_shape, numpy_dtype
 from .reduce import allreduce_tree, allreduce_ltr, allreduce_all
 from .algorithm1 import simulate, DeadlockError
+from .reduce_bcast import simulate_reduce_bcast
 from .blocks import block_bounds, block_rule_lit, block_rule_cal, log2_height
 
 __all__ = [
     "Trees", "build_trees", "heap_postorder_tree",
     "DTYPES", "OPS", "combine", "valid_pair", "element_shape", "numpy_dtype",
     "allreduce_tree", "allreduce_ltr", "allreduce_all",
-    "simulate", "DeadlockError",
+    "simulate", "DeadlockError", "simulate_reduce_bcast",
     "block_bounds", "block_rule_lit", "block_rule_cal", "log2_height",
 ]

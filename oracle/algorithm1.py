@@ -67,11 +67,15 @@ class _Req:
 
 @dataclass
 class Trace:
-    """What the simulation recorded, per rank."""
+    """What the simulation recorded, per rank.  ``final_round[i][k]`` is the
+    round in which block k of rank i took its final value y[k]: for a
+    non-root the round of the parent exchange that delivered it, for a root
+    the round in which it finished Y[k] (after the dual exchange, if any)."""
     active_rounds: Dict[int, List[int]] = field(default_factory=dict)
     exchanges: Dict[int, int] = field(default_factory=dict)
     ops_per_round: Dict[int, Dict[int, int]] = field(default_factory=dict)
     steps_per_round: Dict[int, Dict[int, int]] = field(default_factory=dict)
+    final_round: Dict[int, Dict[int, int]] = field(default_factory=dict)
 
     def span(self, i: int) -> int:
         r = self.active_rounds.get(i, [])
@@ -133,6 +137,9 @@ def simulate(x, dtype: str, op: str, b: int, trees=None,
             if t.parent[i] is None:
                 q = t.dual[i]
                 if q is None:
+                    # a root without a dual has Y[j] complete now
+                    if blk(j) is not None:
+                        trace.final_round.setdefault(i, {})[j] = j
                     continue
                 if skip_void and blk(j) is None:
                     continue
@@ -144,6 +151,7 @@ def simulate(x, dtype: str, op: str, b: int, trees=None,
                     Y[bb[0]:bb[1]] = (combine(dtype, op, mine, got) if i < q
                                       else combine(dtype, op, got, mine))
                     ops = 1
+                    trace.final_round.setdefault(i, {})[j] = j
                 note(i, j, ops, 1)
             else:
                 s_j, r_j = j, j - d
@@ -154,6 +162,7 @@ def simulate(x, dtype: str, op: str, b: int, trees=None,
                 bb = blk(r_j)
                 if bb is not None:
                     Y[bb[0]:bb[1]] = got
+                    trace.final_round.setdefault(i, {})[r_j] = j
                 note(i, j, 0, 1)
 
     gens = {i: program(i) for i in range(p)}

@@ -24,6 +24,10 @@ the text leaves room (each listed in the design notes):
 A second shape, ``wbal`` (recursive weight-balanced split, lower subtree gets
 ceil((n-1)/2)), is provided for experiments only; it is parity unpinned
 except for its p=9 structure.
+
+``layout="single"`` builds one heap-shaped post-order tree over all p ranks
+instead (root p-1, no dual): the single-tree alternative discussed in
+Section 1.2 and the tree of the reduce-then-broadcast comparison of Section 2.
 """
 
 from dataclasses import dataclass, field
@@ -45,7 +49,7 @@ class Trees:
 
     @property
     def height(self) -> int:
-        """Largest depth over both trees (0 for p <= 2)."""
+        """Largest depth over all trees."""
         return max(self.depth) if self.depth else 0
 
     def is_root(self, i: int) -> bool:
@@ -123,14 +127,22 @@ def wbal_postorder_tree(n: int, first: int):
     return parent, child0, child1, depth, lo, root
 
 
-def build_trees(p: int, shape: str = "heap") -> Trees:
-    """Both trees for p >= 1 virtual ranks."""
+def build_trees(p: int, shape: str = "heap", layout: str = "dual") -> Trees:
+    """The trees for p >= 1 virtual ranks.
+
+    ``layout="dual"``: the two trees with dual roots of Section 1.1.
+    ``layout="single"``: one tree of the same shape over all p ranks, root
+    p-1, no dual -- the one-tree variant that Section 1.2 compares against
+    (one doubly-pipelined binary tree) and the tree of the pipelined
+    reduce-then-broadcast of Section 2 (User-Allreduce1)."""
     if p < 1:
         raise ValueError("p must be >= 1")
     make = heap_postorder_tree if shape == "heap" else wbal_postorder_tree
     if shape not in ("heap", "wbal"):
         raise ValueError(shape)
-    n_a = (p + 1) // 2
+    if layout not in ("dual", "single"):
+        raise ValueError(layout)
+    n_a = (p + 1) // 2 if layout == "dual" else p
     t = Trees(p=p)
     t.parent = [None] * p
     t.child0 = [None] * p
