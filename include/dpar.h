@@ -58,6 +58,24 @@ typedef enum {
     DPAR_MATMUL = 2
 } dpar_op_t;
 
+/* Which trees carry the reduction.  The association of every operator
+ * application follows the chosen tree(s), so fp32 results differ between
+ * DUAL_ROOT and the one-tree algorithms; SINGLE_TREE and REDUCE_BCAST give
+ * identical results (the same tree) and differ only in their round structure
+ * (visible with the ROUNDS executors).
+ *   DUAL_ROOT     two post-order trees whose roots exchange (Section 1.1,
+ *                 Algorithm 1): y = S(root A) (.) S(root B).
+ *   SINGLE_TREE   one heap-shaped post-order tree over all p ranks, root
+ *                 p - 1, doubly pipelined (the one-tree variant Section 1.2
+ *                 compares with): y = S(p - 1).
+ *   REDUCE_BCAST  the same tree, a pipelined reduction to the root followed
+ *                 by a pipelined broadcast (Section 2's User-Allreduce1). */
+typedef enum {
+    DPAR_ALG_DUAL_ROOT = 0,
+    DPAR_ALG_SINGLE_TREE = 1,
+    DPAR_ALG_REDUCE_BCAST = 2
+} dpar_alg_t;
+
 /* How the b pipeline rounds are sequenced on the device (Algorithm 1's round
  * loop).  All give bit-identical results.  In the first three, each chunk's
  * y is written to all p outputs right after its up-phase, so reads of later
@@ -74,14 +92,46 @@ typedef enum {
  *                     streams y_0 into the other p - 1 outputs.  HBM reads
  *                     and writes share one bus, so separating the two
  *                     directions avoids read/write turnarounds.
- *   AUTO              SPLIT. */
+ *   AUTO              SPLIT.
+ * The last two run the algorithm's whole round structure, down-phase
+ * included (dpar_schedule_rounds gives the number of rounds R):
+ *   ROUNDS            one launch per round r = 0 .. R-1.  Round r runs the
+ *                     up-step of block r (r < b) for all ranks and writes
+ *                     y[r] to the root(s) only; then every rank at depth
+ *                     d >= 1 receives block r - d (DUAL_ROOT, SINGLE_TREE:
+ *                     Section 1.1's "receive Y[j - d_i] from the parent") or
+ *                     block r - d - b + 1 (REDUCE_BCAST: the broadcast after
+ *                     the reduction), copied from its parent's output, which
+ *                     received it in round r - 1.  Rank i's block j thus
+ *                     becomes final in round j + d_i (REDUCE_BCAST: j for
+ *                     the root, b + j + d_i - 1 otherwise).
+ *   ROUNDS_BARRIER    the same rounds in one persistent (co-resident) launch
+ *                     with a device-wide barrier between rounds.  A barrier
+ *                     that gives up (DPAR_ERR_TIMEOUT) leaves this
+ *                     executor's outputs undefined.
+ * These two read each rank's block from its parent's output, so their HBM
+ * traffic is about 1.5 times the others'. */
 typedef enum {
     DPAR_EXEC_AUTO = 0,
     DPAR_EXEC_LAUNCH_PER_ROUND = 1,
     DPAR_EXEC_GRID_BARRIER = 2,
     DPAR_EXEC_TICKET = 3,
-    DPAR_EXEC_SPLIT = 4
+    DPAR_EXEC_SPLIT = 4,
+    DPAR_EXEC_ROUNDS = 5,
+    DPAR_EXEC_ROUNDS_BARRIER = 6
 } dpar_exec_t;
+
+/* Options of dpar_allreduce_opt.  round_begin / round_end select the rounds
+ * [round_begin, round_end) of a ROUNDS or ROUNDS_BARRIER run (round_end = -1:
+ * to the last round); successive calls that cover [0, R) in order, on the
+ * same stream with the same arguments, give the same outputs as one call.
+ * Other executors need round_begin = 0 and round_end = -1. */
+typedef struct {
+    dpar_alg_t alg;
+    dpar_exec_t exec;
+    int round_begin;
+    int round_end;
+} dpar_options_t;
 
 /* One rank's place in the two trees (Section 1.1).  -1 means "none". */
 typedef struct {
@@ -144,11 +194,29 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
                       dpar_dtype_t dtype, dpar_op_t op, int b,
                       dpar_exec_t exec, hipStream_t stream);
 
+/* dpar_allreduce with an explicit algorithm, executor and round range.
+ * opt == NULL means {DUAL_ROOT, AUTO, 0, -1}.  The ROUNDS executors process
+ * m % 4 trailing elements like the rest (no separate tail pass); when m is
+ * not a multiple of 4 they use one element per lane. */
+int dpar_allreduce_opt(const void* const* x, void* const* y, int p, size_t m,
+                       dpar_dtype_t dtype, dpar_op_t op, int b,
+                       const dpar_options_t* opt, hipStream_t stream);
+
 /* Tree tables of the library's host-side tree builder (Section 1.1: two
  * post-order numbered, heap-shaped complete binary trees; tree A holds ranks
  * [0, ceil(p/2)), tree B the rest; roots ceil(p/2)-1 and p-1 are duals).
  * Fills *out for 0 <= rank < p.  No device work. */
 int dpar_tree_info(int p, int rank, dpar_node_t* out);
+
+/* The same for an algorithm's tree(s): DUAL_ROOT as dpar_tree_info; the
+ * one-tree algorithms give one heap-shaped post-order tree over [0, p) with
+ * root p - 1 and no dual.  No device work. */
+int dpar_tree_info_alg(int p, dpar_alg_t alg, int rank, dpar_node_t* out);
+
+/* Rounds R of the ROUNDS executors' schedule with b blocks: b + H for
+ * DUAL_ROOT and SINGLE_TREE, 2b + H - 1 for REDUCE_BCAST (b when p == 1),
+ * H = the largest depth of the algorithm's tree(s).  No device work. */
+int dpar_schedule_rounds(int p, int b, dpar_alg_t alg);
 
 /* Block-count rule (Section 1.2).  With alpha > 0 and beta > 0 it returns
  * clamp(round(sqrt((4h - 6) beta m / (3 alpha))), 1, m) with h = log2(p + 2)

@@ -47,8 +47,10 @@ constexpr int kStageSlots = 8;
 struct OpsTable {
   uint32_t* dev = nullptr;   // opcodes, padded
   uint32_t* lvl = nullptr;   // level-ordered entries + boundaries (p <= 65534)
+  uint32_t* dn = nullptr;    // parent << 8 | depth of the real tree(s)
   int height = 0;
   int n_a = 0;
+  int root_a = -1, root_b = -1;  // roots of the real tree(s)
 };
 
 struct StageSlot {
@@ -67,7 +69,7 @@ struct DeviceState {
   int lds_limit = 65536;         // dynamic LDS bytes per workgroup
   unsigned* counters = nullptr;  // kCounterSlots slots + one error line
   unsigned next_counter = 0;
-  std::map<int, OpsTable> ops;
+  std::map<std::pair<int, int>, OpsTable> ops;  // (p, one tree?)
   StageSlot stage[kStageSlots];
   unsigned long long tick = 0;
 };
@@ -114,45 +116,58 @@ int get_state(DeviceState** out) {
   return DPAR_SUCCESS;
 }
 
-int get_ops(DeviceState* st, int p, const OpsTable** out) {
-  auto it = st->ops.find(p);
+template <class T>
+int upload(const std::vector<T>& v, T** out, const char* what) {
+  hipError_t e = hipMalloc(out, v.size() * sizeof(T));
+  if (e != hipSuccess)
+    return fail(DPAR_ERR_NOMEM, "%s: %s", what, hipGetErrorString(e));
+  e = hipMemcpy(*out, v.data(), v.size() * sizeof(T), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(*out);
+    *out = nullptr;
+    return hip_fail(e, what);
+  }
+  return DPAR_SUCCESS;
+}
+
+void free_ops(OpsTable& t) {
+  if (t.dev) (void)hipFree(t.dev);
+  if (t.lvl) (void)hipFree(t.lvl);
+  if (t.dn) (void)hipFree(t.dn);
+  t.dev = t.lvl = t.dn = nullptr;
+}
+
+// Device tables for p ranks on the dual-root trees or on one tree: the
+// opcodes and level table of the form the kernels evaluate, and the real
+// tree's parents and depths for the round-structured down-step.
+int get_ops(DeviceState* st, int p, bool single, const OpsTable** out) {
+  const auto key = std::make_pair(p, single ? 1 : 0);
+  auto it = st->ops.find(key);
   if (it != st->ops.end()) {
     *out = &it->second;
     return DPAR_SUCCESS;
   }
-  const dpar::Tree t = dpar::build_tree(p);
-  const std::vector<uint32_t> ops = dpar::make_ops(t);
+  const dpar::Tree kt = single ? dpar::kernel_single_tree(p)
+                               : dpar::build_tree(p);
+  const dpar::Tree real = single ? dpar::build_single_tree(p) : kt;
   OpsTable tab;
-  tab.height = t.height;
-  tab.n_a = t.n_a;
-  std::vector<uint32_t> padded(ops);
-  padded.resize(ops.size() + dpar::kTablePad, 0u);  // kernels read ahead
-  hipError_t e = hipMalloc(&tab.dev, padded.size() * sizeof(uint32_t));
-  if (e != hipSuccess) return fail(DPAR_ERR_NOMEM, "opcode table: %s",
-                                   hipGetErrorString(e));
-  e = hipMemcpy(tab.dev, padded.data(), padded.size() * sizeof(uint32_t),
-                hipMemcpyHostToDevice);
-  if (e != hipSuccess) {
-    (void)hipFree(tab.dev);
-    return hip_fail(e, "hipMemcpy opcodes");
+  tab.height = kt.height;
+  tab.n_a = kt.n_a;
+  tab.root_a = real.root_a;
+  tab.root_b = real.root_b;
+  std::vector<uint32_t> ops = dpar::make_ops(kt);
+  ops.resize(ops.size() + dpar::kTablePad, 0u);  // kernels read ahead
+  int rc = upload(ops, &tab.dev, "opcode table");
+  if (!rc && p <= 65534) rc = upload(dpar::make_levels(kt), &tab.lvl,
+                                     "level table");
+  if (!rc && p < (1 << 24) && real.height < 256)
+    rc = upload(dpar::make_down(real), &tab.dn, "parent table");
+  if (rc) {
+    free_ops(tab);
+    return rc;
   }
-  if (p <= 65534) {
-    const std::vector<uint32_t> lv = dpar::make_levels(t);
-    e = hipMalloc(&tab.lvl, lv.size() * sizeof(uint32_t));
-    if (e != hipSuccess) {
-      (void)hipFree(tab.dev);
-      return fail(DPAR_ERR_NOMEM, "level table: %s", hipGetErrorString(e));
-    }
-    e = hipMemcpy(tab.lvl, lv.data(), lv.size() * sizeof(uint32_t),
-                  hipMemcpyHostToDevice);
-    if (e != hipSuccess) {
-      (void)hipFree(tab.dev);
-      (void)hipFree(tab.lvl);
-      return hip_fail(e, "hipMemcpy level table");
-    }
-  }
-  st->ops[p] = tab;
-  *out = &st->ops[p];
+  st->ops[key] = tab;
+  *out = &st->ops[key];
   return DPAR_SUCCESS;
 }
 
@@ -320,6 +335,41 @@ int dpar_tree_info(int p, int rank, dpar_node_t* out) {
   return DPAR_SUCCESS;
 }
 
+int dpar_tree_info_alg(int p, dpar_alg_t alg, int rank, dpar_node_t* out) {
+  g_err.clear();
+  if (alg < DPAR_ALG_DUAL_ROOT || alg > DPAR_ALG_REDUCE_BCAST)
+    return fail(DPAR_ERR_INVALID_ARG, "dpar_tree_info_alg: unknown alg %d",
+                (int)alg);
+  if (alg == DPAR_ALG_DUAL_ROOT) return dpar_tree_info(p, rank, out);
+  if (p < 1 || rank < 0 || rank >= p || !out)
+    return fail(DPAR_ERR_INVALID_ARG, "dpar_tree_info_alg: bad p/rank/out");
+  const dpar::Tree t = dpar::build_single_tree(p);
+  out->parent = t.parent[rank];
+  out->child0 = t.child0[rank];
+  out->child1 = t.child1[rank];
+  out->depth = t.depth[rank];
+  out->subtree_lo = t.lo[rank];
+  out->dual = -1;
+  return DPAR_SUCCESS;
+}
+
+int dpar_schedule_rounds(int p, int b, dpar_alg_t alg) {
+  g_err.clear();
+  if (p < 1 || b < 1)
+    return fail(DPAR_ERR_INVALID_ARG, "dpar_schedule_rounds: bad p/b");
+  if (alg < DPAR_ALG_DUAL_ROOT || alg > DPAR_ALG_REDUCE_BCAST)
+    return fail(DPAR_ERR_INVALID_ARG, "dpar_schedule_rounds: unknown alg");
+  const dpar::Tree t = alg == DPAR_ALG_DUAL_ROOT ? dpar::build_tree(p)
+                                                 : dpar::build_single_tree(p);
+  const long long r =
+      alg == DPAR_ALG_REDUCE_BCAST
+          ? (t.height > 0 ? 2ll * b + t.height - 1 : (long long)b)
+          : (long long)b + t.height;
+  if (r > 2147483647ll)
+    return fail(DPAR_ERR_UNSUPPORTED, "dpar_schedule_rounds: too many rounds");
+  return (int)r;
+}
+
 int dpar_block_rule(int p, size_t m, double alpha, double beta) {
   g_err.clear();
   if (p < 1) return fail(DPAR_ERR_INVALID_ARG, "dpar_block_rule: p < 1");
@@ -396,18 +446,34 @@ int dpar_block_bounds(const dpar_schedule_t* s, size_t m, int j,
   return DPAR_SUCCESS;
 }
 
-int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
-                      dpar_dtype_t dtype, dpar_op_t op, int b,
-                      dpar_exec_t exec, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
+                   dpar_dtype_t dtype, dpar_op_t op, int b,
+                   const dpar_options_t& opt, hipStream_t stream) {
   g_err.clear();
+  const dpar_exec_t exec = opt.exec;
+  const dpar_alg_t alg = opt.alg;
   if (!x || !y) return fail(DPAR_ERR_INVALID_ARG, "null pointer array");
   if (p < 1) return fail(DPAR_ERR_INVALID_ARG, "p must be >= 1");
   if (b < 0) return fail(DPAR_ERR_INVALID_ARG, "b must be >= 0");
   if (!valid_pair(dtype, op))
     return fail(DPAR_ERR_UNSUPPORTED, "unsupported dtype/op pair (%d, %d)",
                 (int)dtype, (int)op);
-  if (exec < DPAR_EXEC_AUTO || exec > DPAR_EXEC_SPLIT)
+  if (exec < DPAR_EXEC_AUTO || exec > DPAR_EXEC_ROUNDS_BARRIER)
     return fail(DPAR_ERR_INVALID_ARG, "unknown executor %d", (int)exec);
+  if (alg < DPAR_ALG_DUAL_ROOT || alg > DPAR_ALG_REDUCE_BCAST)
+    return fail(DPAR_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+  const bool rounds_exec =
+      exec == DPAR_EXEC_ROUNDS || exec == DPAR_EXEC_ROUNDS_BARRIER;
+  if (!rounds_exec && (opt.round_begin != 0 || opt.round_end != -1))
+    return fail(DPAR_ERR_INVALID_ARG, "a round range needs a ROUNDS executor");
+  if (opt.round_begin < 0 || opt.round_end < -1 ||
+      (opt.round_end >= 0 && opt.round_end < opt.round_begin))
+    return fail(DPAR_ERR_INVALID_ARG, "bad round range [%d, %d)",
+                opt.round_begin, opt.round_end);
   bool aligned16 = true;
   for (int i = 0; i < p; ++i) {
     if (!x[i] || !y[i])
@@ -428,6 +494,19 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
   if (m > (size_t)1 << 40)
     return fail(DPAR_ERR_UNSUPPORTED, "m beyond 2^40 elements");
 
+  int r0 = 0, r1 = 0;
+  if (rounds_exec) {
+    const int R = dpar_schedule_rounds(p, b, alg);
+    if (R < 0) return R;
+    r0 = opt.round_begin;
+    r1 = opt.round_end < 0 ? R : opt.round_end;
+    if (r1 > R)
+      return fail(DPAR_ERR_INVALID_ARG, "round range [%d, %d) beyond R = %d",
+                  r0, r1, R);
+  }
+  // the round-structured executors have no separate tail pass: one element
+  // per lane when 4-element quanta would leave one
+  if (rounds_exec && dtype != DPAR_U32_MAT2X2 && m % 4 != 0) aligned16 = false;
   dpar::Schedule s;
   dpar::Path path;
   choose_schedule(m, dtype, b, aligned16, &s, &path);
@@ -445,12 +524,16 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
                                   "partially overlap an input");
     alias_remember(x, y, p, m * esz);
   }
+  if (rounds_exec && r0 == r1) return DPAR_SUCCESS;
   DeviceState* st = nullptr;
   int rc = get_state(&st);
   if (rc) return rc;
   const OpsTable* ops = nullptr;
-  rc = get_ops(st, p, &ops);
+  const bool single = alg != DPAR_ALG_DUAL_ROOT;
+  rc = get_ops(st, p, single, &ops);
   if (rc) return rc;
+  if (rounds_exec && !ops->dn)
+    return fail(DPAR_ERR_UNSUPPORTED, "ROUNDS executors need p < 2^24");
 
   int waves = p >= 2 ? (env_int("DPAR_WAVES", 2) == 1 ? 1 : 2) : 1;
   const int nslots = ops->height + 1;
@@ -506,10 +589,24 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
   tab.yp = slot->dev + p;
   tab.ops = ops->dev;
   tab.lvl = ops->lvl;
+  tab.dn = ops->dn;
 
-  dpar::Exec ex = (dpar::Exec)exec;
-  if (exec == DPAR_EXEC_AUTO) ex = dpar::Exec::SPLIT;
+  dpar::Exec ex = exec == DPAR_EXEC_ROUNDS           ? dpar::Exec::ROUNDS
+                  : exec == DPAR_EXEC_ROUNDS_BARRIER ? dpar::Exec::ROUNDS_BARRIER
+                  : exec == DPAR_EXEC_AUTO           ? dpar::Exec::SPLIT
+                                                     : (dpar::Exec)exec;
   if (ex == dpar::Exec::SPLIT && p < 2) ex = dpar::Exec::DISPATCH;
+  // outputs the non-fused up-step writes: y_0 for the split executor (the
+  // broadcast pass copies it on), the real root(s) for the round structure
+  prm.out0 = 0;
+  prm.out1 = -1;
+  if (rounds_exec) {
+    prm.out0 = ops->root_a;
+    prm.out1 = ops->root_b;
+  }
+  prm.dshift = alg == DPAR_ALG_REDUCE_BCAST ? b - 1 : 0;
+  prm.r0 = r0;
+  prm.r1 = r1;
 
   // Work-item evaluation: a post-order walk per wavefront (SEQ) unless the
   // chunks of a round (launch per round, grid barrier) or of the whole call
@@ -531,7 +628,9 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
     // measured crossover: per round (launch per round) level items win below
     // ~2 chunks per CU; over a whole ticketed call below ~1/2 chunk per CU
     const bool per_round = ex == dpar::Exec::LAUNCH_PER_ROUND ||
-                           ex == dpar::Exec::GRID_BARRIER;
+                           ex == dpar::Exec::GRID_BARRIER ||
+                           ex == dpar::Exec::ROUNDS ||
+                           ex == dpar::Exec::ROUNDS_BARRIER;
     bool want = per_round ? (uint64_t)s.C < 2ull * (uint64_t)st->num_cus
                           : s.units() < (uint64_t)st->num_cus / 2;
     const char* u = std::getenv("DPAR_UNIT");
@@ -541,7 +640,8 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
     // level work items its co-resident grid stalled in a barrier wait (seen
     // once, at two workgroups per CU; the watchdog ended it) for a reason not
     // yet established, so that combination stays switched off.
-    if (ex == dpar::Exec::GRID_BARRIER) want = false;
+    if (ex == dpar::Exec::GRID_BARRIER || ex == dpar::Exec::ROUNDS_BARRIER)
+      want = false;
     if (want && tmax >= 0) {
       // largest block in quanta; chunk capacity T = a power of two
       const uint64_t maxq = ((s.NL + s.b - 1) / s.b) * (uint64_t)s.lq;
@@ -559,6 +659,8 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
     if ((uint64_t)prm.b * (uint64_t)prm.C >= (1ull << 31))
       return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items");
   }
+  // round-structured down-step: two ranks per wavefront per work item
+  prm.dslice = 2 * (unit == dpar::Unit::LEVEL ? 16 : waves);
 
   // the up-phase of the split executor: one workgroup per work item handed
   // out by the hardware in round order (persistent ticketed workgroups on
@@ -606,6 +708,24 @@ int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
   return DPAR_SUCCESS;
 }
 
+}  // namespace
+
+extern "C" {
+
+int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
+                      dpar_dtype_t dtype, dpar_op_t op, int b,
+                      dpar_exec_t exec, hipStream_t stream) {
+  const dpar_options_t opt{DPAR_ALG_DUAL_ROOT, exec, 0, -1};
+  return allreduce_impl(x, y, p, m, dtype, op, b, opt, stream);
+}
+
+int dpar_allreduce_opt(const void* const* x, void* const* y, int p, size_t m,
+                       dpar_dtype_t dtype, dpar_op_t op, int b,
+                       const dpar_options_t* opt, hipStream_t stream) {
+  const dpar_options_t dflt{DPAR_ALG_DUAL_ROOT, DPAR_EXEC_AUTO, 0, -1};
+  return allreduce_impl(x, y, p, m, dtype, op, b, opt ? *opt : dflt, stream);
+}
+
 int dpar_allreduce(const void* const* x, void* const* y, int p, size_t m,
                    dpar_dtype_t dtype, dpar_op_t op, int b,
                    hipStream_t stream) {
@@ -647,10 +767,7 @@ int dpar_finalize(void) {
     DeviceState* st = kv.second.get();
     (void)hipSetDevice(st->device);
     (void)hipDeviceSynchronize();
-    for (auto& o : st->ops) {
-      (void)hipFree(o.second.dev);
-      if (o.second.lvl) (void)hipFree(o.second.lvl);
-    }
+    for (auto& o : st->ops) free_ops(o.second);
     for (auto& s : st->stage) {
       if (s.ev) (void)hipEventDestroy(s.ev);
       if (s.host) (void)hipHostFree(s.host);

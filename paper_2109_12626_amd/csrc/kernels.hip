@@ -271,9 +271,18 @@ __device__ __forceinline__ void run_unit(const uint64_t* __restrict__ xp,
     y = L::ap(slots[lane], slots[(size_t)prm.nslots * 64 + lane]);
   }
 
-  // Fused broadcast of y to this wavefront's ranks, or y to y_0 only.
+  // Fused broadcast of y to this wavefront's ranks, or y to the outputs of
+  // ranks out0 and out1 only.
   if (!FUSED) {
-    if (active && wave == 0) L::store(yp[0] + unit_off, lane_off, y);
+    if (active) {
+      if (W == 1) {
+        L::store(yp[prm.out0] + unit_off, lane_off, y);
+        if (prm.out1 >= 0) L::store(yp[prm.out1] + unit_off, lane_off, y);
+      } else {
+        const int o = wave == 0 ? prm.out0 : prm.out1;
+        if (o >= 0) L::store(yp[o] + unit_off, lane_off, y);
+      }
+    }
   } else if (active) {
     for (int base = r0; base < r1; base += kU) {
       uint64_t row[kU];
@@ -407,7 +416,9 @@ __device__ __forceinline__ void run_unit_lv(const uint64_t* __restrict__ xp,
       if (q < count) L::store(ptr[idx >> sh], (uint32_t)q * L::bytes, Y[q]);
     }
   } else if (tid < count) {
-    L::store(yp[0] + unit_off, (uint32_t)tid * L::bytes, Y[tid]);
+    L::store(yp[prm.out0] + unit_off, (uint32_t)tid * L::bytes, Y[tid]);
+    if (prm.out1 >= 0)
+      L::store(yp[prm.out1] + unit_off, (uint32_t)tid * L::bytes, Y[tid]);
   }
   __syncthreads();  // LDS is reused by the next work item
 }
@@ -416,6 +427,7 @@ __device__ __forceinline__ void run_unit_lv(const uint64_t* __restrict__ xp,
 
 template <class L, int W, bool FUSED>
 struct SeqUnit {
+  using Lane = L;
   static constexpr int kThreads = 64 * W;
   __device__ static void run(const uint64_t* __restrict__ xp,
                              const uint64_t* __restrict__ yp,
@@ -433,6 +445,7 @@ struct SeqUnit {
 
 template <class L, bool FUSED>
 struct LvUnit {
+  using Lane = L;
   static constexpr int kThreads = kLvThreads;
   __device__ static void run(const uint64_t* __restrict__ xp,
                              const uint64_t* __restrict__ yp,
@@ -498,6 +511,98 @@ __global__ __launch_bounds__(U::kThreads) void k_barrier(DPAR_KARGS) {
     for (uint64_t c = blockIdx.x; c < (uint64_t)prm.C; c += gridDim.x)
       U::run(xp, yp, ops, lvl, prm, (uint64_t)j * prm.C + c, lds_raw);
     if (j + 1 < prm.b) grid_barrier(prm);
+  }
+}
+
+// ------------------------------------------------------------ round-structured executor
+// Algorithm 1's round structure made explicit on the device.  Round r runs
+// the up-step of block r (r < b) for all ranks, writing y[r] to the roots'
+// outputs only, and the down-step: every rank at depth d >= 1 receives block
+// r - d - dshift from its parent, i.e. copies it from the parent's output,
+// which the parent received in round r - 1 (dshift = 0: the doubly-pipelined
+// schedule of Algorithm 1; dshift = b - 1: the broadcast that follows a
+// completed reduction, Section 2's reduce-then-broadcast).
+
+// Down-step for ranks [i0, i1): the workgroup's wavefronts take the ranks in
+// turn; a wavefront copies the whole block, 64 lanes at a time.
+template <class L, int TH>
+__device__ __forceinline__ void down_copy(const uint64_t* __restrict__ yp,
+                                          const uint32_t* __restrict__ dn,
+                                          const Params& prm, int round, int i0,
+                                          int i1) {
+  constexpr int kWaves = TH / 64;
+  constexpr int kB = 4;  // loads in flight per lane
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  for (int i = i0 + wave; i < i1; i += kWaves) {
+    const uint32_t e = dn[i];
+    const uint32_t par = e >> 8;
+    if (par == 0xFFFFFFu) continue;  // a root: its blocks come from the up-step
+    const int64_t j = (int64_t)round - (int64_t)(e & 0xFFu) - prm.dshift;
+    if (j < 0 || j >= prm.b) continue;
+    const uint64_t ls = prm.NL * (uint64_t)j / (uint64_t)prm.b;
+    const uint64_t le = prm.NL * (uint64_t)(j + 1) / (uint64_t)prm.b;
+    const uint64_t qs = min(ls * prm.lq, prm.Q);
+    const uint64_t qe = min(le * prm.lq, prm.Q);
+    const uint64_t base = (prm.qbase + qs) * (uint64_t)L::bytes;
+    const uint64_t src = yp[par] + base, dst = yp[i] + base;
+    const uint64_t n = qe - qs;
+    for (uint64_t q0 = 0; q0 < n; q0 += 64 * kB) {
+      typename L::T v[kB];
+#pragma unroll
+      for (int k = 0; k < kB; ++k) {
+        const uint64_t q = q0 + (uint64_t)k * 64 + lane;
+        if (q < n) v[k] = L::load(src + q * L::bytes, 0);
+      }
+#pragma unroll
+      for (int k = 0; k < kB; ++k) {
+        const uint64_t q = q0 + (uint64_t)k * 64 + lane;
+        if (q < n) L::store(dst + q * L::bytes, 0, v[k]);
+      }
+    }
+  }
+}
+
+// Work item `item` of round r: the first C items (r < b) are the up-step's
+// chunks of block r, the rest are down-step slices of dslice ranks.
+template <class U>
+__device__ __forceinline__ void round_item(DPAR_KARGS,
+                                           const uint32_t* __restrict__ dn,
+                                           int r, uint64_t item, char* lds) {
+  const uint64_t nup = r < prm.b ? (uint64_t)prm.C : 0;
+  if (item < nup) {
+    U::run(xp, yp, ops, lvl, prm, (uint64_t)r * prm.C + item, lds);
+    return;
+  }
+  const int i0 = (int)(item - nup) * prm.dslice;
+  down_copy<typename U::Lane, U::kThreads>(yp, dn, prm, r, i0,
+                                           min(prm.p, i0 + prm.dslice));
+}
+
+template <class U>
+__global__ __launch_bounds__(U::kThreads) void k_rounds(
+    DPAR_KARGS, const uint32_t* __restrict__ dn, int round) {
+  extern __shared__ char lds_raw[];
+  round_item<U>(xp, yp, ops, lvl, prm, dn, round, blockIdx.x, lds_raw);
+}
+
+template <class U>
+__global__ __launch_bounds__(U::kThreads) void k_rounds_barrier(
+    DPAR_KARGS, const uint32_t* __restrict__ dn) {
+  extern __shared__ char lds_raw[];
+  const uint64_t ndown = (uint64_t)(prm.p + prm.dslice - 1) / prm.dslice;
+  for (int r = prm.r0; r < prm.r1; ++r) {
+    const uint64_t items = (r < prm.b ? (uint64_t)prm.C : 0) + ndown;
+    for (uint64_t it = blockIdx.x; it < items; it += gridDim.x)
+      round_item<U>(xp, yp, ops, lvl, prm, dn, r, it, lds_raw);
+    if (r + 1 < prm.r1) {
+      // the next round reads blocks other workgroups (other XCDs, other L2s)
+      // wrote in this one: every thread releases its stores at agent scope
+      // before the barrier and acquires after it
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      grid_barrier(prm);
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
   }
 }
 
@@ -642,25 +747,40 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
                          tab.xp, tab.yp, tab.ops, tab.lvl, prm, j);
     return hipGetLastError();
   }
-  const void* kfn = exec == Exec::GRID_BARRIER
-                        ? reinterpret_cast<const void*>(&k_barrier<U>)
-                        : reinterpret_cast<const void*>(&k_ticket<U>);
+  const uint64_t ndown = (uint64_t)(prm.p + prm.dslice - 1) / prm.dslice;
+  if (exec == Exec::ROUNDS) {
+    for (int r = prm.r0; r < prm.r1; ++r) {
+      const uint64_t items = (r < prm.b ? (uint64_t)prm.C : 0) + ndown;
+      hipLaunchKernelGGL((k_rounds<U>), dim3((unsigned)items), block, lds,
+                         stream, tab.xp, tab.yp, tab.ops, tab.lvl, prm, tab.dn,
+                         r);
+    }
+    return hipGetLastError();
+  }
+  const void* kfn =
+      exec == Exec::GRID_BARRIER     ? reinterpret_cast<const void*>(&k_barrier<U>)
+      : exec == Exec::ROUNDS_BARRIER ? reinterpret_cast<const void*>(&k_rounds_barrier<U>)
+                                     : reinterpret_cast<const void*>(&k_ticket<U>);
   int per_cu = 0;
   hipError_t e = occupancy(kfn, U::kThreads, lds, &per_cu);
   if (e != hipSuccess) return e;
-  if (exec == Exec::GRID_BARRIER) {
+  if (exec == Exec::GRID_BARRIER || exec == Exec::ROUNDS_BARRIER) {
     if (per_cu < 1) return hipErrorInvalidConfiguration;
     // every workgroup must be resident at once; leave one slot per CU free
     // rather than fill the machine to the last slot
     if (per_cu > 1) --per_cu;
     uint64_t grid = (uint64_t)per_cu * num_cus;
-    if (grid > (uint64_t)prm.C) grid = prm.C;  // more would only wait
+    // more than the largest round's work items would only wait
+    const uint64_t most =
+        exec == Exec::GRID_BARRIER ? (uint64_t)prm.C : (uint64_t)prm.C + ndown;
+    if (grid > most) grid = most;
     const uint64_t* xp = tab.xp;
     const uint64_t* yp = tab.yp;
     const uint32_t* ops = tab.ops;
     const uint32_t* lvl = tab.lvl;
+    const uint32_t* dn = tab.dn;
     Params p2 = prm;
-    void* args[] = {&xp, &yp, &ops, &lvl, &p2};
+    void* args[] = {&xp, &yp, &ops, &lvl, &p2, &dn};
     return hipLaunchCooperativeKernel(kfn, dim3((unsigned)grid), block, args,
                                       (unsigned)lds, stream);
   }
@@ -676,7 +796,8 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
 template <class L>
 hipError_t launch_l(Unit unit, int waves, Exec exec, const Tables& tab,
                     const Params& prm, hipStream_t stream, int num_cus) {
-  const bool fused = exec != Exec::TICKET_SPLIT && exec != Exec::SPLIT;
+  const bool fused = exec != Exec::TICKET_SPLIT && exec != Exec::SPLIT &&
+                     exec != Exec::ROUNDS && exec != Exec::ROUNDS_BARRIER;
   const Exec ex = exec == Exec::TICKET_SPLIT ? Exec::TICKET
                   : exec == Exec::SPLIT      ? Exec::DISPATCH
                                              : exec;

@@ -25,6 +25,11 @@ enum class Exec : int {
   DISPATCH = 5,      // one launch, one workgroup per work item in round
                      // order (the hardware dispatcher hands them out)
   TICKET_SPLIT = 6,  // as SPLIT with a ticketed up-phase (experiments)
+  ROUNDS = 7,        // the algorithm's full round structure, one launch per
+                     // round: up-step of block r to the roots' outputs,
+                     // down-step of every rank from its parent's output
+  ROUNDS_BARRIER = 8,  // the same rounds in one persistent launch with a
+                       // grid barrier (and agent-scope fences) per round
 };
 
 // Scalars every kernel needs.  The tables (device pointers to the x and y
@@ -52,6 +57,11 @@ struct Params {
   unsigned* bar_gen;    // GRID_BARRIER: generation
   unsigned* err;        // bit 0: a barrier wait gave up
   unsigned long long spin_limit;
+  int out0, out1;       // non-fused up-step: ranks whose outputs receive y
+                        // (out1 < 0: none)
+  int dshift;           // ROUNDS: depth-d rank receives block r - d - dshift
+  int dslice;           // ROUNDS: ranks per down-step work item
+  int r0, r1;           // ROUNDS: run rounds [r0, r1)
 };
 
 // Ticket counters per call (each on its own 128-byte line): work-item batch
@@ -68,6 +78,7 @@ struct Tables {
   const uint64_t* yp;   // [p] device addresses of y_i
   const uint32_t* ops;  // [p] opcodes (plan.hpp)
   const uint32_t* lvl;  // [p] level-ordered entries, then H + 2 offsets
+  const uint32_t* dn;   // [p] ROUNDS: parent << 8 | depth (plan.hpp)
 };
 
 // Enqueue one executor run over all b*C chunks of a schedule.

@@ -77,10 +77,60 @@ Tree build_tree(int p) {
   return t;
 }
 
+Tree build_single_tree(int p) {
+  Tree t;
+  t.p = p;
+  t.n_a = p;
+  t.parent.assign(p, -1);
+  t.child0.assign(p, -1);
+  t.child1.assign(p, -1);
+  t.depth.assign(p, 0);
+  t.lo.assign(p, 0);
+  t.dual.assign(p, -1);
+  add_heap_tree(t, 0, p);
+  t.root_a = p - 1;
+  t.root_b = -1;
+  t.height = 0;
+  for (int d : t.depth) t.height = std::max(t.height, d);
+  return t;
+}
+
+Tree kernel_single_tree(int p) {
+  if (p <= 2) return build_tree(p);
+  Tree t = build_single_tree(p);
+  const int r = p - 1, c0 = t.child0[r], c1 = t.child1[r];
+  t.n_a = t.lo[c0];              // part A = [0, lo(c0)), its root is c1
+  t.root_a = c1;
+  t.root_b = r;
+  t.parent[c1] = -1;
+  t.child1[r] = -1;              // the root keeps only its first child
+  t.dual[c1] = r;
+  t.dual[r] = c1;
+  t.slot_shift = 1;
+  return t;
+}
+
+std::vector<uint32_t> make_down(const Tree& t) {
+  std::vector<uint32_t> dn(t.p, 0);
+  for (int i = 0; i < t.p; ++i) {
+    const uint32_t par = t.parent[i] < 0 ? 0xFFFFFFu : (uint32_t)t.parent[i];
+    dn[i] = (par << 8) | ((uint32_t)t.depth[i] & 0xFFu);
+  }
+  return dn;
+}
+
+int device_rounds(const Tree& real, Alg alg, int b) {
+  if (alg == Alg::REDUCE_BCAST)
+    return real.height > 0 ? 2 * b + real.height - 1 : b;
+  return b + real.height;
+}
+
 std::vector<uint32_t> make_ops(const Tree& t) {
   std::vector<uint32_t> ops(t.p, 0);
   for (int i = 0; i < t.p; ++i) {
-    uint32_t op = (uint32_t)t.depth[i] & OP_DEPTH_MASK;
+    // the slot a waiting value uses; only SAVE and second-child reads use it
+    const int slot = std::max(0, t.depth[i] - t.slot_shift);
+    uint32_t op = (uint32_t)slot & OP_DEPTH_MASK;
     if (t.child0[i] >= 0) op |= OP_C0;
     if (t.child1[i] >= 0) op |= OP_C1;
     const int par = t.parent[i];

@@ -21,19 +21,51 @@ enum : uint32_t {
   OP_SAVE = 1u << 8,      // result waits in slot[d] (else it becomes current)
 };
 
+// Which trees carry the reduction (Sections 1.1, 1.2 and 2).
+enum class Alg : int {
+  DUAL_ROOT = 0,     // two trees, roots exchange (Algorithm 1)
+  SINGLE_TREE = 1,   // one doubly-pipelined tree over all ranks
+  REDUCE_BCAST = 2,  // one tree: pipelined reduce, then pipelined broadcast
+};
+
 struct Tree {
   int p = 0;
   int n_a = 0;            // tree A = [0, n_a), tree B = [n_a, p)
   int root_a = -1, root_b = -1;
   int height = 0;         // largest depth over both trees
+  // slot of a rank's waiting value = depth - slot_shift (see make_ops)
+  int slot_shift = 0;
   std::vector<int> parent, child0, child1, depth, lo, dual;
 };
 
 // Heap-shaped complete binary trees, post-order numbered (Section 1.1).
 Tree build_tree(int p);
 
+// One heap-shaped post-order tree over all p ranks, root p - 1 (the
+// single-tree variants of Sections 1.2 and 2).
+Tree build_single_tree(int p);
+
+// The single tree in the two-part form the device round program runs: part
+// A = the root's second-child subtree [0, lo(child0)), part B = the
+// first-child subtree plus the root, which keeps only its first child.  Then
+// y = S(A) (.) S(B) = S(child1) (.) (S(child0) (.) x_root), the single tree's
+// value.  Depths stay the real ones (the root's level comes after its
+// children's); slot_shift = 1 puts part A's root in slot 0.  For p <= 2 the
+// single tree and the dual-root trees give the same product and the
+// dual-root form is returned.
+Tree kernel_single_tree(int p);
+
 // Opcodes for ranks 0..p-1 (uint32 each).
 std::vector<uint32_t> make_ops(const Tree& t);
+
+// Per-rank down-phase entries for the round-structured executor:
+// parent << 8 | depth, parent 0xFFFFFF for a root.  Needs p < 2^24, depth
+// < 256.
+std::vector<uint32_t> make_down(const Tree& t);
+
+// Rounds of the round-structured device schedule (b + H, or 2b + H - 1 for
+// REDUCE_BCAST with H > 0).
+int device_rounds(const Tree& real, Alg alg, int b);
 
 // Ranks in level order for level-synchronous evaluation: deepest level
 // first, ranks ascending within a level; entry = rank << 16 | code with code

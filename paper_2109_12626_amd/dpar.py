@@ -25,14 +25,19 @@ DPAR_ERR_TIMEOUT = -6
 DPAR_INT32, DPAR_FLOAT32, DPAR_U32_MAT2X2 = 0, 1, 2
 DPAR_SUM, DPAR_MAX, DPAR_MATMUL = 0, 1, 2
 DPAR_EXEC_AUTO, DPAR_EXEC_LAUNCH_PER_ROUND, DPAR_EXEC_GRID_BARRIER, \
-    DPAR_EXEC_TICKET, DPAR_EXEC_SPLIT = 0, 1, 2, 3, 4
+    DPAR_EXEC_TICKET, DPAR_EXEC_SPLIT, DPAR_EXEC_ROUNDS, \
+    DPAR_EXEC_ROUNDS_BARRIER = 0, 1, 2, 3, 4, 5, 6
+DPAR_ALG_DUAL_ROOT, DPAR_ALG_SINGLE_TREE, DPAR_ALG_REDUCE_BCAST = 0, 1, 2
 
 DTYPES = {"int32": DPAR_INT32, "float32": DPAR_FLOAT32,
           "u32mat2x2": DPAR_U32_MAT2X2}
 OPS = {"sum": DPAR_SUM, "max": DPAR_MAX, "matmul": DPAR_MATMUL}
 EXECS = {"auto": DPAR_EXEC_AUTO, "launch": DPAR_EXEC_LAUNCH_PER_ROUND,
          "barrier": DPAR_EXEC_GRID_BARRIER, "ticket": DPAR_EXEC_TICKET,
-         "split": DPAR_EXEC_SPLIT}
+         "split": DPAR_EXEC_SPLIT, "rounds": DPAR_EXEC_ROUNDS,
+         "rounds_barrier": DPAR_EXEC_ROUNDS_BARRIER}
+ALGS = {"dual": DPAR_ALG_DUAL_ROOT, "single": DPAR_ALG_SINGLE_TREE,
+        "reduce_bcast": DPAR_ALG_REDUCE_BCAST}
 
 
 class DparError(RuntimeError):
@@ -45,6 +50,11 @@ class dpar_node_t(ctypes.Structure):
     _fields_ = [("parent", ctypes.c_int), ("child0", ctypes.c_int),
                 ("child1", ctypes.c_int), ("depth", ctypes.c_int),
                 ("subtree_lo", ctypes.c_int), ("dual", ctypes.c_int)]
+
+
+class dpar_options_t(ctypes.Structure):
+    _fields_ = [("alg", ctypes.c_int), ("exec", ctypes.c_int),
+                ("round_begin", ctypes.c_int), ("round_end", ctypes.c_int)]
 
 
 class dpar_schedule_t(ctypes.Structure):
@@ -71,7 +81,11 @@ def lib():
     vp, sz, i = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
     L.dpar_allreduce.argtypes = [vp, vp, i, sz, i, i, i, vp]
     L.dpar_allreduce_ex.argtypes = [vp, vp, i, sz, i, i, i, i, vp]
+    L.dpar_allreduce_opt.argtypes = [vp, vp, i, sz, i, i, i,
+                                     ctypes.POINTER(dpar_options_t), vp]
     L.dpar_tree_info.argtypes = [i, i, ctypes.POINTER(dpar_node_t)]
+    L.dpar_tree_info_alg.argtypes = [i, i, i, ctypes.POINTER(dpar_node_t)]
+    L.dpar_schedule_rounds.argtypes = [i, i, i]
     L.dpar_block_rule.argtypes = [i, sz, ctypes.c_double, ctypes.c_double]
     L.dpar_rounds.argtypes = [i, i, i]
     L.dpar_schedule_info.argtypes = [i, sz, i, i, i,
@@ -83,9 +97,11 @@ def lib():
     L.dpar_last_error.restype = ctypes.c_char_p
     L.dpar_last_error.argtypes = []
     L.dpar_finalize.argtypes = []
-    for name in ("dpar_allreduce", "dpar_allreduce_ex", "dpar_tree_info",
-                 "dpar_block_rule", "dpar_rounds", "dpar_schedule_info",
-                 "dpar_block_bounds", "dpar_check_status", "dpar_finalize",
+    for name in ("dpar_allreduce", "dpar_allreduce_ex", "dpar_allreduce_opt",
+                 "dpar_tree_info", "dpar_tree_info_alg",
+                 "dpar_schedule_rounds", "dpar_block_rule", "dpar_rounds",
+                 "dpar_schedule_info", "dpar_block_bounds",
+                 "dpar_check_status", "dpar_finalize",
                  "dpar_set_phase_event"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -149,10 +165,30 @@ def dpar_allreduce_ex(x, y, p, m, dtype, op, b=0, exec="auto", stream=None):
         _enum(OPS, op), int(b), _enum(EXECS, exec), _stream(stream)))
 
 
+def dpar_allreduce_opt(x, y, p, m, dtype, op, b=0, alg="dual", exec="auto",
+                       round_begin=0, round_end=-1, stream=None):
+    opt = dpar_options_t(_enum(ALGS, alg), _enum(EXECS, exec),
+                         int(round_begin), int(round_end))
+    return _check(lib().dpar_allreduce_opt(
+        _ptr_array(x), _ptr_array(y), int(p), int(m), _enum(DTYPES, dtype),
+        _enum(OPS, op), int(b), ctypes.byref(opt), _stream(stream)))
+
+
 def dpar_tree_info(p, rank):
     out = dpar_node_t()
     _check(lib().dpar_tree_info(int(p), int(rank), ctypes.byref(out)))
     return {f: getattr(out, f) for f, _ in dpar_node_t._fields_}
+
+
+def dpar_tree_info_alg(p, alg, rank):
+    out = dpar_node_t()
+    _check(lib().dpar_tree_info_alg(int(p), _enum(ALGS, alg), int(rank),
+                                    ctypes.byref(out)))
+    return {f: getattr(out, f) for f, _ in dpar_node_t._fields_}
+
+
+def dpar_schedule_rounds(p, b, alg="dual"):
+    return _check(lib().dpar_schedule_rounds(int(p), int(b), _enum(ALGS, alg)))
 
 
 def dpar_block_rule(p, m, alpha=0.0, beta=0.0):
@@ -208,7 +244,8 @@ def dpar_finalize():
 _ELEM = {"int32": 4, "float32": 4, "u32mat2x2": 16}
 
 
-def allreduce(x, y=None, dtype=None, op="sum", b=0, exec="auto", stream=None):
+def allreduce(x, y=None, dtype=None, op="sum", b=0, exec="auto", stream=None,
+              alg="dual"):
     """Tensor front end: x is a [p, m] (or [p, m, 4] uint32 for matrices)
     device tensor, or a list of p 1-D tensors; y likewise (default: a new
     [p, ...] tensor).  Returns y.  Only marshals addresses."""
@@ -230,5 +267,5 @@ def allreduce(x, y=None, dtype=None, op="sum", b=0, exec="auto", stream=None):
     ys = rows(y) if isinstance(y, torch.Tensor) else [t.data_ptr() for t in y]
     if stream is None:
         stream = torch.cuda.current_stream(sample.device)
-    dpar_allreduce_ex(xs, ys, p, m, dtype, op, b, exec, stream)
+    dpar_allreduce_opt(xs, ys, p, m, dtype, op, b, alg, exec, 0, -1, stream)
     return y

@@ -116,9 +116,9 @@ def test_scalar_path_matches_canonical_partition():
 A = 1 << 30  # fake, never dereferenced: every case fails before device work
 
 
-def _err(fn, *args):
+def _err(fn, *args, **kw):
     with pytest.raises(dpar.DparError) as e:
-        fn(*args)
+        fn(*args, **kw)
     return e.value.code
 
 
@@ -191,3 +191,68 @@ def test_info_argument_errors():
     assert _err(dpar.dpar_tree_info, 5, 5) == dpar.DPAR_ERR_INVALID_ARG
     assert _err(dpar.dpar_rounds, 5, 0, 1) == dpar.DPAR_ERR_INVALID_ARG
     assert _err(dpar.dpar_block_rule, 0, 10) == dpar.DPAR_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("p", list(range(1, 40)) + [127, 128, 1151, 1152])
+@pytest.mark.parametrize("alg", ["single", "reduce_bcast"])
+def test_tree_info_alg_matches_oracle_single_tree(p, alg):
+    t = oracle.build_trees(p, layout="single")
+    none = lambda v: -1 if v is None else v  # noqa: E731
+    for i in range(p):
+        got = dpar.dpar_tree_info_alg(p, alg, i)
+        assert got == {"parent": none(t.parent[i]), "child0": none(t.child0[i]),
+                       "child1": none(t.child1[i]), "depth": t.depth[i],
+                       "subtree_lo": t.lo[i], "dual": -1}, i
+    assert dpar.dpar_tree_info_alg(p, "dual", p - 1) == \
+        dpar.dpar_tree_info(p, p - 1)
+
+
+@pytest.mark.parametrize("p", [1, 2, 3, 5, 7, 14, 36, 64, 100])
+@pytest.mark.parametrize("b", [1, 2, 5])
+def test_schedule_rounds_match_simulations(p, b):
+    """The device round structure's length equals the rounds the oracle's
+    simulations use: Algorithm 1 on the dual-root trees and on one tree,
+    and the reduce-then-broadcast."""
+    x = np.zeros((p, 2 * b + 2), dtype=np.int32)
+    _, tr = oracle.simulate(x, "int32", "sum", b)
+    want = tr.global_rounds() if p > 1 else b
+    assert dpar.dpar_schedule_rounds(p, b, "dual") == want
+    t1 = oracle.build_trees(p, layout="single")
+    _, tr = oracle.simulate(x, "int32", "sum", b, trees=t1)
+    want = tr.global_rounds() if p > 1 else b
+    assert dpar.dpar_schedule_rounds(p, b, "single") == want
+    _, tr = oracle.simulate_reduce_bcast(x, "int32", "sum", b)
+    assert dpar.dpar_schedule_rounds(p, b, "reduce_bcast") == \
+        tr.global_rounds()
+
+
+def test_option_errors():
+    xs = [A + i * 4096 for i in range(4)]
+    ys = [A + (1 << 20) + i * 4096 for i in range(4)]
+    f = dpar.dpar_allreduce_opt
+    args = (xs, ys, 4, 1000, "int32", "sum", 4)
+    assert _err(f, *args, alg=7) == dpar.DPAR_ERR_INVALID_ARG
+    assert _err(f, *args, exec=7) == dpar.DPAR_ERR_INVALID_ARG
+    # a round range needs a round-structured executor
+    assert _err(f, *args, exec="split", round_begin=1) == \
+        dpar.DPAR_ERR_INVALID_ARG
+    assert _err(f, *args, exec="launch", round_end=2) == \
+        dpar.DPAR_ERR_INVALID_ARG
+    # reversed, negative and too long ranges (R = 4 + 1 here)
+    assert dpar.dpar_schedule_rounds(4, 4, "dual") == 5
+    assert _err(f, *args, exec="rounds", round_begin=3, round_end=2) == \
+        dpar.DPAR_ERR_INVALID_ARG
+    assert _err(f, *args, exec="rounds", round_begin=-1) == \
+        dpar.DPAR_ERR_INVALID_ARG
+    assert _err(f, *args, exec="rounds", round_end=6) == \
+        dpar.DPAR_ERR_INVALID_ARG
+    # the alias rules hold for every executor
+    bad = list(ys)
+    bad[2] = ys[1] + 16
+    assert _err(f, xs, bad, 4, 1000, "int32", "sum", 4, alg="single",
+                exec="rounds") == dpar.DPAR_ERR_ALIAS
+    assert _err(dpar.dpar_tree_info_alg, 5, 3, 0) == dpar.DPAR_ERR_INVALID_ARG
+    assert _err(dpar.dpar_schedule_rounds, 5, 0, 0) == \
+        dpar.DPAR_ERR_INVALID_ARG
+    # an empty round range is a successful no-op (no device work)
+    assert f(*args, exec="rounds", round_begin=2, round_end=2) == 0

@@ -1,0 +1,175 @@
+"""GPU parity for the one-tree algorithms (Section 1.2's single doubly-
+pipelined tree, Section 2's reduce-then-broadcast) and for the
+round-structured executors, whose per-round state is checked against the
+round in which the oracle's simulations make every block of every rank
+final (Section 1.1's induction).  Expected values come from the oracle only.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests._gpu import (POISON, assert_all_ranks_equal, env_unit, from_dev,
+                        lib, need_gpu, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+ALGS = ["dual", "single", "reduce_bcast"]
+EXECS = ["split", "ticket", "launch", "barrier", "rounds", "rounds_barrier"]
+
+
+def _trees(alg, p):
+    return oracle.build_trees(p) if alg == "dual" else \
+        oracle.build_trees(p, layout="single")
+
+
+def _want(x, dtype, op, alg):
+    return oracle.allreduce_tree(x, dtype, op, trees=_trees(alg, x.shape[0]))
+
+
+def _run(x, dtype, op, b, alg, exec, y=None, xs=None, ys=None, r0=0, r1=-1):
+    dpar = lib()
+    p, m = x.shape[0], x.shape[1]
+    xd = to_dev(x) if xs is None else None
+    if y is None:
+        y = torch.empty_like(xd)
+        y.view(torch.int32).fill_(POISON)
+    s = torch.cuda.current_stream()
+    dpar.dpar_allreduce_opt(dpar.rows(xd) if xs is None else xs,
+                            dpar.rows(y) if ys is None else ys, p, m, dtype,
+                            op, b, alg, exec, r0, r1, s)
+    dpar.dpar_check_status(s)
+    return y
+
+
+def _input(dist, seed, p, m, **kw):
+    return synth.generate(dist, seed, p, m, **kw)
+
+
+@pytest.mark.parametrize("alg", ALGS)
+@pytest.mark.parametrize("exec", EXECS)
+@pytest.mark.parametrize("unit", ["seq", "level"])
+@pytest.mark.parametrize("b", [1, 8, 64])
+def test_fp32_every_alg_and_executor(alg, exec, unit, b):
+    need_gpu()
+    x = _input("normal_f32", 2120, 36, 4099)
+    want = _want(x, "float32", "sum", alg)
+    with env_unit(unit):
+        out = from_dev(_run(x, "float32", "sum", b, alg, exec), x)
+    assert_all_ranks_equal(out, want, f"{alg}/{exec}/{unit}/b={b}")
+
+
+@pytest.mark.parametrize("alg", ALGS)
+@pytest.mark.parametrize("exec", EXECS)
+def test_matrix_product_keeps_rank_order(alg, exec):
+    need_gpu()
+    x = _input("uniform_u32_mat", 2121, 64, 1 << 10)
+    want = oracle.allreduce_ltr(x, "u32mat2x2", "matmul")
+    out = from_dev(_run(x, "u32mat2x2", "matmul", 32, alg, exec), x)
+    assert_all_ranks_equal(out, want, f"{alg}/{exec}")
+
+
+@pytest.mark.parametrize("alg", ALGS)
+@pytest.mark.parametrize("exec", ["split", "rounds", "rounds_barrier"])
+@pytest.mark.parametrize("p", [1, 2, 3, 4, 5, 7, 129])
+def test_small_and_odd_p(alg, exec, p):
+    need_gpu()
+    x = _input("normal_f32", 2122 + p, p, 1001)
+    want = _want(x, "float32", "sum", alg)
+    out = from_dev(_run(x, "float32", "sum", 3, alg, exec), x)
+    assert_all_ranks_equal(out, want, f"{alg}/{exec}/p={p}")
+
+
+@pytest.mark.parametrize("alg", ALGS)
+@pytest.mark.parametrize("exec", ["rounds", "rounds_barrier"])
+@pytest.mark.parametrize("dtype,op", [("int32", "max"), ("int32", "sum")])
+def test_rounds_in_place(alg, exec, dtype, op):
+    need_gpu()
+    x = _input("uniform_int", 2123, 36, 5000, lo=-1000, hi=1000)
+    want = _want(x, dtype, op, alg)
+    xd = to_dev(x)
+    dpar = lib()
+    s = torch.cuda.current_stream()
+    dpar.dpar_allreduce_opt(dpar.rows(xd), dpar.rows(xd), 36, 5000, dtype, op,
+                            16, alg, exec, 0, -1, s)
+    dpar.dpar_check_status(s)
+    assert_all_ranks_equal(from_dev(xd, x), want, f"in place {alg}/{exec}")
+
+
+# ---------------------------------------------------------- round structure
+
+def _final_rounds(x, b, alg):
+    """Oracle: round in which block j of rank i becomes final."""
+    t = _trees(alg, x.shape[0])
+    if alg == "reduce_bcast":
+        _, tr = oracle.simulate_reduce_bcast(x, "int32", "sum", b, trees=t)
+    else:
+        _, tr = oracle.simulate(x, "int32", "sum", b, trees=t)
+    return tr.final_round
+
+
+def _unaligned_rows(t, m):
+    """Row addresses 4 bytes into each row of a [p, m + 1] int32 tensor:
+    not 16-byte aligned, so the library takes one element per lane and the
+    canonical block partition [floor(j m / b), floor((j + 1) m / b))."""
+    return [a + 4 for a in lib().rows(t)]
+
+
+@pytest.mark.parametrize("alg", ALGS)
+@pytest.mark.parametrize("exec", ["rounds", "rounds_barrier"])
+@pytest.mark.parametrize("p,b", [(7, 4), (36, 9), (100, 3)])
+def test_state_after_every_round_prefix(alg, exec, p, b):
+    """After rounds [0, R') every rank holds exactly the blocks the oracle's
+    simulation makes final by round R' - 1, the rest still poisoned; running
+    the remaining rounds [R', R) then completes every output."""
+    need_gpu()
+    dpar = lib()
+    m = 257
+    x = _input("uniform_int", 2124, p, m, lo=-1000, hi=1000)
+    want = oracle.allreduce_tree(x, "int32", "sum", trees=_trees(alg, p))
+    final = _final_rounds(x, b, alg)
+    R = dpar.dpar_schedule_rounds(p, b, alg)
+    assert R == 1 + max(max(v.values()) for v in final.values())
+    xpad = np.zeros((p, m + 1), dtype=np.int32)
+    xpad[:, 1:] = x
+    xd = to_dev(xpad)
+    xs = _unaligned_rows(xd, m)
+    bounds = [oracle.block_bounds(m, b, j) for j in range(b)]
+    s = torch.cuda.current_stream()
+    for cut in sorted({0, 1, 2, b // 2, b, b + 1, R - 1, R}):
+        if not 0 <= cut <= R:
+            continue
+        yd = torch.full((p, m + 1), POISON, dtype=torch.int32, device="cuda")
+        ys = _unaligned_rows(yd, m)
+        dpar.dpar_allreduce_opt(xs, ys, p, m, "int32", "sum", b, alg, exec,
+                                0, cut, s)
+        dpar.dpar_check_status(s)
+        got = yd.cpu().numpy()[:, 1:]
+        for i in range(p):
+            for j, (lo, hi) in enumerate(bounds):
+                if final[i][j] < cut:
+                    assert np.array_equal(got[i, lo:hi], want[lo:hi]), \
+                        (cut, i, j, "should be final")
+                else:
+                    assert np.all(got[i, lo:hi] == POISON), \
+                        (cut, i, j, "should be untouched")
+        dpar.dpar_allreduce_opt(xs, ys, p, m, "int32", "sum", b, alg, exec,
+                                cut, -1, s)
+        dpar.dpar_check_status(s)
+        got = yd.cpu().numpy()[:, 1:]
+        assert_all_ranks_equal(got, want, f"{alg}/{exec} cut {cut}")
+
+
+@pytest.mark.parametrize("alg", ALGS)
+def test_rounds_large_p_level_unit(alg):
+    """p = 1152 at a reduced m: the level work item in the round-structured
+    executor (few chunks per round), every element checked."""
+    need_gpu()
+    x = _input("normal_f32", 2125, 1152, 1 << 12)
+    want = _want(x, "float32", "sum", alg)
+    for unit in ("level", "seq"):
+        with env_unit(unit):
+            out = from_dev(_run(x, "float32", "sum", 16, alg, "rounds"), x)
+        assert_all_ranks_equal(out, want, f"{alg}/rounds/{unit}")
