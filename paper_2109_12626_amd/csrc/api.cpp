@@ -636,12 +636,6 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     const char* u = std::getenv("DPAR_UNIT");
     if (u && !std::strcmp(u, "seq")) want = false;
     if (u && !std::strcmp(u, "level")) want = true;
-    // The grid-barrier executor keeps the post-order unit: with 1024-thread
-    // level work items its co-resident grid stalled in a barrier wait (seen
-    // once, at two workgroups per CU; the watchdog ended it) for a reason not
-    // yet established, so that combination stays switched off.
-    if (ex == dpar::Exec::GRID_BARRIER || ex == dpar::Exec::ROUNDS_BARRIER)
-      want = false;
     if (want && tmax >= 0) {
       // largest block in quanta; chunk capacity T = a power of two
       const uint64_t maxq = ((s.NL + s.b - 1) / s.b) * (uint64_t)s.lq;
@@ -661,6 +655,10 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   }
   // round-structured down-step: two ranks per wavefront per work item
   prm.dslice = 2 * (unit == dpar::Unit::LEVEL ? 16 : waves);
+  if (ex == dpar::Exec::ROUNDS &&
+      (uint64_t)prm.C * (1 + (uint64_t)((p + prm.dslice - 1) / prm.dslice)) >=
+          (1ull << 31))
+    return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items per round");
 
   // the up-phase of the split executor: one workgroup per work item handed
   // out by the hardware in round order (persistent ticketed workgroups on

@@ -478,7 +478,7 @@ __device__ inline void grid_barrier(const Params& prm) {
   __syncthreads();
   if (threadIdx.x == 0) {
     const unsigned g =
-        __hip_atomic_load(prm.bar_gen, __ATOMIC_ACQUIRE,
+        __hip_atomic_load(prm.bar_gen, __ATOMIC_RELAXED,
                           __HIP_MEMORY_SCOPE_AGENT);
     const unsigned arrived = __hip_atomic_fetch_add(
         prm.bar_count, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
@@ -490,8 +490,12 @@ __device__ inline void grid_barrier(const Params& prm) {
     } else if (__hip_atomic_load(prm.err, __ATOMIC_RELAXED,
                                  __HIP_MEMORY_SCOPE_AGENT) == 0) {
       // (once a wait has given up, later barriers of the call do not wait)
+      // Poll with relaxed loads: on this multi-XCD part an agent-scope
+      // acquire invalidates the XCD's L2, and polling with it from many
+      // workgroups would keep every L2 invalidating under the workgroups
+      // still working.  One acquire after the wait is enough.
       unsigned long long spins = 0;
-      while (__hip_atomic_load(prm.bar_gen, __ATOMIC_ACQUIRE,
+      while (__hip_atomic_load(prm.bar_gen, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT) == g) {
         __builtin_amdgcn_s_sleep(2);
         if (++spins > prm.spin_limit) {  // watchdog: give up, report
@@ -500,6 +504,7 @@ __device__ inline void grid_barrier(const Params& prm) {
         }
       }
     }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
   __syncthreads();
 }
@@ -523,15 +528,15 @@ __global__ __launch_bounds__(U::kThreads) void k_barrier(DPAR_KARGS) {
 // schedule of Algorithm 1; dshift = b - 1: the broadcast that follows a
 // completed reduction, Section 2's reduce-then-broadcast).
 
-// Down-step for ranks [i0, i1): the workgroup's wavefronts take the ranks in
-// turn; a wavefront copies the whole block, 64 lanes at a time.
+// Down-step for ranks [i0, i1), piece c of C of their blocks: the
+// workgroup's wavefronts take the ranks in turn, one quantum per lane.  A
+// piece has at most 64 quanta (the blocks' chunks hold at most 64).
 template <class L, int TH>
 __device__ __forceinline__ void down_copy(const uint64_t* __restrict__ yp,
                                           const uint32_t* __restrict__ dn,
                                           const Params& prm, int round, int i0,
-                                          int i1) {
+                                          int i1, uint64_t c) {
   constexpr int kWaves = TH / 64;
-  constexpr int kB = 4;  // loads in flight per lane
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   for (int i = i0 + wave; i < i1; i += kWaves) {
@@ -544,27 +549,19 @@ __device__ __forceinline__ void down_copy(const uint64_t* __restrict__ yp,
     const uint64_t le = prm.NL * (uint64_t)(j + 1) / (uint64_t)prm.b;
     const uint64_t qs = min(ls * prm.lq, prm.Q);
     const uint64_t qe = min(le * prm.lq, prm.Q);
-    const uint64_t base = (prm.qbase + qs) * (uint64_t)L::bytes;
-    const uint64_t src = yp[par] + base, dst = yp[i] + base;
     const uint64_t n = qe - qs;
-    for (uint64_t q0 = 0; q0 < n; q0 += 64 * kB) {
-      typename L::T v[kB];
-#pragma unroll
-      for (int k = 0; k < kB; ++k) {
-        const uint64_t q = q0 + (uint64_t)k * 64 + lane;
-        if (q < n) v[k] = L::load(src + q * L::bytes, 0);
-      }
-#pragma unroll
-      for (int k = 0; k < kB; ++k) {
-        const uint64_t q = q0 + (uint64_t)k * 64 + lane;
-        if (q < n) L::store(dst + q * L::bytes, 0, v[k]);
-      }
+    const uint64_t ps = qs + c * n / (uint64_t)prm.C;
+    const uint64_t pe = qs + (c + 1) * n / (uint64_t)prm.C;
+    if ((uint64_t)lane < pe - ps) {
+      const uint64_t off = (prm.qbase + ps + lane) * (uint64_t)L::bytes;
+      L::store(yp[i] + off, 0, L::load(yp[par] + off, 0));
     }
   }
 }
 
 // Work item `item` of round r: the first C items (r < b) are the up-step's
-// chunks of block r, the rest are down-step slices of dslice ranks.
+// chunks of block r; then, for each slice of dslice ranks, C down-step
+// pieces.
 template <class U>
 __device__ __forceinline__ void round_item(DPAR_KARGS,
                                            const uint32_t* __restrict__ dn,
@@ -574,9 +571,10 @@ __device__ __forceinline__ void round_item(DPAR_KARGS,
     U::run(xp, yp, ops, lvl, prm, (uint64_t)r * prm.C + item, lds);
     return;
   }
-  const int i0 = (int)(item - nup) * prm.dslice;
-  down_copy<typename U::Lane, U::kThreads>(yp, dn, prm, r, i0,
-                                           min(prm.p, i0 + prm.dslice));
+  const uint64_t d = item - nup;
+  const int i0 = (int)(d / (uint64_t)prm.C) * prm.dslice;
+  down_copy<typename U::Lane, U::kThreads>(
+      yp, dn, prm, r, i0, min(prm.p, i0 + prm.dslice), d % (uint64_t)prm.C);
 }
 
 template <class U>
@@ -590,18 +588,18 @@ template <class U>
 __global__ __launch_bounds__(U::kThreads) void k_rounds_barrier(
     DPAR_KARGS, const uint32_t* __restrict__ dn) {
   extern __shared__ char lds_raw[];
-  const uint64_t ndown = (uint64_t)(prm.p + prm.dslice - 1) / prm.dslice;
+  const uint64_t ndown =
+      (uint64_t)((prm.p + prm.dslice - 1) / prm.dslice) * (uint64_t)prm.C;
   for (int r = prm.r0; r < prm.r1; ++r) {
     const uint64_t items = (r < prm.b ? (uint64_t)prm.C : 0) + ndown;
     for (uint64_t it = blockIdx.x; it < items; it += gridDim.x)
       round_item<U>(xp, yp, ops, lvl, prm, dn, r, it, lds_raw);
     if (r + 1 < prm.r1) {
       // the next round reads blocks other workgroups (other XCDs, other L2s)
-      // wrote in this one: every thread releases its stores at agent scope
-      // before the barrier and acquires after it
+      // wrote in this one: every wavefront releases its stores at agent
+      // scope before the barrier; the barrier acquires for the workgroup
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
       grid_barrier(prm);
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
   }
 }
@@ -747,7 +745,8 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
                          tab.xp, tab.yp, tab.ops, tab.lvl, prm, j);
     return hipGetLastError();
   }
-  const uint64_t ndown = (uint64_t)(prm.p + prm.dslice - 1) / prm.dslice;
+  const uint64_t ndown =
+      (uint64_t)((prm.p + prm.dslice - 1) / prm.dslice) * (uint64_t)prm.C;
   if (exec == Exec::ROUNDS) {
     for (int r = prm.r0; r < prm.r1; ++r) {
       const uint64_t items = (r < prm.b ? (uint64_t)prm.C : 0) + ndown;
@@ -769,6 +768,9 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
     // every workgroup must be resident at once; leave one slot per CU free
     // rather than fill the machine to the last slot
     if (per_cu > 1) --per_cu;
+    // the round-structured rounds are short: two workgroups per CU keep the
+    // waiting (polling) workgroups few
+    if (exec == Exec::ROUNDS_BARRIER && per_cu > 2) per_cu = 2;
     uint64_t grid = (uint64_t)per_cu * num_cus;
     // more than the largest round's work items would only wait
     const uint64_t most =

@@ -38,16 +38,10 @@ def _want(x, dtype, op):
 
 # ------------------------------------------------------------ p = 7, m = 1000
 
-LEVEL_BARRIER_OFF = ("the grid-barrier executor does not use level work items "
-                     "(switched off after a barrier stall at 2 workgroups/CU)")
-
-
 @pytest.mark.parametrize("unit", UNITS)
 @pytest.mark.parametrize("exec", EXECS)
 @pytest.mark.parametrize("b", [4, 1, 2, 7, 249, 250, 251, 1000])
 def test_p7_int32_sum_every_executor_and_b(exec, b, unit):
-    if unit == "level" and exec == "barrier":
-        pytest.skip(LEVEL_BARRIER_OFF)
     w = configs.P7_SMALL
     x = workload_input(w)
     with env_unit(unit):
@@ -102,8 +96,6 @@ def test_small_p_and_m(p, m, unit):
     ("int32", "max", "uniform_int"), ("float32", "sum", "normal_f32"),
     ("u32mat2x2", "matmul", "odd_det_u32_mat")])
 def test_level_unit_all_dtypes_and_executors(exec, dtype, op, dist):
-    if exec == "barrier":
-        pytest.skip(LEVEL_BARRIER_OFF)
     p, m = 300, 1000
     kw = {"lo": -99, "hi": 99} if dist == "uniform_int" else {}
     x = synth.generate(dist, 61, p, m, **kw)

@@ -173,3 +173,17 @@ def test_rounds_large_p_level_unit(alg):
         with env_unit(unit):
             out = from_dev(_run(x, "float32", "sum", 16, alg, "rounds"), x)
         assert_all_ranks_equal(out, want, f"{alg}/rounds/{unit}")
+
+
+@pytest.mark.parametrize("alg", ALGS)
+@pytest.mark.parametrize("exec", ["rounds", "rounds_barrier", "barrier"])
+@pytest.mark.parametrize("b", [1, 2, 8])
+def test_round_executors_large_blocks(alg, exec, b):
+    """Blocks of up to 2^20 elements: thousands of work items per round and
+    a persistent grid filling every CU, with rounds in which only the
+    down-step has work."""
+    need_gpu()
+    x = _input("uniform_int", 2126, 36, 1 << 20, lo=-(1 << 20), hi=1 << 20)
+    want = _want(x, "int32", "sum", alg)
+    out = from_dev(_run(x, "int32", "sum", b, alg, exec), x)
+    assert_all_ranks_equal(out, want, f"{alg}/{exec}/b={b}")
