@@ -3,7 +3,8 @@
 Workload: p = 1152 virtual ranks (the 36 x 32 layout), m = 2^22 fp32 values
 per rank drawn N(0, 1) from a seeded generator, operator SUM, block count b
 from the sqrt(m log2 p) rule (b = 6532), the library's default executor
-(ticketed up-phase in round order, then the broadcast pass).  One step = one
+(the up-phase of every round, one workgroup per work item in round order,
+then the broadcast pass).  One step = one
 dpar_allreduce call: the tree-order reduction of all p vectors and the write
 of y to all p output buffers, inputs and outputs resident in HBM.
 
@@ -99,7 +100,8 @@ def calib_copy():
     print(json.dumps({"calib_copy_bytes": n * 4, "dispatches": 3}))
 
 
-def sweep(out_path, only=()):
+def sweep(out_path, only=(), execs=("split", "ticket", "launch", "barrier"),
+          algs=("dual",)):
     """Every workload x executor x block count, cold caches (a 512 MiB
     scratch write between calls), min and median of several calls.  Writes
     JSON lines to out_path and a table to stderr."""
@@ -113,7 +115,6 @@ def sweep(out_path, only=()):
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
     scratch = torch.empty(1 << 27, dtype=torch.float32, device=dev)
-    execs = ["split", "ticket", "launch", "barrier"]
     out = open(out_path, "w")
 
     def timed(fn, reps):
@@ -160,16 +161,19 @@ def sweep(out_path, only=()):
                 if bb not in [v for v, _ in blist]:
                     blist.append((bb, tag))
             for bb, tag in blist:
+              for alg in algs:
                 for ex in execs:
-                    slow = ex in ("launch", "barrier") and bb > 512
+                    slow = ex in ("launch", "barrier", "rounds",
+                                  "rounds_barrier") and bb > 512
                     reps = 2 if slow else 7
-                    fn = lambda: dpar.dpar_allreduce_ex(  # noqa: E731
-                        xs, ys, w.p, w.m, w.dtype, op, bb, ex, stream)
+                    fn = lambda: dpar.dpar_allreduce_opt(  # noqa: E731
+                        xs, ys, w.p, w.m, w.dtype, op, bb, alg, ex, 0, -1,
+                        stream)
                     fn()
                     dpar.dpar_check_status(stream)
                     tmin, tmed = timed(fn, reps)
                     rec = {"workload": w.name, "op": op, "b": bb, "b_kind": tag,
-                           "exec": ex, "ms_min": round(tmin, 4),
+                           "alg": alg, "exec": ex, "ms_min": round(tmin, 4),
                            "ms_median": round(tmed, 4),
                            "GB/s": round(nbytes / (tmin * 1e-3) / 1e9, 2),
                            "pct_peak": round(100 * nbytes / (tmin * 1e-3) / 1e9
@@ -178,7 +182,8 @@ def sweep(out_path, only=()):
                            "beta_ns": round(beta * 1e9, 4)}
                     out.write(json.dumps(rec) + "\n")
                     out.flush()
-                    log(f"{w.name:34s} {op:4s} b={bb:<6d} ({tag:5s}) {ex:8s} "
+                    log(f"{w.name:34s} {op:4s} b={bb:<6d} ({tag:5s}) "
+                        f"{alg:12s} {ex:14s} "
                         f"min {tmin:9.4f} ms  med {tmed:9.4f} ms  "
                         f"{rec['GB/s']:9.1f} GB/s  {rec['pct_peak']:5.1f}%")
         del xd, yd, x
@@ -197,6 +202,14 @@ def main():
                     help="measure every workload, executor and block count")
     ap.add_argument("--only", default="",
                     help="with --sweep: comma-separated workload-name parts")
+    ap.add_argument("--sweep-execs", default="split,ticket,launch,barrier",
+                    help="with --sweep: comma-separated executors")
+    ap.add_argument("--sweep-algs", default="dual",
+                    help="with --sweep: comma-separated algorithms")
+    ap.add_argument("--alg", default="dual",
+                    choices=["dual", "single", "reduce_bcast"],
+                    help="trees: dual roots (the paper's algorithm), one "
+                         "tree, or one tree with reduce then broadcast")
     ap.add_argument("--workload", default=WORKLOAD,
                     help="time another workload (name from synth.configs) "
                          "with the same protocol; the default is the headline")
@@ -204,7 +217,8 @@ def main():
     ap.add_argument("--b", type=int, default=None,
                     help="block count (default: the sqrt(m log2 p) rule)")
     ap.add_argument("--exec", default="auto",
-                    choices=["auto", "launch", "barrier", "ticket", "split"])
+                    choices=["auto", "launch", "barrier", "ticket", "split",
+                             "rounds", "rounds_barrier"])
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -215,7 +229,9 @@ def main():
         calib_copy()
         return
     if args.sweep:
-        sweep(args.sweep, [v for v in args.only.split(",") if v])
+        sweep(args.sweep, [v for v in args.only.split(",") if v],
+              [v for v in args.sweep_execs.split(",") if v],
+              [v for v in args.sweep_algs.split(",") if v])
         return
 
     import numpy as np
@@ -228,7 +244,8 @@ def main():
     w = next(v for v in configs.ALL if v.name == args.workload)
     op = args.op or w.ops[0]
     p_, m_, esz = w.p, w.m, (16 if w.dtype == "u32mat2x2" else 4)
-    headline = w.name == WORKLOAD and op == "sum" and args.b is None
+    headline = (w.name == WORKLOAD and op == "sum" and args.b is None
+                and args.alg == "dual")
     dev = torch.device("cuda:0")
     t0 = time.perf_counter()
     x_host = synth.generate(w.dist, w.seed, p_, m_, **w.dist_kw)
@@ -242,8 +259,8 @@ def main():
     stream = torch.cuda.current_stream(dev)
 
     def step():
-        dpar.dpar_allreduce_ex(xs, ys, p_, m_, w.dtype, op, b, args.exec,
-                               stream)
+        dpar.dpar_allreduce_opt(xs, ys, p_, m_, w.dtype, op, b, args.alg,
+                                args.exec, 0, -1, stream)
 
     for _ in range(args.warmup):
         step()
@@ -306,7 +323,9 @@ def main():
     # spot check: a few columns against the oracle (outside the timed region)
     import oracle
     cols = np.unique(np.array([0, 1, 2, 3, 1000, m_ // 2, m_ - 1]) % m_)
-    want = oracle.allreduce_tree(x_host[:, cols], w.dtype, op)
+    trees = (oracle.build_trees(p_) if args.alg == "dual" else
+             oracle.build_trees(p_, layout="single"))
+    want = oracle.allreduce_tree(x_host[:, cols], w.dtype, op, trees=trees)
     got = yd[:, torch.from_numpy(cols).to(dev)].cpu().numpy()
     if x_host.dtype == np.uint32:
         got = got.view(np.uint32)
@@ -338,6 +357,7 @@ def main():
                    "b": b, "block_rule": ("ceil(sqrt(m log2 p))"
                                           if args.b is None else "given"),
                    "executor": "split" if args.exec == "auto" else args.exec,
+                   "algorithm": args.alg,
                    "bytes_per_step": int(nbytes)},
         "roofline": {"bound": "hbm", "kernel": dk["kernel"],
                      "achieved": dk["GB/s"], "peak": HBM_PEAK_GBS,
