@@ -48,7 +48,10 @@ struct OpsTable {
   uint32_t* dev = nullptr;   // opcodes, padded
   uint32_t* lvl = nullptr;   // level-ordered entries + boundaries (p <= 65534)
   uint32_t* dn = nullptr;    // parent << 8 | depth of the real tree(s)
-  int height = 0;
+  uint32_t* dord = nullptr;  // depth offsets + non-root ranks by depth
+  std::vector<uint32_t> doff;  // the depth offsets, host copy
+  int height = 0;              // of the kernel form
+  int real_height = 0;         // of the real tree(s)
   int n_a = 0;
   int root_a = -1, root_b = -1;  // roots of the real tree(s)
 };
@@ -134,7 +137,8 @@ void free_ops(OpsTable& t) {
   if (t.dev) (void)hipFree(t.dev);
   if (t.lvl) (void)hipFree(t.lvl);
   if (t.dn) (void)hipFree(t.dn);
-  t.dev = t.lvl = t.dn = nullptr;
+  if (t.dord) (void)hipFree(t.dord);
+  t.dev = t.lvl = t.dn = t.dord = nullptr;
 }
 
 // Device tables for p ranks on the dual-root trees or on one tree: the
@@ -155,13 +159,18 @@ int get_ops(DeviceState* st, int p, bool single, const OpsTable** out) {
   tab.n_a = kt.n_a;
   tab.root_a = real.root_a;
   tab.root_b = real.root_b;
+  tab.real_height = real.height;
   std::vector<uint32_t> ops = dpar::make_ops(kt);
   ops.resize(ops.size() + dpar::kTablePad, 0u);  // kernels read ahead
   int rc = upload(ops, &tab.dev, "opcode table");
   if (!rc && p <= 65534) rc = upload(dpar::make_levels(kt), &tab.lvl,
                                      "level table");
-  if (!rc && p < (1 << 24) && real.height < 256)
+  if (!rc && p < (1 << 24) && real.height < 256) {
     rc = upload(dpar::make_down(real), &tab.dn, "parent table");
+    const std::vector<uint32_t> dord = dpar::make_depth_order(real);
+    if (!rc) rc = upload(dord, &tab.dord, "depth order table");
+    tab.doff.assign(dord.begin(), dord.begin() + real.height + 2);
+  }
   if (rc) {
     free_ops(tab);
     return rc;
@@ -590,6 +599,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   tab.ops = ops->dev;
   tab.lvl = ops->lvl;
   tab.dn = ops->dn;
+  tab.dord = ops->dord;
+  tab.doff_host = ops->doff.empty() ? nullptr : ops->doff.data();
 
   dpar::Exec ex = exec == DPAR_EXEC_ROUNDS           ? dpar::Exec::ROUNDS
                   : exec == DPAR_EXEC_ROUNDS_BARRIER ? dpar::Exec::ROUNDS_BARRIER
@@ -605,6 +616,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     prm.out1 = ops->root_b;
   }
   prm.dshift = alg == DPAR_ALG_REDUCE_BCAST ? b - 1 : 0;
+  prm.dheight = ops->real_height;
   prm.r0 = r0;
   prm.r1 = r1;
 
@@ -653,12 +665,17 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     if ((uint64_t)prm.b * (uint64_t)prm.C >= (1ull << 31))
       return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items");
   }
-  // round-structured down-step: two ranks per wavefront per work item
+  // round-structured down-step: two ranks per wavefront per work item, the
+  // largest block in pieces of kDownPiece quanta
   prm.dslice = 2 * (unit == dpar::Unit::LEVEL ? 16 : waves);
-  if (ex == dpar::Exec::ROUNDS &&
-      (uint64_t)prm.C * (1 + (uint64_t)((p + prm.dslice - 1) / prm.dslice)) >=
-          (1ull << 31))
-    return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items per round");
+  {
+    const uint64_t maxq = ((s.NL + s.b - 1) / s.b) * (uint64_t)s.lq;
+    const uint64_t np = (maxq + dpar::kDownPiece - 1) / dpar::kDownPiece;
+    const uint64_t slices = ((uint64_t)p + prm.dslice - 1) / prm.dslice;
+    if (rounds_exec && (uint64_t)prm.C + slices * np >= (1ull << 31))
+      return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items per round");
+    prm.npieces = (int)std::max<uint64_t>(np, 1);
+  }
 
   // the up-phase of the split executor: one workgroup per work item handed
   // out by the hardware in round order (persistent ticketed workgroups on

@@ -528,72 +528,111 @@ __global__ __launch_bounds__(U::kThreads) void k_barrier(DPAR_KARGS) {
 // schedule of Algorithm 1; dshift = b - 1: the broadcast that follows a
 // completed reduction, Section 2's reduce-then-broadcast).
 
-// Down-step for ranks [i0, i1), piece c of C of their blocks: the
-// workgroup's wavefronts take the ranks in turn, one quantum per lane.  A
-// piece has at most 64 quanta (the blocks' chunks hold at most 64).
+// Down-step for the ranks at positions [a0, a1) of the depth-ordered rank
+// table, piece k (kDownPiece quanta) of their blocks: the workgroup's
+// wavefronts take the ranks in turn; a lane copies 4 quanta, all loads in
+// flight before the stores.
 template <class L, int TH>
 __device__ __forceinline__ void down_copy(const uint64_t* __restrict__ yp,
                                           const uint32_t* __restrict__ dn,
-                                          const Params& prm, int round, int i0,
-                                          int i1, uint64_t c) {
+                                          const uint32_t* __restrict__ ranks,
+                                          const Params& prm, int round,
+                                          uint32_t a0, uint32_t a1,
+                                          uint64_t k) {
   constexpr int kWaves = TH / 64;
+  constexpr int kQ = kDownPiece / 64;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  for (int i = i0 + wave; i < i1; i += kWaves) {
+  for (uint32_t a = a0 + wave; a < a1; a += kWaves) {
+    const uint32_t i = ranks[a];
     const uint32_t e = dn[i];
     const uint32_t par = e >> 8;
-    if (par == 0xFFFFFFu) continue;  // a root: its blocks come from the up-step
     const int64_t j = (int64_t)round - (int64_t)(e & 0xFFu) - prm.dshift;
-    if (j < 0 || j >= prm.b) continue;
+    if (par == 0xFFFFFFu || j < 0 || j >= prm.b) continue;  // not in range
     const uint64_t ls = prm.NL * (uint64_t)j / (uint64_t)prm.b;
     const uint64_t le = prm.NL * (uint64_t)(j + 1) / (uint64_t)prm.b;
     const uint64_t qs = min(ls * prm.lq, prm.Q);
     const uint64_t qe = min(le * prm.lq, prm.Q);
-    const uint64_t n = qe - qs;
-    const uint64_t ps = qs + c * n / (uint64_t)prm.C;
-    const uint64_t pe = qs + (c + 1) * n / (uint64_t)prm.C;
-    if ((uint64_t)lane < pe - ps) {
-      const uint64_t off = (prm.qbase + ps + lane) * (uint64_t)L::bytes;
-      L::store(yp[i] + off, 0, L::load(yp[par] + off, 0));
+    const uint64_t ps = qs + k * kDownPiece;
+    if (ps >= qe) continue;
+    const uint64_t src = yp[par] + prm.qbase * L::bytes;
+    const uint64_t dst = yp[i] + prm.qbase * L::bytes;
+    typename L::T v[kQ];
+#pragma unroll
+    for (int u = 0; u < kQ; ++u) {
+      const uint64_t q = ps + (uint64_t)u * 64 + lane;
+      if (q < qe) v[u] = L::load(src + q * L::bytes, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < kQ; ++u) {
+      const uint64_t q = ps + (uint64_t)u * 64 + lane;
+      if (q < qe) L::store(dst + q * L::bytes, 0, v[u]);
     }
   }
 }
 
+// The ranks receiving a block in round r have depths [dlo, dhi]; their
+// positions in the depth-ordered table are [*a0, *a0 + *n).
+__host__ __device__ inline void active_ranks(const uint32_t* doff, int H,
+                                             int b, int dshift, int r,
+                                             uint32_t* a0, uint32_t* n) {
+  const int dlo = max(1, r - dshift - (b - 1));
+  const int dhi = min(H, r - dshift);
+  if (dlo > dhi) {
+    *a0 = 0;
+    *n = 0;
+    return;
+  }
+  *a0 = doff[dlo];
+  *n = doff[dhi + 1] - doff[dlo];
+}
+
 // Work item `item` of round r: the first C items (r < b) are the up-step's
-// chunks of block r; then, for each slice of dslice ranks, C down-step
-// pieces.
+// chunks of block r; then, for each slice of dslice active ranks, npieces
+// down-step pieces.
 template <class U>
 __device__ __forceinline__ void round_item(DPAR_KARGS,
                                            const uint32_t* __restrict__ dn,
-                                           int r, uint64_t item, char* lds) {
+                                           const uint32_t* __restrict__ ranks,
+                                           int r, uint32_t act0, uint32_t nact,
+                                           uint64_t item, char* lds) {
   const uint64_t nup = r < prm.b ? (uint64_t)prm.C : 0;
   if (item < nup) {
     U::run(xp, yp, ops, lvl, prm, (uint64_t)r * prm.C + item, lds);
     return;
   }
   const uint64_t d = item - nup;
-  const int i0 = (int)(d / (uint64_t)prm.C) * prm.dslice;
-  down_copy<typename U::Lane, U::kThreads>(
-      yp, dn, prm, r, i0, min(prm.p, i0 + prm.dslice), d % (uint64_t)prm.C);
+  const uint32_t a0 = act0 + (uint32_t)(d / (uint64_t)prm.npieces) * prm.dslice;
+  const uint32_t a1 = min(act0 + nact, a0 + (uint32_t)prm.dslice);
+  down_copy<typename U::Lane, U::kThreads>(yp, dn, ranks, prm, r, a0, a1,
+                                           d % (uint64_t)prm.npieces);
 }
 
 template <class U>
 __global__ __launch_bounds__(U::kThreads) void k_rounds(
-    DPAR_KARGS, const uint32_t* __restrict__ dn, int round) {
+    DPAR_KARGS, const uint32_t* __restrict__ dn,
+    const uint32_t* __restrict__ dord, int round, uint32_t act0,
+    uint32_t nact) {
   extern __shared__ char lds_raw[];
-  round_item<U>(xp, yp, ops, lvl, prm, dn, round, blockIdx.x, lds_raw);
+  round_item<U>(xp, yp, ops, lvl, prm, dn, dord + prm.dheight + 2, round,
+                act0, nact, blockIdx.x, lds_raw);
 }
 
 template <class U>
 __global__ __launch_bounds__(U::kThreads) void k_rounds_barrier(
-    DPAR_KARGS, const uint32_t* __restrict__ dn) {
+    DPAR_KARGS, const uint32_t* __restrict__ dn,
+    const uint32_t* __restrict__ dord) {
   extern __shared__ char lds_raw[];
-  const uint64_t ndown =
-      (uint64_t)((prm.p + prm.dslice - 1) / prm.dslice) * (uint64_t)prm.C;
+  const int H = prm.dheight;
   for (int r = prm.r0; r < prm.r1; ++r) {
-    const uint64_t items = (r < prm.b ? (uint64_t)prm.C : 0) + ndown;
+    uint32_t act0, nact;
+    active_ranks(dord, H, prm.b, prm.dshift, r, &act0, &nact);
+    const uint64_t items =
+        (r < prm.b ? (uint64_t)prm.C : 0) +
+        (uint64_t)((nact + prm.dslice - 1) / prm.dslice) * prm.npieces;
     for (uint64_t it = blockIdx.x; it < items; it += gridDim.x)
-      round_item<U>(xp, yp, ops, lvl, prm, dn, r, it, lds_raw);
+      round_item<U>(xp, yp, ops, lvl, prm, dn, dord + H + 2, r, act0, nact,
+                    it, lds_raw);
     if (r + 1 < prm.r1) {
       // the next round reads blocks other workgroups (other XCDs, other L2s)
       // wrote in this one: every wavefront releases its stores at agent
@@ -745,14 +784,24 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
                          tab.xp, tab.yp, tab.ops, tab.lvl, prm, j);
     return hipGetLastError();
   }
+  // down-step items of the busiest round: every non-root rank active
+  const int H = prm.dheight;
   const uint64_t ndown =
-      (uint64_t)((prm.p + prm.dslice - 1) / prm.dslice) * (uint64_t)prm.C;
+      tab.doff_host
+          ? (uint64_t)((tab.doff_host[H + 1] + prm.dslice - 1) / prm.dslice) *
+                (uint64_t)prm.npieces
+          : 0;
   if (exec == Exec::ROUNDS) {
     for (int r = prm.r0; r < prm.r1; ++r) {
-      const uint64_t items = (r < prm.b ? (uint64_t)prm.C : 0) + ndown;
+      uint32_t act0, nact;
+      active_ranks(tab.doff_host, H, prm.b, prm.dshift, r, &act0, &nact);
+      const uint64_t items =
+          (r < prm.b ? (uint64_t)prm.C : 0) +
+          (uint64_t)((nact + prm.dslice - 1) / prm.dslice) * prm.npieces;
+      if (items == 0) continue;
       hipLaunchKernelGGL((k_rounds<U>), dim3((unsigned)items), block, lds,
                          stream, tab.xp, tab.yp, tab.ops, tab.lvl, prm, tab.dn,
-                         r);
+                         tab.dord, r, act0, nact);
     }
     return hipGetLastError();
   }
@@ -781,8 +830,9 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
     const uint32_t* ops = tab.ops;
     const uint32_t* lvl = tab.lvl;
     const uint32_t* dn = tab.dn;
+    const uint32_t* dord = tab.dord;
     Params p2 = prm;
-    void* args[] = {&xp, &yp, &ops, &lvl, &p2, &dn};
+    void* args[] = {&xp, &yp, &ops, &lvl, &p2, &dn, &dord};
     return hipLaunchCooperativeKernel(kfn, dim3((unsigned)grid), block, args,
                                       (unsigned)lds, stream);
   }

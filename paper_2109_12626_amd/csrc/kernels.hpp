@@ -61,8 +61,15 @@ struct Params {
                         // (out1 < 0: none)
   int dshift;           // ROUNDS: depth-d rank receives block r - d - dshift
   int dslice;           // ROUNDS: ranks per down-step work item
+  int npieces;          // ROUNDS: down-step pieces per block (kDownPiece
+                        // quanta each)
+  int dheight;          // ROUNDS: height of the real tree(s) (the kernel
+                        // form of one tree with p <= 2 is lower)
   int r0, r1;           // ROUNDS: run rounds [r0, r1)
 };
+
+// Quanta per down-step piece: 64 lanes x 4 quanta per lane.
+constexpr int kDownPiece = 256;
 
 // Ticket counters per call (each on its own 128-byte line): work-item batch
 // k belongs to counter k % kTicketCounters, which spreads the atomics.
@@ -79,6 +86,9 @@ struct Tables {
   const uint32_t* ops;  // [p] opcodes (plan.hpp)
   const uint32_t* lvl;  // [p] level-ordered entries, then H + 2 offsets
   const uint32_t* dn;   // [p] ROUNDS: parent << 8 | depth (plan.hpp)
+  const uint32_t* dord;  // ROUNDS: H + 2 depth offsets, then the non-root
+                         // ranks by depth (plan.hpp make_depth_order)
+  const uint32_t* doff_host;  // the same offsets in host memory
 };
 
 // Enqueue one executor run over all b*C chunks of a schedule.

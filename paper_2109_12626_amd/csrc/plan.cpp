@@ -119,6 +119,18 @@ std::vector<uint32_t> make_down(const Tree& t) {
   return dn;
 }
 
+std::vector<uint32_t> make_depth_order(const Tree& t) {
+  const int H = t.height;
+  std::vector<uint32_t> out(H + 2, 0u);
+  for (int d = 1; d <= H; ++d) {
+    out[d] = (uint32_t)(out.size() - (H + 2));
+    for (int i = 0; i < t.p; ++i)
+      if (t.depth[i] == d) out.push_back((uint32_t)i);
+  }
+  out[H + 1] = (uint32_t)(out.size() - (H + 2));
+  return out;
+}
+
 int device_rounds(const Tree& real, Alg alg, int b) {
   if (alg == Alg::REDUCE_BCAST)
     return real.height > 0 ? 2 * b + real.height - 1 : b;

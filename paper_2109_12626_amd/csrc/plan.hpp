@@ -63,6 +63,13 @@ std::vector<uint32_t> make_ops(const Tree& t);
 // < 256.
 std::vector<uint32_t> make_down(const Tree& t);
 
+// Non-root ranks ordered by depth for the round-structured down-step: H + 2
+// offsets (entry d = index of the first rank at depth d; entries 0 and 1 are
+// 0), then the ranks of depth 1, depth 2, ... in ascending order.  The ranks
+// that receive a block in one round have consecutive depths, so they are one
+// index range of this table.
+std::vector<uint32_t> make_depth_order(const Tree& t);
+
 // Rounds of the round-structured device schedule (b + H, or 2b + H - 1 for
 // REDUCE_BCAST with H > 0).
 int device_rounds(const Tree& real, Alg alg, int b);
