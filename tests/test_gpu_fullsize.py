@@ -1,6 +1,7 @@
 """Full-size workloads at p = 1152, m = 2^22 (19.3 GB in, 19.3 GB out), run
 in the launch configuration the benchmark times (block count from the
-sqrt(m log2 p) rule, ticketed persistent executor).
+sqrt(m log2 p) rule, the default split executor), and with every algorithm
+and executor at that size.
 
 * Sampled columns (the first and last chunks, every column around a few
   block boundaries, and random ones) are compared with the CPU oracle for
@@ -46,9 +47,9 @@ def _run_full(w, op):
     return x, xd, yd, b
 
 
-def _check_sampled(x, yd, b, dtype, op, seed):
+def _check_sampled(x, yd, b, dtype, op, seed, trees=None):
     cols = _sample_cols(x.shape[1], b, np.random.default_rng(seed))
-    want = oracle.allreduce_tree(x[:, cols], dtype, op)
+    want = oracle.allreduce_tree(x[:, cols], dtype, op, trees=trees)
     got = yd[:, torch.from_numpy(cols).cuda()].cpu().numpy()
     for i in range(x.shape[0]):
         assert np.array_equal(got[i], want), f"rank {i}"
@@ -105,3 +106,37 @@ def test_p1152_int32_full_size(op):
         else:
             want = blk.max(0).values
         assert torch.equal(y0[c:c + step], want), f"columns from {c}"
+
+
+@pytest.fixture(scope="module")
+def fp32_full():
+    need_gpu()
+    w = configs.P1152_F32
+    x = workload_input(w)
+    xd = to_dev(x)
+    yield w, x, xd
+    del xd
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("alg", ["dual", "single", "reduce_bcast"])
+@pytest.mark.parametrize("exec", ["split", "ticket", "launch", "barrier",
+                                  "rounds", "rounds_barrier"])
+def test_p1152_fp32_every_alg_and_executor(fp32_full, alg, exec):
+    """The headline shape through every algorithm and executor at the rule's
+    b: sampled columns bit-exact against the oracle's tree(s), every rank's
+    row identical to rank 0's."""
+    from paper_2109_12626_amd import dpar
+    w, x, xd = fp32_full
+    b = oracle.block_rule_lit(w.p, w.m)
+    yd = poisoned_like(xd)
+    s = torch.cuda.current_stream()
+    dpar.dpar_allreduce_opt(dpar.rows(xd), dpar.rows(yd), w.p, w.m, w.dtype,
+                            "sum", b, alg, exec, 0, -1, s)
+    dpar.dpar_check_status(s)
+    trees = (oracle.build_trees(w.p) if alg == "dual" else
+             oracle.build_trees(w.p, layout="single"))
+    _check_sampled(x, yd, b, "float32", "sum", 3, trees=trees)
+    _check_rows_identical(yd)
+    del yd
