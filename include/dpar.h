@@ -110,7 +110,11 @@ typedef enum {
  *                     that gives up (DPAR_ERR_TIMEOUT) leaves this
  *                     executor's outputs undefined.
  * These two read each rank's block from its parent's output, so their HBM
- * traffic is about 1.5 times the others'. */
+ * traffic is about 1.5 times the others'.
+ * GRID_BARRIER and ROUNDS_BARRIER need every workgroup of their grid resident
+ * at once (a cooperative launch sized to that): do not run them while other
+ * work occupies the GPU, e.g. on a concurrent stream.  The other executors
+ * may run concurrently with anything, including other dpar calls. */
 typedef enum {
     DPAR_EXEC_AUTO = 0,
     DPAR_EXEC_LAUNCH_PER_ROUND = 1,
@@ -256,6 +260,16 @@ int dpar_set_phase_event(hipEvent_t ev);
 
 /* Text of the calling thread's last error ("" if none). */
 const char* dpar_last_error(void);
+
+/* Tuning and test knobs, read from the environment at every call; none of
+ * them changes what a call computes:
+ *   DPAR_UNIT=seq|level     force the post-order or the level work item
+ *   DPAR_WAVES=1|2          wavefronts per post-order work item
+ *   DPAR_TICKET_BATCH=k     work items claimed per ticket (TICKET)
+ *   DPAR_SPLIT_UP=ticket    SPLIT's up-phase on the ticketed persistent
+ *                           kernel instead of one launch (comparison)
+ *   DPAR_BCAST_QPT=1..16, DPAR_BCAST_ROWS=n   broadcast pass tile shape
+ *   DPAR_SPIN_LIMIT=n       grid-barrier watchdog, in polls (default 2^26) */
 
 /* Frees every library-owned device and pinned host buffer (device tables,
  * counters, staging).  The library re-creates them lazily on the next call.

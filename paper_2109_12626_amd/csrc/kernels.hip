@@ -13,11 +13,19 @@
 //   * dual-root exchange: with two wavefronts per workgroup, wavefront 0 owns
 //     tree A and wavefront 1 tree B; the two root blocks meet in LDS and both
 //     compute y = T_A (.) T_B, the lower root's value on the left;
-//   * fused broadcast: y goes from registers to all p output buffers.
+//   * write-out: y goes from registers to all p output buffers (fused), or
+//     to y_0 only, from where a broadcast pass copies it on (split), or to
+//     the roots' outputs only, from where the round-structured down-step
+//     passes it from parent to child one depth per round.
 //
-// Round sequencing: one launch per round, a persistent kernel with a grid
-// barrier per round, or a persistent kernel that claims work items from an
-// atomic ticket in round order.
+// Short chunks can instead be evaluated level by level with the chunk staged
+// in LDS (run_unit_lv).  Round sequencing: all work items in round order in
+// one launch (split: the hardware dispatcher hands them out), one launch per
+// round, a persistent kernel with a grid barrier per round, a persistent
+// kernel that claims work items from atomic tickets in round order, or the
+// full round structure including the down-phase (k_rounds,
+// k_rounds_barrier).  One tree (Sections 1.2, 2) runs through the same code
+// in a two-part form (plan.hpp kernel_single_tree).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>

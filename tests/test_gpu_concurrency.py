@@ -1,0 +1,92 @@
+"""Calls in flight on two streams at once, and from two host threads: each
+call has its own counter slot and staged pointer table, so results must not
+mix.  The persistent grid-barrier executors are left out: they need every
+workgroup of their grid resident at once and are not meant to share the GPU
+with other work."""
+
+import threading
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests._gpu import POISON, assert_all_ranks_equal, lib, need_gpu, to_dev
+
+pytestmark = pytest.mark.gpu
+
+EXECS = ["split", "ticket", "launch", "rounds"]
+
+
+def _case(seed, p, m):
+    x = synth.generate("normal_f32", seed, p, m)
+    return x, oracle.allreduce_tree(x, "float32", "sum")
+
+
+def _poisoned(xd):
+    y = torch.empty_like(xd)
+    y.view(torch.int32).fill_(POISON)
+    return y
+
+
+@pytest.mark.parametrize("e1", EXECS)
+@pytest.mark.parametrize("e2", EXECS)
+def test_two_streams_interleaved(e1, e2):
+    need_gpu()
+    dpar = lib()
+    (x1, w1), (x2, w2) = _case(2130, 36, 50001), _case(2131, 100, 20011)
+    x1d, x2d = to_dev(x1), to_dev(x2)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = []
+    torch.cuda.synchronize()
+    for it in range(3):
+        y1, y2 = _poisoned(x1d), _poisoned(x2d)
+        torch.cuda.synchronize()
+        dpar.dpar_allreduce_opt(dpar.rows(x1d), dpar.rows(y1), 36, 50001,
+                                "float32", "sum", 5 + it, "dual", e1, 0, -1, s1)
+        dpar.dpar_allreduce_opt(dpar.rows(x2d), dpar.rows(y2), 100, 20011,
+                                "float32", "sum", 7 + it, "dual", e2, 0, -1, s2)
+        outs.append((y1, y2))
+    torch.cuda.synchronize()
+    dpar.dpar_check_status(s1)
+    dpar.dpar_check_status(s2)
+    for y1, y2 in outs:
+        assert_all_ranks_equal(y1.cpu().numpy(), w1, f"stream 1 {e1}")
+        assert_all_ranks_equal(y2.cpu().numpy(), w2, f"stream 2 {e2}")
+
+
+def test_two_host_threads():
+    need_gpu()
+    dpar = lib()
+    cases = [_case(2132 + k, 20 + 17 * k, 30000 + 7 * k) for k in range(2)]
+    devs = [to_dev(x) for x, _ in cases]
+    errors = []
+
+    def work(k):
+        try:
+            s = torch.cuda.Stream()
+            x, want = cases[k]
+            p, m = x.shape
+            with torch.cuda.stream(s):
+                for it in range(4):
+                    y = _poisoned(devs[k])
+                    dpar.dpar_allreduce_opt(
+                        dpar.rows(devs[k]), dpar.rows(y), p, m, "float32",
+                        "sum", 3 + it, "dual", EXECS[(k + it) % len(EXECS)],
+                        0, -1, s)
+                    s.synchronize()
+                    got = y.cpu().numpy()
+                    for i in range(p):
+                        if not np.array_equal(got[i], want):
+                            errors.append((k, it, i))
+                            break
+        except Exception as e:  # noqa: BLE001 - reported below
+            errors.append((k, repr(e)))
+
+    ts = [threading.Thread(target=work, args=(k,)) for k in range(2)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    assert not errors, errors
