@@ -49,6 +49,8 @@ struct OpsTable {
   uint32_t* lvl = nullptr;   // level-ordered entries + boundaries (p <= 65534)
   uint32_t* dn = nullptr;    // parent << 8 | depth of the real tree(s)
   uint32_t* dord = nullptr;  // depth offsets + non-root ranks by depth
+  uint32_t* sub = nullptr;   // subtree work-item plan (null: not available)
+  int sub_ns = 0;            // its slots per wavefront
   std::vector<uint32_t> doff;  // the depth offsets, host copy
   int height = 0;              // of the kernel form
   int real_height = 0;         // of the real tree(s)
@@ -138,7 +140,8 @@ void free_ops(OpsTable& t) {
   if (t.lvl) (void)hipFree(t.lvl);
   if (t.dn) (void)hipFree(t.dn);
   if (t.dord) (void)hipFree(t.dord);
-  t.dev = t.lvl = t.dn = t.dord = nullptr;
+  if (t.sub) (void)hipFree(t.sub);
+  t.dev = t.lvl = t.dn = t.dord = t.sub = nullptr;
 }
 
 // Device tables for p ranks on the dual-root trees or on one tree: the
@@ -161,8 +164,15 @@ int get_ops(DeviceState* st, int p, bool single, const OpsTable** out) {
   tab.root_b = real.root_b;
   tab.real_height = real.height;
   std::vector<uint32_t> ops = dpar::make_ops(kt);
+  std::vector<uint32_t> sub;
+  // the subtree work item cuts each tree two levels below its root
+  const bool has_sub = p >= 64 && dpar::make_sub(kt, ops, 2, &sub);
   ops.resize(ops.size() + dpar::kTablePad, 0u);  // kernels read ahead
   int rc = upload(ops, &tab.dev, "opcode table");
+  if (!rc && has_sub) {
+    rc = upload(sub, &tab.sub, "subtree plan");
+    tab.sub_ns = (int)sub[3];
+  }
   if (!rc && p <= 65534) rc = upload(dpar::make_levels(kt), &tab.lvl,
                                      "level table");
   if (!rc && p < (1 << 24) && real.height < 256) {
@@ -665,9 +675,34 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     if ((uint64_t)prm.b * (uint64_t)prm.C >= (1ull << 31))
       return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items");
   }
+  // subtree work items (the trees cut into dpar::kSubParts subtrees, one
+  // wavefront each, then the spines): for few chunks with long rank chains
+  {
+    const char* u = std::getenv("DPAR_UNIT");
+    // measured: with the whole call in fewer than two full chunks per CU and
+    // long chains (p >= 256), eight subtree walks per chunk beat two tree
+    // walks (p = 1152, m = 2^16, b = 1: 0.113 vs 0.165 ms); with short
+    // chunks or per-round executors they do not
+    const bool whole_call = ex == dpar::Exec::SPLIT || ex == dpar::Exec::TICKET;
+    bool want_sub = whole_call && unit == dpar::Unit::SEQ && p >= 256 &&
+                    s.units() < 2ull * (uint64_t)st->num_cus &&
+                    s.Q >= 32ull * s.units();
+    if (u && *u) want_sub = !std::strcmp(u, "sub");
+    const size_t lane_bytes =
+        (path == dpar::Path::VEC16 || kind == dpar::Kind::MAT) ? 16 : 4;
+    if (want_sub && ops->sub &&
+        dpar::sub_lds_bytes(lane_bytes, ops->sub_ns) <=
+            (size_t)st->lds_limit) {
+      unit = dpar::Unit::SUB;
+      tab.lvl = ops->sub;
+      prm.nslots = ops->sub_ns;
+    }
+  }
   // round-structured down-step: two ranks per wavefront per work item, the
   // largest block in pieces of kDownPiece quanta
-  prm.dslice = 2 * (unit == dpar::Unit::LEVEL ? 16 : waves);
+  prm.dslice = 2 * (unit == dpar::Unit::LEVEL ? 16
+                    : unit == dpar::Unit::SUB ? dpar::kSubParts
+                                              : waves);
   {
     const uint64_t maxq = ((s.NL + s.b - 1) / s.b) * (uint64_t)s.lq;
     const uint64_t np = (maxq + dpar::kDownPiece - 1) / dpar::kDownPiece;

@@ -185,6 +185,66 @@ struct LaneMat4 {  // one matrix, only 4-byte aligned: four dword accesses
 constexpr int kU = DPAR_KU;
 static_assert(2 * kU <= kTablePad, "tables are padded for 2 * kU reads");
 
+// Up-step of one chunk over the ranks [r0, r1) in post-order (Algorithm 1's
+// "Y <- t (.) Y" with the first child's block, then with the second
+// child's): rank i's block is loaded, combined with its first child's value
+// (`cur`, a register) and its second child's (waiting in slot d + 1), and
+// then waits in slot d (a second child) or becomes `cur`; d is the opcode's
+// slot depth, slots are my[(d - base) * 64].  Loads run in a rotating
+// pipeline of kU: slot k of `buf` holds rank base + k; it is consumed and at
+// once refilled with rank base + kU + k.  The tables are padded by kU
+// entries, so reading kU entries ahead stays inside them; ranks past r1
+// re-read row r1 - 1 (cache hits) and are not processed.  Returns the value
+// of the last rank walked.
+template <class L>
+__device__ __forceinline__ typename L::T walk(const uint64_t* __restrict__ xp,
+                                              const uint32_t* __restrict__ ops,
+                                              int r0, int r1,
+                                              uint64_t unit_off,
+                                              uint32_t lane_off,
+                                              typename L::T* my, int base,
+                                              typename L::T& cur) {
+  using T = typename L::T;
+  T last = T{};
+  auto step = [&](T v, uint32_t op) {
+    const int d = (int)(op & OP_DEPTH_MASK) - base;
+    if (op & OP_C0) v = L::ap(cur, v);                 // first child
+    if (op & OP_C1) v = L::ap(my[(d + 1) * 64], v);    // second child
+    if (op & OP_SAVE)
+      my[d * 64] = v;
+    else
+      cur = v;
+    last = v;
+  };
+  const uint64_t last_row = xp[r1 - 1] + unit_off;
+  T buf[kU];
+#pragma unroll
+  for (int k = 0; k < kU; ++k) {
+    const uint64_t row = xp[r0 + k] + unit_off;
+    buf[k] = L::load(r0 + k < r1 ? row : last_row, lane_off);
+    // keep the loads in slot order: the wait before consuming slot k then
+    // only needs the oldest load, in the prologue and in the loop alike
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (int rb = r0; rb < r1; rb += kU) {
+    uint64_t next_row[kU];
+    uint32_t op[kU];
+#pragma unroll
+    for (int k = 0; k < kU; ++k) {
+      next_row[k] = xp[rb + kU + k] + unit_off;
+      op[k] = ops[rb + k];
+    }
+#pragma unroll
+    for (int k = 0; k < kU; ++k) {
+      const T v = buf[k];
+      buf[k] = L::load(rb + kU + k < r1 ? next_row[k] : last_row, lane_off);
+      __builtin_amdgcn_sched_barrier(0);
+      if (rb + k < r1) step(v, op[k]);
+    }
+  }
+  return last;
+}
+
 // Processes work item t (block j = t / C, chunk c = t % C).  FUSED: y goes
 // straight to all p outputs; otherwise only to y_0, from where a separate
 // broadcast pass copies it to the other p - 1 outputs.
@@ -227,47 +287,7 @@ __device__ __forceinline__ void run_unit(const uint64_t* __restrict__ xp,
   T* my = slots + (size_t)wave * prm.nslots * 64 + lane;
 
   T cur = T{};
-  auto step = [&](T v, uint32_t op) {
-    const uint32_t d = op & OP_DEPTH_MASK;
-    if (op & OP_C0) v = L::ap(cur, v);                 // first child
-    if (op & OP_C1) v = L::ap(my[(d + 1) * 64], v);    // second child
-    if (op & OP_SAVE)
-      my[d * 64] = v;
-    else
-      cur = v;
-  };
-
-  // Up-phase over ranks [r0, r1): a rotating pipeline of kU loads.  Slot k
-  // of `buf` holds rank base + k; it is consumed and at once refilled with
-  // rank base + kU + k, so kU loads stay in flight.  The tables are padded
-  // by kU entries, so reading kU entries ahead stays inside them; ranks past
-  // r1 re-read row r1 - 1 (cache hits) and are not processed.
-  const uint64_t last_row = xp[r1 - 1] + unit_off;
-  T buf[kU];
-#pragma unroll
-  for (int k = 0; k < kU; ++k) {
-    const uint64_t row = xp[r0 + k] + unit_off;
-    buf[k] = L::load(r0 + k < r1 ? row : last_row, lane_off);
-    // keep the loads in slot order: the wait before consuming slot k then
-    // only needs the oldest load, in the prologue and in the loop alike
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  for (int base = r0; base < r1; base += kU) {
-    uint64_t next_row[kU];
-    uint32_t op[kU];
-#pragma unroll
-    for (int k = 0; k < kU; ++k) {
-      next_row[k] = xp[base + kU + k] + unit_off;
-      op[k] = ops[base + k];
-    }
-#pragma unroll
-    for (int k = 0; k < kU; ++k) {
-      const T v = buf[k];
-      buf[k] = L::load(base + kU + k < r1 ? next_row[k] : last_row, lane_off);
-      __builtin_amdgcn_sched_barrier(0);
-      if (base + k < r1) step(v, op[k]);
-    }
-  }
+  walk<L>(xp, ops, r0, r1, unit_off, lane_off, my, 0, cur);
 
   // Dual-root exchange.
   T y;
@@ -431,6 +451,126 @@ __device__ __forceinline__ void run_unit_lv(const uint64_t* __restrict__ xp,
   __syncthreads();  // LDS is reused by the next work item
 }
 
+size_t sub_lds_bytes(size_t lane_bytes, int ns) {
+  return ((size_t)kSubParts * ns + kSubParts + 2 * kSubSpineRanks) * 64 *
+         lane_bytes;
+}
+
+// ------------------------------------------------------------ subtree units
+// Work item for chunks too few to keep a GPU busy when p is large: the trees
+// are cut kSubParts ways (plan.hpp make_sub), wavefront w walks part w (a
+// whole subtree, a contiguous rank range) with the post-order walk above,
+// and then wavefront 0 (tree A) and 1 (tree B) walk their spines in the same
+// post-order, taking each part's value where the part's root would come.
+// The chains are p / kSubParts loads long instead of p / 2.  Same
+// association, same operations as the post-order work item.
+//
+// LDS: slots [kSubParts][NS][64] | part values [kSubParts][64] | spine
+// blocks [2][kSubSpineRanks][64].
+template <class L, bool FUSED>
+__device__ __forceinline__ void run_unit_sub(const uint64_t* __restrict__ xp,
+                                             const uint64_t* __restrict__ yp,
+                                             const uint32_t* __restrict__ ops,
+                                             const uint32_t* __restrict__ sub,
+                                             const Params& prm, uint64_t t,
+                                             typename L::T* lds) {
+  using T = typename L::T;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+
+  // chunk -> quanta [cs, ce), as in run_unit
+  const uint64_t j = t / (uint64_t)prm.C, c = t % (uint64_t)prm.C;
+  const uint64_t ls = prm.NL * j / (uint64_t)prm.b;
+  const uint64_t le = prm.NL * (j + 1) / (uint64_t)prm.b;
+  const uint64_t nl = le - ls;
+  const uint64_t cls = ls + c * nl / (uint64_t)prm.C;
+  const uint64_t cle = ls + (c + 1) * nl / (uint64_t)prm.C;
+  const uint64_t cs = min(cls * prm.lq, prm.Q);
+  const uint64_t ce = min(cle * prm.lq, prm.Q);
+  const uint32_t count = (uint32_t)(ce - cs);
+  if (count == 0) return;  // uniform
+  const uint64_t unit_off = (prm.qbase + cs) * (uint64_t)L::bytes;
+  const uint32_t lane_off =
+      (uint32_t)(lane < (int)count ? lane : (int)count - 1) * L::bytes;
+  const bool active = lane < (int)count;
+
+  const int nparts = (int)sub[0];
+  const int NS = (int)sub[3];
+  const uint32_t* parts = sub + 4;
+  const uint32_t* sranks = parts + 3 * nparts;   // [2][kSubSpineRanks]
+  const uint32_t* spine = sranks + 2 * kSubSpineRanks;
+  T* my = lds + (size_t)wave * NS * 64 + lane;
+  T* pval = lds + (size_t)kSubParts * NS * 64;
+  T* sx = pval + (size_t)kSubParts * 64;
+
+  // the spine wavefronts start the loads of their spine ranks' blocks first
+  T pre[kSubSpineRanks];
+  if (wave < 2) {
+#pragma unroll
+    for (int k = 0; k < kSubSpineRanks; ++k)
+      pre[k] = L::load(xp[sranks[wave * kSubSpineRanks + k]] + unit_off,
+                       lane_off);
+  }
+  if (wave < nparts) {
+    const int lo = (int)parts[3 * wave], hi = (int)parts[3 * wave + 1];
+    const int base = (int)parts[3 * wave + 2];
+    T cur = T{};
+    pval[(size_t)wave * 64 + lane] =
+        walk<L>(xp, ops, lo, hi + 1, unit_off, lane_off, my, base, cur);
+  }
+  if (wave < 2) {
+#pragma unroll
+    for (int k = 0; k < kSubSpineRanks; ++k)
+      sx[(size_t)(wave * kSubSpineRanks + k) * 64 + lane] = pre[k];
+  }
+  __syncthreads();
+
+  // spines: the post-order of the top levels, parts taken from pval
+  if (wave < 2) {
+    const int n0 = (int)sub[1];
+    const int n = wave == 0 ? n0 : (int)sub[2];
+    const uint32_t* e = spine + (wave == 0 ? 0 : 2 * n0);
+    T cur = T{};
+    for (int k = 0; k < n; ++k) {
+      const uint32_t code = e[2 * k], op = e[2 * k + 1];
+      T v = (code & 0x80000000u)
+                ? pval[(size_t)(code & 0xFFFFu) * 64 + lane]
+                : sx[(size_t)(wave * kSubSpineRanks + code) * 64 + lane];
+      const int d = (int)(op & OP_DEPTH_MASK);
+      if (op & OP_C0) v = L::ap(cur, v);
+      if (op & OP_C1) v = L::ap(my[(d + 1) * 64], v);
+      if (op & OP_SAVE)
+        my[d * 64] = v;
+      else
+        cur = v;
+    }
+    if (wave == 1) my[0] = cur;  // tree B's root value; tree A's is in slot 0
+  }
+  __syncthreads();
+  const T y = L::ap(lds[lane], lds[(size_t)NS * 64 + lane]);
+
+  if (!FUSED) {
+    if (active) {
+      if (wave == 0) L::store(yp[prm.out0] + unit_off, lane_off, y);
+      if (wave == 1 && prm.out1 >= 0)
+        L::store(yp[prm.out1] + unit_off, lane_off, y);
+    }
+  } else if (active) {
+    // every wavefront writes its share of the p outputs
+    const int r0 = (int)((int64_t)prm.p * wave / kSubParts);
+    const int r1 = (int)((int64_t)prm.p * (wave + 1) / kSubParts);
+    for (int rb = r0; rb < r1; rb += kU) {
+      uint64_t row[kU];
+#pragma unroll
+      for (int k = 0; k < kU; ++k) row[k] = yp[rb + k] + unit_off;
+#pragma unroll
+      for (int k = 0; k < kU; ++k)
+        if (rb + k < r1) L::store(row[k], lane_off, y);
+    }
+  }
+  __syncthreads();  // LDS is reused by the next work item
+}
+
 // ------------------------------------------------------------ unit policies
 
 template <class L, int W, bool FUSED>
@@ -448,6 +588,23 @@ struct SeqUnit {
   }
   static size_t lds(const Params& prm) {
     return (size_t)W * prm.nslots * 64 * sizeof(typename L::T);
+  }
+};
+
+template <class L, bool FUSED>
+struct SubUnit {
+  using Lane = L;
+  static constexpr int kThreads = 64 * kSubParts;
+  __device__ static void run(const uint64_t* __restrict__ xp,
+                             const uint64_t* __restrict__ yp,
+                             const uint32_t* __restrict__ ops,
+                             const uint32_t* __restrict__ lvl,
+                             const Params& prm, uint64_t t, char* lds) {
+    run_unit_sub<L, FUSED>(xp, yp, ops, lvl, prm, t,
+                           reinterpret_cast<typename L::T*>(lds));
+  }
+  static size_t lds(const Params& prm) {
+    return sub_lds_bytes(sizeof(typename L::T), prm.nslots);
   }
 };
 
@@ -864,6 +1021,9 @@ hipError_t launch_l(Unit unit, int waves, Exec exec, const Tables& tab,
   if (unit == Unit::LEVEL)
     return fused ? launch_u<LvUnit<L, true>>(ex, tab, prm, stream, num_cus)
                  : launch_u<LvUnit<L, false>>(ex, tab, prm, stream, num_cus);
+  if (unit == Unit::SUB)
+    return fused ? launch_u<SubUnit<L, true>>(ex, tab, prm, stream, num_cus)
+                 : launch_u<SubUnit<L, false>>(ex, tab, prm, stream, num_cus);
   if (waves == 2)
     return fused
                ? launch_u<SeqUnit<L, 2, true>>(ex, tab, prm, stream, num_cus)

@@ -15,7 +15,9 @@ enum class Path : int { VEC16 = 0, SCALAR = 1 };
 // How one work item (a chunk of a block) is evaluated: a post-order walk per
 // wavefront over 16-byte lanes (SEQ) or level by level with the whole chunk
 // staged in LDS (LEVEL; short chunks, latency-bound cases).
-enum class Unit : int { SEQ = 0, LEVEL = 1 };
+// SUB: the trees cut into subtrees, one wavefront each, then the spines
+// (few chunks, large p).
+enum class Unit : int { SEQ = 0, LEVEL = 1, SUB = 2 };
 enum class Exec : int {
   LAUNCH_PER_ROUND = 1,
   GRID_BARRIER = 2,
@@ -84,7 +86,8 @@ struct Tables {
   const uint64_t* xp;   // [p] device addresses of x_i
   const uint64_t* yp;   // [p] device addresses of y_i
   const uint32_t* ops;  // [p] opcodes (plan.hpp)
-  const uint32_t* lvl;  // [p] level-ordered entries, then H + 2 offsets
+  const uint32_t* lvl;  // LEVEL: [p] level-ordered entries, then H + 2
+                        // offsets; SUB: the subtree plan (plan.hpp)
   const uint32_t* dn;   // [p] ROUNDS: parent << 8 | depth (plan.hpp)
   const uint32_t* dord;  // ROUNDS: H + 2 depth offsets, then the non-root
                          // ranks by depth (plan.hpp make_depth_order)
@@ -99,6 +102,10 @@ hipError_t launch(Kind kind, Path path, Unit unit, int waves, Exec exec,
 
 // Bytes of dynamic LDS a LEVEL work item needs.
 size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev);
+
+// Bytes of dynamic LDS a SUB work item needs with `ns` slots per wavefront
+// (lane_bytes: 16 on the vector path and for matrices, else 4).
+size_t sub_lds_bytes(size_t lane_bytes, int ns);
 
 // Broadcast pass of the split executor: copies bytes [0, nbytes) of y_0 into
 // y_1 .. y_{p-1} (16-byte lanes when vec16, else 4-byte lanes).  A workgroup

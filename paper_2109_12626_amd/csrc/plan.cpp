@@ -110,6 +110,67 @@ Tree kernel_single_tree(int p) {
   return t;
 }
 
+bool make_sub(const Tree& t, const std::vector<uint32_t>& ops, int s,
+              std::vector<uint32_t>* out) {
+  if (t.root_a < 0 || t.root_b < 0) return false;
+  std::vector<uint32_t> parts;                 // lo, hi, base
+  std::vector<uint32_t> ranks[2], entries[2];  // per tree
+  int ns = 1;
+  for (int tr = 0; tr < 2; ++tr) {
+    const int root = tr == 0 ? t.root_a : t.root_b;
+    const int d0 = t.depth[root];
+    // post-order over the top s levels: the second child's subtree (lower
+    // ranks), the first child's, then the node
+    std::vector<std::pair<int, bool>> st{{root, false}};
+    while (!st.empty()) {
+      auto [v, expanded] = st.back();
+      st.pop_back();
+      const uint32_t slot = ops[v] & OP_DEPTH_MASK;
+      if (t.depth[v] - d0 == s) {              // a part: [lo(v), v]
+        if ((int)(parts.size() / 3) >= kSubParts) return false;
+        uint32_t top = slot;
+        for (int i = t.lo[v]; i <= v; ++i)
+          top = std::max<uint32_t>(top, ops[i] & OP_DEPTH_MASK);
+        ns = std::max<int>(ns, (int)(top - slot) + 2);
+        entries[tr].push_back(0x80000000u | (uint32_t)(parts.size() / 3));
+        entries[tr].push_back(ops[v] & ~(uint32_t)(OP_C0 | OP_C1));
+        parts.push_back((uint32_t)t.lo[v]);
+        parts.push_back((uint32_t)v);
+        parts.push_back(slot);
+        continue;
+      }
+      if (expanded) {                          // a spine node
+        if ((int)ranks[tr].size() >= kSubSpineRanks) return false;
+        entries[tr].push_back((uint32_t)ranks[tr].size());
+        entries[tr].push_back(ops[v]);
+        ranks[tr].push_back((uint32_t)v);
+        ns = std::max<int>(ns, (int)slot + 2);
+        continue;
+      }
+      st.push_back({v, true});
+      if (t.child0[v] >= 0) st.push_back({t.child0[v], false});
+      if (t.child1[v] >= 0) st.push_back({t.child1[v], false});
+    }
+  }
+  if (parts.empty()) return false;
+  out->clear();
+  out->push_back((uint32_t)(parts.size() / 3));
+  out->push_back((uint32_t)(entries[0].size() / 2));
+  out->push_back((uint32_t)(entries[1].size() / 2));
+  out->push_back((uint32_t)ns);
+  out->insert(out->end(), parts.begin(), parts.end());
+  for (int tr = 0; tr < 2; ++tr) {
+    std::vector<uint32_t> r = ranks[tr];
+    const uint32_t pad = r.empty() ? (uint32_t)(tr == 0 ? t.root_a : t.root_b)
+                                   : r[0];
+    r.resize(kSubSpineRanks, pad);
+    out->insert(out->end(), r.begin(), r.end());
+  }
+  out->insert(out->end(), entries[0].begin(), entries[0].end());
+  out->insert(out->end(), entries[1].begin(), entries[1].end());
+  return true;
+}
+
 std::vector<uint32_t> make_down(const Tree& t) {
   std::vector<uint32_t> dn(t.p, 0);
   for (int i = 0; i < t.p; ++i) {

@@ -58,6 +58,25 @@ Tree kernel_single_tree(int p);
 // Opcodes for ranks 0..p-1 (uint32 each).
 std::vector<uint32_t> make_ops(const Tree& t);
 
+// Plan of the subtree work item: every tree (the two trees, or the two parts
+// of one tree) is cut at `s` levels below its root; each subtree rooted
+// there is a "part" that one wavefront walks in post-order (a contiguous
+// rank range), and one wavefront per tree then walks the spine (the nodes
+// above the parts) with the parts' values, in the same post-order.  Layout
+// (uint32):
+//   [0] nparts  [1] spine entries of tree A  [2] of tree B  [3] NS = slots
+//   per wavefront; then per part: lo, hi (its root), base (slot depth of its
+//   root); then kSubSpineRanks spine ranks of tree A and of tree B (the ranks
+//   whose own blocks the spine walk needs, padded with a valid rank); then
+//   the spine entries of A and of B, two words each: code (0x80000000 |
+//   part, or the index of the rank in the tree's spine ranks) and opcode (a
+//   part's root opcode without its child bits: the part's value already
+//   contains its children).
+constexpr int kSubParts = 8;        // wavefronts per subtree work item
+constexpr int kSubSpineRanks = 4;   // spine ranks per tree at most
+bool make_sub(const Tree& t, const std::vector<uint32_t>& ops, int s,
+              std::vector<uint32_t>* out);
+
 // Per-rank down-phase entries for the round-structured executor:
 // parent << 8 | depth, parent 0xFFFFFF for a root.  Needs p < 2^24, depth
 // < 256.

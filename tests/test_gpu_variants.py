@@ -187,3 +187,32 @@ def test_round_executors_large_blocks(alg, exec, b):
     want = _want(x, "int32", "sum", alg)
     out = from_dev(_run(x, "int32", "sum", b, alg, exec), x)
     assert_all_ranks_equal(out, want, f"{alg}/{exec}/b={b}")
+
+
+@pytest.mark.parametrize("alg", ALGS)
+@pytest.mark.parametrize("exec", EXECS)
+@pytest.mark.parametrize("p", [64, 100, 300, 1152])
+def test_subtree_unit(alg, exec, p):
+    """The subtree work item (trees cut into subtrees, one wavefront each,
+    then the spines): bit-exact fp32 for every algorithm and executor."""
+    need_gpu()
+    x = _input("normal_f32", 2127 + p, p, 2053)
+    want = _want(x, "float32", "sum", alg)
+    for b in (1, 5):
+        with env_unit("sub"):
+            out = from_dev(_run(x, "float32", "sum", b, alg, exec), x)
+        assert_all_ranks_equal(out, want, f"sub {alg}/{exec}/p={p}/b={b}")
+
+
+@pytest.mark.parametrize("dtype,op,dist", [("int32", "max", "uniform_int"),
+                                           ("u32mat2x2", "matmul",
+                                            "uniform_u32_mat")])
+def test_subtree_unit_other_operators(dtype, op, dist):
+    need_gpu()
+    kw = {"lo": -99, "hi": 99} if dist == "uniform_int" else {}
+    x = _input(dist, 2128, 200, 999, **kw)
+    want = oracle.allreduce_ltr(x, dtype, op)
+    for exec in ("split", "ticket", "rounds"):
+        with env_unit("sub"):
+            out = from_dev(_run(x, dtype, op, 3, "dual", exec), x)
+        assert_all_ranks_equal(out, want, f"sub {dtype}/{exec}")
