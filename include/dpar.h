@@ -92,7 +92,9 @@ typedef enum {
  *                     streams y_0 into the other p - 1 outputs.  HBM reads
  *                     and writes share one bus, so separating the two
  *                     directions avoids read/write turnarounds.
- *   AUTO              SPLIT.
+ *   AUTO              SPLIT; for calls moving at most 80 MB (2 p m bytes
+ *                     per element size) one launch of every work item in
+ *                     round order with the fused write-out instead.
  * The last two run the algorithm's whole round structure, down-phase
  * included (dpar_schedule_rounds gives the number of rounds R):
  *   ROUNDS            one launch per round r = 0 .. R-1.  Round r runs the
@@ -263,12 +265,14 @@ const char* dpar_last_error(void);
 
 /* Tuning and test knobs, read from the environment at every call; none of
  * them changes what a call computes:
- *   DPAR_UNIT=seq|level     force the post-order or the level work item
+ *   DPAR_UNIT=seq|level|sub force the post-order, level or subtree work
+ *                           item
  *   DPAR_WAVES=1|2          wavefronts per post-order work item
  *   DPAR_TICKET_BATCH=k     work items claimed per ticket (TICKET)
  *   DPAR_SPLIT_UP=ticket    SPLIT's up-phase on the ticketed persistent
  *                           kernel instead of one launch (comparison)
  *   DPAR_BCAST_QPT=1..16, DPAR_BCAST_ROWS=n   broadcast pass tile shape
+ *   DPAR_FUSE_BELOW_KB=n    AUTO's single-launch threshold (default 81920)
  *   DPAR_SPIN_LIMIT=n       grid-barrier watchdog, in polls (default 2^26) */
 
 /* Frees every library-owned device and pinned host buffer (device tables,

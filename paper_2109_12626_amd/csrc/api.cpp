@@ -617,6 +617,13 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
                   : exec == DPAR_EXEC_AUTO           ? dpar::Exec::SPLIT
                                                      : (dpar::Exec)exec;
   if (ex == dpar::Exec::SPLIT && p < 2) ex = dpar::Exec::DISPATCH;
+  // small calls: one launch (every work item in round order, y written to
+  // all outputs at once) instead of the up-phase and the broadcast pass;
+  // measured: 2-3 us faster up to 75 MB moved, slower at 157 MB
+  if (exec == DPAR_EXEC_AUTO &&
+      2ull * (uint64_t)p * (uint64_t)m * esz <=
+          (uint64_t)env_int("DPAR_FUSE_BELOW_KB", 80 * 1024) * 1024ull)
+    ex = dpar::Exec::DISPATCH;
   // outputs the non-fused up-step writes: y_0 for the split executor (the
   // broadcast pass copies it on), the real root(s) for the round structure
   prm.out0 = 0;
@@ -655,8 +662,14 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
                            ex == dpar::Exec::GRID_BARRIER ||
                            ex == dpar::Exec::ROUNDS ||
                            ex == dpar::Exec::ROUNDS_BARRIER;
-    bool want = (per_round ? (uint64_t)s.C : s.units()) <
-                (uint64_t)st->num_cus / 2;
+    const uint64_t items = per_round ? (uint64_t)s.C : s.units();
+    bool want = items < (uint64_t)st->num_cus / 2;
+    // few but short chunks with long chains: a post-order item costs its
+    // p/2-load chain however little it carries (p = 1152, m = 4096,
+    // b = 205: 117 us post-order)
+    if (p >= 256 && items < 2ull * (uint64_t)st->num_cus &&
+        s.Q < 32ull * (per_round ? (uint64_t)s.C * s.b : s.units()))
+      want = true;
     const char* u = std::getenv("DPAR_UNIT");
     if (u && !std::strcmp(u, "seq")) want = false;
     if (u && !std::strcmp(u, "level")) want = true;
