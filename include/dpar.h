@@ -208,6 +208,17 @@ int dpar_allreduce_opt(const void* const* x, void* const* y, int p, size_t m,
                        dpar_dtype_t dtype, dpar_op_t op, int b,
                        const dpar_options_t* opt, hipStream_t stream);
 
+/* Graph capture.  A call may be recorded into a HIP graph (stream capture)
+ * with every executor except GRID_BARRIER and ROUNDS_BARRIER (refused with
+ * DPAR_ERR_UNSUPPORTED).  Under capture a call only enqueues kernels, so an
+ * eager call with the same p, algorithm and pointer arrays must come first
+ * (it builds the device tables and stages the pointers; otherwise
+ * DPAR_ERR_UNSUPPORTED).  The staged pointer table is then held for the
+ * graph: it is never restaged, and dpar_finalize, which frees it, must wait
+ * until no graph that captured a call is replayed again.  A replay computes
+ * from the buffers' contents at replay time.  Replays of one graph, and a
+ * replay and a TICKET call, must not run concurrently. */
+
 /* Tree tables of the library's host-side tree builder (Section 1.1: two
  * post-order numbered, heap-shaped complete binary trees; tree A holds ranks
  * [0, ceil(p/2)), tree B the rest; roots ceil(p/2)-1 and p-1 are duals).

@@ -65,6 +65,7 @@ struct StageSlot {
   size_t cap = 0;             // entries
   hipEvent_t ev = nullptr;
   bool pending = false;
+  bool pinned = false;        // read by a captured graph: never restaged
   unsigned long long last_use = 0;
 };
 
@@ -250,9 +251,12 @@ int stage_pointers(DeviceState* st, const void* const* x, void* const* y,
     key[p + i] = (uint64_t)(uintptr_t)y[i];
   }
   ++st->tick;
-  StageSlot* s = &st->stage[0];
+  StageSlot* s = nullptr;
   for (auto& c : st->stage)
-    if (c.last_use < s->last_use) s = &c;
+    if (!c.pinned && (!s || c.last_use < s->last_use)) s = &c;
+  if (!s)
+    return fail(DPAR_ERR_NOMEM, "every pointer staging slot is held by a "
+                                "captured graph (dpar_finalize releases them)");
   hipError_t e;
   if (s->pending) {  // the slot's previous table may still be read
     e = hipEventSynchronize(s->ev);
@@ -544,11 +548,35 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     alias_remember(x, y, p, m * esz);
   }
   if (rounds_exec && r0 == r1) return DPAR_SUCCESS;
+  // Under stream capture (a HIP graph being recorded) a call may only
+  // enqueue kernels: the device tables and the staged pointer set must exist
+  // already (an eager call with the same arguments made them), the staging
+  // slot is pinned for the graph's lifetime, and no event is recorded.
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  {
+    hipError_t e = hipStreamIsCapturing(stream, &cap);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
+  }
+  const bool capturing = cap != hipStreamCaptureStatusNone;
+  if (capturing && (exec == DPAR_EXEC_GRID_BARRIER ||
+                    exec == DPAR_EXEC_ROUNDS_BARRIER))
+    return fail(DPAR_ERR_UNSUPPORTED,
+                "the cooperative executors cannot be captured into a graph");
+  const bool single = alg != DPAR_ALG_DUAL_ROOT;
+  if (capturing) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    auto it = g_devices.find(dev);
+    if (it == g_devices.end() ||
+        !it->second->ops.count(std::make_pair(p, single ? 1 : 0)))
+      return fail(DPAR_ERR_UNSUPPORTED,
+                  "capture: make one eager call with these arguments first");
+  }
   DeviceState* st = nullptr;
   int rc = get_state(&st);
   if (rc) return rc;
   const OpsTable* ops = nullptr;
-  const bool single = alg != DPAR_ALG_DUAL_ROOT;
   rc = get_ops(st, p, single, &ops);
   if (rc) return rc;
   if (rounds_exec && !ops->dn)
@@ -564,9 +592,13 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
 
   StageSlot* slot = nullptr;
   if (!find_staged(st, x, y, p, &slot)) {
+    if (capturing)
+      return fail(DPAR_ERR_UNSUPPORTED, "capture: make one eager call with "
+                                        "these pointer arrays first");
     rc = stage_pointers(st, x, y, p, stream, &slot);
     if (rc) return rc;
   }
+  if (capturing) slot->pinned = true;
 
   const unsigned cslot = st->next_counter++ % kCounterSlots;
   unsigned* slot_base =
@@ -767,9 +799,11 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
                         env_int("DPAR_BCAST_ROWS", 0));
     if (e != hipSuccess) return hip_fail(e, "broadcast launch");
   }
-  e = hipEventRecord(slot->ev, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-  slot->pending = true;
+  if (!capturing) {  // a pinned slot is never restaged, so never waited on
+    e = hipEventRecord(slot->ev, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    slot->pending = true;
+  }
   return DPAR_SUCCESS;
 }
 
