@@ -473,6 +473,94 @@ int dpar_block_bounds(const dpar_schedule_t* s, size_t m, int j,
 
 namespace {
 
+// The device executor for a public one.  AUTO is the split executor, or,
+// for calls moving at most DPAR_FUSE_BELOW_KB (default 80 MB), one launch of
+// every work item in round order with the fused write-out (measured: 2-3 us
+// faster up to 75 MB moved, slower at 157 MB).
+dpar::Exec device_exec(dpar_exec_t exec, int p, uint64_t bytes_moved) {
+  switch (exec) {
+    case DPAR_EXEC_LAUNCH_PER_ROUND: return dpar::Exec::LAUNCH_PER_ROUND;
+    case DPAR_EXEC_GRID_BARRIER: return dpar::Exec::GRID_BARRIER;
+    case DPAR_EXEC_TICKET: return dpar::Exec::TICKET;
+    case DPAR_EXEC_ROUNDS: return dpar::Exec::ROUNDS;
+    case DPAR_EXEC_ROUNDS_BARRIER: return dpar::Exec::ROUNDS_BARRIER;
+    case DPAR_EXEC_SPLIT:
+      return p < 2 ? dpar::Exec::DISPATCH : dpar::Exec::SPLIT;
+    default: break;
+  }
+  if (p < 2 || bytes_moved <= (uint64_t)env_int("DPAR_FUSE_BELOW_KB",
+                                                80 * 1024) * 1024ull)
+    return dpar::Exec::DISPATCH;
+  return dpar::Exec::SPLIT;
+}
+
+struct UnitChoice {
+  dpar::Unit unit = dpar::Unit::SEQ;
+  int lv_log2t = 0;  // LEVEL: log2 of the chunk capacity in quanta
+  int lv_C = 1;      // LEVEL: chunks per block
+};
+
+// How work items are evaluated (DPAR_UNIT=seq|level|sub forces one):
+//   SEQ   post-order walk, one wavefront per tree: the default;
+//   LEVEL the chunk staged in LDS, level by level: when the chunks of a round
+//         (per-round executors) or of the whole call number fewer than half
+//         a chunk per CU (measured crossover at p = 1152, m = 2^22: 249
+//         chunks per round 10.1 ms post-order vs 12.8 ms level; 110 chunks
+//         17.9 vs 15.8 ms), or for few short chunks with long chains (a
+//         post-order item costs its p/2-load chain however little it
+//         carries: p = 1152, m = 4096, b = 205: 117 us post-order, 31 level);
+//   SUB   eight subtree walks, then the spines: a whole call (split, ticket)
+//         in fewer than two full chunks per CU with p >= 256 (p = 1152,
+//         m = 2^16, b = 1: 0.113 vs 0.165 ms); not for per-round executors
+//         or short chunks, where it loses.
+UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s,
+                       dpar::Path path, dpar::Kind kind, int p,
+                       const OpsTable& ops, const DeviceState& st) {
+  UnitChoice uc;
+  const char* u = std::getenv("DPAR_UNIT");
+  const bool forced = u && *u;
+  const uint64_t cus = (uint64_t)st.num_cus;
+  const bool per_round = ex == dpar::Exec::LAUNCH_PER_ROUND ||
+                         ex == dpar::Exec::GRID_BARRIER ||
+                         ex == dpar::Exec::ROUNDS ||
+                         ex == dpar::Exec::ROUNDS_BARRIER;
+  const uint64_t items = per_round ? (uint64_t)s.C : s.units();
+  const uint64_t all_items = s.units();
+  if (ops.lvl) {
+    int tmax = -1;
+    for (int lg = 6; lg >= 0; --lg) {
+      if (dpar::level_lds_bytes(path, kind, p, lg, ops.height + 1) <=
+          (size_t)st.lds_limit) {
+        tmax = lg;
+        break;
+      }
+    }
+    bool want = items < cus / 2 ||
+                (p >= 256 && items < 2 * cus && s.Q < 32 * all_items);
+    if (forced) want = !std::strcmp(u, "level");
+    if (want && tmax >= 0) {
+      // largest block in quanta; chunk capacity T = a power of two
+      const uint64_t maxq = ((s.NL + s.b - 1) / s.b) * (uint64_t)s.lq;
+      int lg = 0;
+      while (lg < tmax && (1ull << lg) < maxq) ++lg;
+      uc.unit = dpar::Unit::LEVEL;
+      uc.lv_log2t = lg;
+      uc.lv_C = (int)((maxq + (1ull << lg) - 1) >> lg);
+      return uc;
+    }
+  }
+  const bool whole_call = ex == dpar::Exec::SPLIT || ex == dpar::Exec::TICKET;
+  bool want_sub = whole_call && p >= 256 && all_items < 2 * cus &&
+                  s.Q >= 32 * all_items;
+  if (forced) want_sub = !std::strcmp(u, "sub");
+  const size_t lane_bytes =
+      (path == dpar::Path::VEC16 || kind == dpar::Kind::MAT) ? 16 : 4;
+  if (want_sub && ops.sub &&
+      dpar::sub_lds_bytes(lane_bytes, ops.sub_ns) <= (size_t)st.lds_limit)
+    uc.unit = dpar::Unit::SUB;
+  return uc;
+}
+
 int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
                    dpar_dtype_t dtype, dpar_op_t op, int b,
                    const dpar_options_t& opt, hipStream_t stream) {
@@ -644,18 +732,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   tab.dord = ops->dord;
   tab.doff_host = ops->doff.empty() ? nullptr : ops->doff.data();
 
-  dpar::Exec ex = exec == DPAR_EXEC_ROUNDS           ? dpar::Exec::ROUNDS
-                  : exec == DPAR_EXEC_ROUNDS_BARRIER ? dpar::Exec::ROUNDS_BARRIER
-                  : exec == DPAR_EXEC_AUTO           ? dpar::Exec::SPLIT
-                                                     : (dpar::Exec)exec;
-  if (ex == dpar::Exec::SPLIT && p < 2) ex = dpar::Exec::DISPATCH;
-  // small calls: one launch (every work item in round order, y written to
-  // all outputs at once) instead of the up-phase and the broadcast pass;
-  // measured: 2-3 us faster up to 75 MB moved, slower at 157 MB
-  if (exec == DPAR_EXEC_AUTO &&
-      2ull * (uint64_t)p * (uint64_t)m * esz <=
-          (uint64_t)env_int("DPAR_FUSE_BELOW_KB", 80 * 1024) * 1024ull)
-    ex = dpar::Exec::DISPATCH;
+  const dpar::Exec ex = device_exec(exec, p, 2ull * p * m * esz);
   // outputs the non-fused up-step writes: y_0 for the split executor (the
   // broadcast pass copies it on), the real root(s) for the round structure
   prm.out0 = 0;
@@ -669,81 +746,19 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   prm.r0 = r0;
   prm.r1 = r1;
 
-  // Work-item evaluation: a post-order walk per wavefront (SEQ) unless the
-  // chunks of a round (launch per round, grid barrier) or of the whole call
-  // (ticket) are too few to keep the CUs busy, in which case each chunk is
-  // staged in LDS and evaluated level by level (LEVEL), if it fits.
-  dpar::Unit unit = dpar::Unit::SEQ;
-  int lv_log2t = 0;
-  int lv_C = 1;
+  const UnitChoice uc = choose_unit(ex, s, path, kind, p, *ops, *st);
+  const dpar::Unit unit = uc.unit;
   prm.nlev = ops->height + 1;
-  if (ops->lvl) {
-    int tmax = -1;
-    for (int lg = 6; lg >= 0; --lg) {
-      if (dpar::level_lds_bytes(path, kind, p, lg, prm.nlev) <=
-          (size_t)st->lds_limit) {
-        tmax = lg;
-        break;
-      }
-    }
-    // measured crossover, per round (the per-round executors) and over a
-    // whole call alike: level items win below ~1/2 chunk per CU (p = 1152,
-    // m = 2^22, launch per round: 249 chunks per round 10.1 ms post-order
-    // vs 12.8 ms level; 110 chunks 17.9 vs 15.8 ms)
-    const bool per_round = ex == dpar::Exec::LAUNCH_PER_ROUND ||
-                           ex == dpar::Exec::GRID_BARRIER ||
-                           ex == dpar::Exec::ROUNDS ||
-                           ex == dpar::Exec::ROUNDS_BARRIER;
-    const uint64_t items = per_round ? (uint64_t)s.C : s.units();
-    bool want = items < (uint64_t)st->num_cus / 2;
-    // few but short chunks with long chains: a post-order item costs its
-    // p/2-load chain however little it carries (p = 1152, m = 4096,
-    // b = 205: 117 us post-order)
-    if (p >= 256 && items < 2ull * (uint64_t)st->num_cus &&
-        s.Q < 32ull * (per_round ? (uint64_t)s.C * s.b : s.units()))
-      want = true;
-    const char* u = std::getenv("DPAR_UNIT");
-    if (u && !std::strcmp(u, "seq")) want = false;
-    if (u && !std::strcmp(u, "level")) want = true;
-    if (want && tmax >= 0) {
-      // largest block in quanta; chunk capacity T = a power of two
-      const uint64_t maxq = ((s.NL + s.b - 1) / s.b) * (uint64_t)s.lq;
-      int lg = 0;
-      while (lg < tmax && (1ull << lg) < maxq) ++lg;
-      lv_log2t = lg;
-      lv_C = (int)((maxq + (1ull << lg) - 1) >> lg);
-      unit = dpar::Unit::LEVEL;
-    }
-  }
   if (unit == dpar::Unit::LEVEL) {
-    prm.C = lv_C;
-    prm.lv_log2t = lv_log2t;
+    prm.C = uc.lv_C;
+    prm.lv_log2t = uc.lv_log2t;
     prm.batch = 1;
     if ((uint64_t)prm.b * (uint64_t)prm.C >= (1ull << 31))
       return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items");
   }
-  // subtree work items (the trees cut into dpar::kSubParts subtrees, one
-  // wavefront each, then the spines): for few chunks with long rank chains
-  {
-    const char* u = std::getenv("DPAR_UNIT");
-    // measured: with the whole call in fewer than two full chunks per CU and
-    // long chains (p >= 256), eight subtree walks per chunk beat two tree
-    // walks (p = 1152, m = 2^16, b = 1: 0.113 vs 0.165 ms); with short
-    // chunks or per-round executors they do not
-    const bool whole_call = ex == dpar::Exec::SPLIT || ex == dpar::Exec::TICKET;
-    bool want_sub = whole_call && unit == dpar::Unit::SEQ && p >= 256 &&
-                    s.units() < 2ull * (uint64_t)st->num_cus &&
-                    s.Q >= 32ull * s.units();
-    if (u && *u) want_sub = !std::strcmp(u, "sub");
-    const size_t lane_bytes =
-        (path == dpar::Path::VEC16 || kind == dpar::Kind::MAT) ? 16 : 4;
-    if (want_sub && ops->sub &&
-        dpar::sub_lds_bytes(lane_bytes, ops->sub_ns) <=
-            (size_t)st->lds_limit) {
-      unit = dpar::Unit::SUB;
-      tab.lvl = ops->sub;
-      prm.nslots = ops->sub_ns;
-    }
+  if (unit == dpar::Unit::SUB) {
+    tab.lvl = ops->sub;
+    prm.nslots = ops->sub_ns;
   }
   // round-structured down-step: two ranks per wavefront per work item, the
   // largest block in pieces of kDownPiece quanta
@@ -774,6 +789,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     // the elements after the last whole 16-byte quantum: one more chunk of
     // the last block, with one scalar per lane
     dpar::Params tp = prm;
+    tp.nslots = nslots;  // the post-order item's slots (SUB changed prm's)
     tp.Q = s.tail;
     tp.NL = s.tail;
     tp.lq = 1;

@@ -216,3 +216,17 @@ def test_subtree_unit_other_operators(dtype, op, dist):
         with env_unit("sub"):
             out = from_dev(_run(x, dtype, op, 3, "dual", exec), x)
         assert_all_ranks_equal(out, want, f"sub {dtype}/{exec}")
+
+
+@pytest.mark.parametrize("m", [(1 << 16) + 1, (1 << 16) + 3])
+def test_subtree_unit_chosen_with_a_tail(m):
+    """p = 1152, one block: the library picks subtree work items for the
+    chunked part; the m mod 4 trailing elements go through a separate
+    post-order pass with its own LDS slots."""
+    need_gpu()
+    x = _input("normal_f32", 2129, 1152, m)
+    want = _want(x, "float32", "sum", "dual")
+    with env_unit(None):
+        for exec in ("split", "ticket"):
+            out = from_dev(_run(x, "float32", "sum", 1, "dual", exec), x)
+            assert_all_ranks_equal(out, want, f"auto unit {exec} m={m}")
