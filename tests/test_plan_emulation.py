@@ -1,0 +1,69 @@
+"""The device work items' evaluation order, replayed symbolically on the
+CPU from the library's own host tables (tests/cpp/plan_emulation.cpp links
+the library's planner: opcodes, level table, subtree plan), must form
+exactly the product the oracle's trees define:
+S(i) = S(child1) (.) (S(child0) (.) x_i), y = S(root A) (.) S(root B) on the
+dual-root trees, y = S(p - 1) on one tree (Sections 1.1, 1.2)."""
+
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2109_12626_amd", "csrc")
+
+P_LIST = list(range(1, 130)) + [191, 255, 256, 257, 300, 511, 576, 1000,
+                                  1151, 1152]
+
+
+@pytest.fixture(scope="module")
+def emulated(tmp_path_factory):
+    gxx = shutil.which("g++")
+    if gxx is None:
+        pytest.skip("g++ not available")
+    out = tmp_path_factory.mktemp("emul") / "plan_emulation"
+    subprocess.run([gxx, "-O1", "-std=c++17", "-I", CSRC,
+                    os.path.join(ROOT, "tests", "cpp", "plan_emulation.cpp"),
+                    os.path.join(CSRC, "plan.cpp"), "-o", str(out)],
+                   check=True)
+    res = subprocess.run([str(out)], input=" ".join(map(str, P_LIST)),
+                         capture_output=True, text=True, check=True)
+    table = {}
+    for line in res.stdout.splitlines():
+        p, layout, unit, expr = line.split(" ", 3)
+        table[(int(p), layout, unit)] = expr
+    return table
+
+
+def _expr(t, i):
+    y = f"x{i}"
+    if t.child0[i] is not None:
+        y = f"({_expr(t, t.child0[i])}*{y})"
+    if t.child1[i] is not None:
+        y = f"({_expr(t, t.child1[i])}*{y})"
+    return y
+
+
+def _want(p, layout):
+    t = oracle.build_trees(p, layout=layout)
+    if len(t.roots) == 1:
+        return _expr(t, t.roots[0])
+    return f"({_expr(t, t.roots[0])}*{_expr(t, t.roots[1])})"
+
+
+@pytest.mark.parametrize("layout", ["dual", "single"])
+@pytest.mark.parametrize("p", P_LIST)
+def test_every_work_item_forms_the_oracle_product(emulated, p, layout):
+    sys.setrecursionlimit(10000)
+    want = _want(p, layout)
+    units = [u for (q, lay, u) in emulated if q == p and lay == layout]
+    assert {"seq1", "seq2", "level"} <= set(units)
+    if p >= 256:
+        assert "sub" in units  # the subtree plan exists where it is used
+    for u in units:
+        assert emulated[(p, layout, u)] == want, (p, layout, u)
