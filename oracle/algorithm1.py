@@ -76,6 +76,9 @@ class Trace:
     ops_per_round: Dict[int, Dict[int, int]] = field(default_factory=dict)
     steps_per_round: Dict[int, Dict[int, int]] = field(default_factory=dict)
     final_round: Dict[int, Dict[int, int]] = field(default_factory=dict)
+    # per rank, every exchange in order: (round, kind, partner, block sent,
+    # block received), a block index None where it is virtual
+    exchange_log: Dict[int, List[tuple]] = field(default_factory=dict)
 
     def span(self, i: int) -> int:
         r = self.active_rounds.get(i, [])
@@ -115,6 +118,11 @@ def simulate(x, dtype: str, op: str, b: int, trees=None,
         bb = blk(j)
         return None if bb is None else Y[bb[0]:bb[1]].copy()
 
+    def log(i, j, kind, partner, s_j, r_j):
+        trace.exchange_log.setdefault(i, []).append(
+            (j, kind, partner, s_j if blk(s_j) is not None else None,
+             r_j if blk(r_j) is not None else None))
+
     def program(i):
         Y = rows[i]                                    # Y <- x_i
         d = t.depth[i]
@@ -128,6 +136,7 @@ def simulate(x, dtype: str, op: str, b: int, trees=None,
                 if skip_void and blk(s_j) is None and blk(r_j) is None:
                     continue
                 got = yield _Req(c, "child", j, s_j, r_j, take(Y, s_j))
+                log(i, j, "child", c, s_j, r_j)
                 bb = blk(r_j)
                 ops = 0
                 if bb is not None:
@@ -144,6 +153,7 @@ def simulate(x, dtype: str, op: str, b: int, trees=None,
                 if skip_void and blk(j) is None:
                     continue
                 got = yield _Req(q, "dual", j, j, j, take(Y, j))
+                log(i, j, "dual", q, j, j)
                 bb = blk(j)
                 ops = 0
                 if bb is not None:
@@ -159,6 +169,7 @@ def simulate(x, dtype: str, op: str, b: int, trees=None,
                     continue
                 got = yield _Req(t.parent[i], "parent", j, s_j, r_j,
                                 take(Y, s_j))
+                log(i, j, "parent", t.parent[i], s_j, r_j)
                 bb = blk(r_j)
                 if bb is not None:
                     Y[bb[0]:bb[1]] = got

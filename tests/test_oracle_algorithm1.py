@@ -147,3 +147,22 @@ def test_block_bounds():
             assert min(sizes) >= 1
             assert block_bounds(m, b, -1) is None
             assert block_bounds(m, b, b) is None
+
+
+def test_p7_b4_rank1_exchanges():
+    """Rank 1 (depth 1, one child: rank 0, parent: rank 3) at b = 4, from
+    Algorithm 1's steps: in round j it exchanges with child0 (sends
+    Y[j - 2], receives Y[j]) and then with its parent (sends Y[j], receives
+    Y[j - 1]); blocks outside [0, 4) are virtual.  Round 2 is therefore
+    (child: send 0, receive 2), (parent: send 2, receive 1), and round 5
+    only sends Y[3] to the child."""
+    x = np.zeros((7, 8), dtype=np.int32)
+    _, tr = simulate(x, "int32", "sum", 4)
+    log = tr.exchange_log[1]
+    by_round = {}
+    for (j, kind, partner, sj, rj) in log:
+        by_round.setdefault(j, []).append((kind, partner, sj, rj))
+    assert by_round[2] == [("child", 0, 0, 2), ("parent", 3, 2, 1)]
+    assert by_round[5] == [("child", 0, 3, None)]
+    assert by_round[0] == [("child", 0, None, 0), ("parent", 3, 0, None)]
+    assert sorted(by_round) == [0, 1, 2, 3, 4, 5]

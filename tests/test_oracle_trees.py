@@ -165,3 +165,47 @@ def test_left_filled_last_level():
              for i in range(1152)]
     assert kinds.count(0) == 576 and kinds.count(1) == 2 \
         and kinds.count(2) == 574
+
+
+def _max_stack(t):
+    """Largest number of partial values alive at once between the steps of
+    a post-order stack machine (each step replaces its children's values by
+    S(i)); tree A's root value stays alive while tree B is evaluated, until
+    the dual step."""
+    best = live = 0
+    for r in t.roots:
+        # iterative post-order over the tree of root r
+        order, st = [], [(r, False)]
+        while st:
+            v, done = st.pop()
+            if done:
+                order.append(v)
+                continue
+            st.append((v, True))
+            for c in (t.child0[v], t.child1[v]):
+                if c is not None:
+                    st.append((c, False))
+        for v in order:
+            nch = sum(c is not None for c in (t.child0[v], t.child1[v]))
+            live += 1 - nch              # children's values -> S(v)
+            best = max(best, live)
+    return best
+
+
+@pytest.mark.parametrize("p,leaves,one,two,H,stack", [
+    (36, 18, 2, 16, 4, 5), (64, 32, 2, 30, 5, 6), (1152, 576, 2, 574, 9, 10)])
+def test_tree_statistics(p, leaves, one, two, H, stack):
+    t = build_trees(p)
+    nch = [sum(c is not None for c in (t.child0[i], t.child1[i]))
+           for i in range(p)]
+    assert (nch.count(0), nch.count(1), nch.count(2)) == (leaves, one, two)
+    assert t.height == H
+    assert _max_stack(t) == stack
+
+
+def test_depth2_subtree_sizes_of_576():
+    """The four depth-2 subtrees of a 576-rank heap tree, in rank order: the
+    last level is filled from the left, so the first one is the largest."""
+    t = build_trees(1152)
+    roots = sorted(i for i in range(576) if t.depth[i] == 2)
+    assert [r - t.lo[r] + 1 for r in roots] == [192, 127, 127, 127]
