@@ -633,10 +633,11 @@ struct LvUnit {
       Params prm
 
 template <class U>
-__global__ __launch_bounds__(U::kThreads) void k_round(DPAR_KARGS, int round) {
+__global__ __launch_bounds__(U::kThreads) void k_round(DPAR_KARGS, int round,
+                                                      uint64_t first) {
   extern __shared__ char lds_raw[];
-  U::run(xp, yp, ops, lvl, prm, (uint64_t)round * prm.C + blockIdx.x,
-         lds_raw);
+  U::run(xp, yp, ops, lvl, prm,
+         (uint64_t)round * prm.C + first + blockIdx.x, lds_raw);
 }
 
 __device__ inline void grid_barrier(const Params& prm) {
@@ -777,10 +778,10 @@ template <class U>
 __global__ __launch_bounds__(U::kThreads) void k_rounds(
     DPAR_KARGS, const uint32_t* __restrict__ dn,
     const uint32_t* __restrict__ dord, int round, uint32_t act0,
-    uint32_t nact) {
+    uint32_t nact, uint64_t first) {
   extern __shared__ char lds_raw[];
   round_item<U>(xp, yp, ops, lvl, prm, dn, dord + prm.dheight + 2, round,
-                act0, nact, blockIdx.x, lds_raw);
+                act0, nact, first + blockIdx.x, lds_raw);
 }
 
 template <class U>
@@ -938,15 +939,26 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
   const size_t lds = U::lds(prm);
   const dim3 block(U::kThreads);
   const uint64_t nunits = (uint64_t)prm.b * prm.C;
-  if (exec == Exec::DISPATCH) {  // work item t = blockIdx.x, all rounds
-    hipLaunchKernelGGL((k_round<U>), dim3((unsigned)nunits), block, lds,
-                       stream, tab.xp, tab.yp, tab.ops, tab.lvl, prm, 0);
+  // One workgroup per work item: a launch's total thread count must stay
+  // below 2^32, so a grid of more than kMaxGrid workgroups goes out as
+  // several launches, each given the index of its first item.
+  const uint64_t kMaxGrid = (1ull << 31) / U::kThreads;
+  if (exec == Exec::DISPATCH) {  // work item t = first + blockIdx.x
+    for (uint64_t first = 0; first < nunits; first += kMaxGrid) {
+      const uint64_t n = min(kMaxGrid, nunits - first);
+      hipLaunchKernelGGL((k_round<U>), dim3((unsigned)n), block, lds, stream,
+                         tab.xp, tab.yp, tab.ops, tab.lvl, prm, 0, first);
+    }
     return hipGetLastError();
   }
   if (exec == Exec::LAUNCH_PER_ROUND) {
     for (int j = 0; j < prm.b; ++j)
-      hipLaunchKernelGGL((k_round<U>), dim3(prm.C), block, lds, stream,
-                         tab.xp, tab.yp, tab.ops, tab.lvl, prm, j);
+      for (uint64_t first = 0; first < (uint64_t)prm.C; first += kMaxGrid) {
+        const uint64_t n = min(kMaxGrid, (uint64_t)prm.C - first);
+        hipLaunchKernelGGL((k_round<U>), dim3((unsigned)n), block, lds,
+                           stream, tab.xp, tab.yp, tab.ops, tab.lvl, prm, j,
+                           first);
+      }
     return hipGetLastError();
   }
   // down-step items of the busiest round: every non-root rank active
@@ -963,10 +975,12 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
       const uint64_t items =
           (r < prm.b ? (uint64_t)prm.C : 0) +
           (uint64_t)((nact + prm.dslice - 1) / prm.dslice) * prm.npieces;
-      if (items == 0) continue;
-      hipLaunchKernelGGL((k_rounds<U>), dim3((unsigned)items), block, lds,
-                         stream, tab.xp, tab.yp, tab.ops, tab.lvl, prm, tab.dn,
-                         tab.dord, r, act0, nact);
+      for (uint64_t first = 0; first < items; first += kMaxGrid) {
+        const uint64_t n = min(kMaxGrid, items - first);
+        hipLaunchKernelGGL((k_rounds<U>), dim3((unsigned)n), block, lds,
+                           stream, tab.xp, tab.yp, tab.ops, tab.lvl, prm,
+                           tab.dn, tab.dord, r, act0, nact, first);
+      }
     }
     return hipGetLastError();
   }

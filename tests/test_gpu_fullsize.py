@@ -140,3 +140,33 @@ def test_p1152_fp32_every_alg_and_executor(fp32_full, alg, exec):
     _check_sampled(x, yd, b, "float32", "sum", 3, trees=trees)
     _check_rows_identical(yd)
     del yd
+
+
+@pytest.mark.parametrize("exec,b", [("auto", 0), ("ticket", 0), ("rounds", 0),
+                                    ("auto", 1), ("launch", 1)])
+def test_rows_beyond_32_bit_offsets(exec, b):
+    """p = 3 rows of 2^31 + 4099 int32 (8.6 GB each, 52 GB in and out): every
+    byte offset past 2^32 goes through 64-bit address arithmetic, and the
+    rows (not 16-byte aligned) take one element per lane, so one launch of
+    all work items (split) or of one round's chunks (b = 1) would need more
+    than 2^32 threads and goes out in pieces.  Checked against the exact
+    wrapped column sum, computed on the device in int64, for every element
+    (a property that holds at any size)."""
+    from paper_2109_12626_amd import dpar
+    need_gpu()
+    p, m = 3, (1 << 31) + 4099
+    g = torch.Generator(device="cuda").manual_seed(2170)
+    xd = torch.randint(-(1 << 30), 1 << 30, (p, m), dtype=torch.int32,
+                       device="cuda", generator=g)
+    yd = poisoned_like(xd)
+    s = torch.cuda.current_stream()
+    dpar.dpar_allreduce_opt(dpar.rows(xd), dpar.rows(yd), p, m, "int32",
+                            "sum", b, "dual", exec, 0, -1, s)
+    dpar.dpar_check_status(s)
+    step = 1 << 28
+    for c in range(0, m, step):
+        want = xd[:, c:c + step].to(torch.int64).sum(0)
+        want = ((want + 2 ** 31) % 2 ** 32 - 2 ** 31).to(torch.int32)
+        for i in range(p):
+            assert torch.equal(yd[i, c:c + step], want), (exec, i, c)
+    del xd, yd
