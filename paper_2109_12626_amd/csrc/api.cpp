@@ -623,8 +623,14 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   choose_schedule(m, dtype, b, aligned16, &s, &path);
   if ((unsigned __int128)s.NL * (unsigned)(b + 1) >= ((unsigned __int128)1 << 63))
     return fail(DPAR_ERR_UNSUPPORTED, "m * b beyond the index range");
-  if (s.units() >= (1ull << 31))
-    return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items");
+  {
+    // work items = b * chunks per block, counted before the int narrowing
+    const uint64_t max_lines = (s.NL + (uint64_t)b - 1) / (uint64_t)b;
+    const uint64_t per_chunk = 64 / (uint64_t)s.lq;
+    const uint64_t c64 = (max_lines + per_chunk - 1) / per_chunk;
+    if ((unsigned __int128)c64 * (unsigned)b >= ((unsigned __int128)1 << 31))
+      return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items");
+  }
 
   std::lock_guard<std::mutex> lock(g_mu);
   // aliasing rules: checked before any device work; a pointer set that

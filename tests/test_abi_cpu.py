@@ -256,3 +256,12 @@ def test_option_errors():
         dpar.DPAR_ERR_INVALID_ARG
     # an empty round range is a successful no-op (no device work)
     assert f(*args, exec="rounds", round_begin=2, round_end=2) == 0
+
+
+def test_work_item_limit_is_checked_before_narrowing():
+    # b = 1 over 2^39 elements would need 2^31 chunks of 64 quanta: refused
+    # before any device work, whatever the int width of the chunk count
+    xs = [A, A + (1 << 41)]
+    ys = [A + (2 << 41), A + (3 << 41)]
+    assert _err(dpar.dpar_allreduce_ex, xs, ys, 2, 1 << 39, "int32", "sum", 1,
+                "split") == dpar.DPAR_ERR_UNSUPPORTED
