@@ -1,0 +1,90 @@
+"""Seeded random combinations of every call parameter, each checked bit for
+bit against the oracle: p, m, b (or the rule), dtype and operator, tree
+layout, executor, work-item kind, 16-byte or only 4-byte alignment, in-place
+or separate outputs, one tensor or separate allocations."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests._gpu import POISON, assert_all_ranks_equal, env_unit, lib, need_gpu
+
+pytestmark = pytest.mark.gpu
+
+PAIRS = [("int32", "sum", "uniform_int"), ("int32", "max", "uniform_int"),
+         ("float32", "sum", "normal_f32"),
+         ("u32mat2x2", "matmul", "uniform_u32_mat")]
+EXECS = ["auto", "split", "ticket", "launch", "barrier", "rounds",
+         "rounds_barrier"]
+ALGS = ["dual", "single", "reduce_bcast"]
+UNITS = [None, "seq", "level", "sub"]
+
+
+def _case(k):
+    r = np.random.default_rng(9000 + k)
+    p = int(r.choice([1, 2, 3, 5, 7, 16, 33, 64, 100, 257, 300]))
+    m = int(r.integers(1, 4000))
+    b = int(r.choice([0, 1, 2, 3, int(r.integers(1, m + 1))]))
+    b = min(b, m)
+    dtype, op, dist = PAIRS[int(r.integers(len(PAIRS)))]
+    return dict(p=p, m=m, b=b, dtype=dtype, op=op, dist=dist,
+                alg=ALGS[int(r.integers(3))],
+                exec=EXECS[int(r.integers(len(EXECS)))],
+                unit=UNITS[int(r.integers(len(UNITS)))],
+                misalign=bool(r.integers(2)), inplace=bool(r.integers(4) == 0),
+                separate=bool(r.integers(2)), seed=2200 + k)
+
+
+@pytest.mark.parametrize("k", range(300))
+def test_random_combination(k):
+    need_gpu()
+    dpar = lib()
+    c = _case(k)
+    p, m = c["p"], c["m"]
+    kw = {"lo": -50, "hi": 50} if c["dist"] == "uniform_int" else {}
+    x = synth.generate(c["dist"], c["seed"], p, m, **kw)
+    trees = oracle.build_trees(p) if c["alg"] == "dual" else \
+        oracle.build_trees(p, layout="single")
+    want = oracle.allreduce_tree(x, c["dtype"], c["op"], trees=trees)
+    words = 4 if c["dtype"] == "u32mat2x2" else 1     # int32 words/element
+    row = m * words + 1                                 # spare word per row
+    off = 1 if c["misalign"] else 0                     # 4-byte offset
+    xi = np.ascontiguousarray(x).view(np.int32).reshape(p, m * words)
+
+    def alloc():
+        if c["separate"]:
+            bufs = [torch.full((row + 4,), POISON, dtype=torch.int32,
+                               device="cuda") for _ in range(p)]
+            return bufs, [t.data_ptr() + 4 * off for t in bufs]
+        t = torch.full((p, row + 4), POISON, dtype=torch.int32, device="cuda")
+        return [t], [t.data_ptr() + 4 * (i * (row + 4) + off)
+                     for i in range(p)]
+
+    xb, xs = alloc()
+    for i in range(p):
+        src = torch.from_numpy(xi[i].copy()).cuda()
+        if c["separate"]:
+            xb[i][off:off + m * words] = src
+        else:
+            xb[0][i, off:off + m * words] = src
+    if c["inplace"]:
+        yb, ys = xb, xs
+    else:
+        yb, ys = alloc()
+    torch.cuda.synchronize()
+    s = torch.cuda.current_stream()
+    with env_unit(c["unit"]):
+        dpar.dpar_allreduce_opt(xs, ys, p, m, c["dtype"], c["op"], c["b"],
+                                c["alg"], c["exec"], 0, -1, s)
+    dpar.dpar_check_status(s)
+    rows = []
+    for i in range(p):
+        t = (yb[i] if c["separate"] else yb[0][i]).cpu().numpy()
+        rows.append(t[off:off + m * words])
+        # nothing written outside the m elements of each row
+        assert np.all(t[:off] == POISON) and \
+            np.all(t[off + m * words:] == POISON), (str(c), i)
+    got = np.stack(rows).view(x.dtype).reshape(x.shape)
+    assert_all_ranks_equal(got, want, str(c))
