@@ -282,7 +282,6 @@ const char* dpar_last_error(void);
  *   DPAR_TICKET_BATCH=k     work items claimed per ticket (TICKET)
  *   DPAR_SPLIT_UP=ticket    SPLIT's up-phase on the ticketed persistent
  *                           kernel instead of one launch (comparison)
- *   DPAR_BCAST_QPT=1..16, DPAR_BCAST_ROWS=n   broadcast pass tile shape
  *   DPAR_FUSE_BELOW_KB=n    AUTO's single-launch threshold (default 81920)
  *   DPAR_SPIN_LIMIT=n       grid-barrier watchdog, in polls (default 2^26) */
 

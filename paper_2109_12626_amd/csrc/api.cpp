@@ -816,9 +816,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     }
     // y_0 now holds y for the whole chunked part; stream it to y_1..y_{p-1}
     const uint64_t main_bytes = s.Q * (uint64_t)s.g * esz;
-    e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16, stream,
-                        st->num_cus, env_int("DPAR_BCAST_QPT", 0),
-                        env_int("DPAR_BCAST_ROWS", 0));
+    e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16,
+                        stream);
     if (e != hipSuccess) return hip_fail(e, "broadcast launch");
   }
   if (!capturing) {  // a pinned slot is never restaged, so never waited on

@@ -108,10 +108,10 @@ size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev);
 size_t sub_lds_bytes(size_t lane_bytes, int ns);
 
 // Broadcast pass of the split executor: copies bytes [0, nbytes) of y_0 into
-// y_1 .. y_{p-1} (16-byte lanes when vec16, else 4-byte lanes).  A workgroup
-// handles qpt * 256 lanes of one group of `rows` consecutive ranks.
+// y_1 .. y_{p-1} (16-byte lanes when vec16, else 4-byte lanes), one
+// workgroup per (row, 256-lane tile).
 hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
-                     hipStream_t stream, int num_cus, int qpt, int rows);
+                     hipStream_t stream);
 
 // Bytes of dynamic LDS a workgroup needs.
 size_t lds_bytes(Path path, Kind kind, int waves, int nslots);
