@@ -100,6 +100,35 @@ def calib_copy():
     print(json.dumps({"calib_copy_bytes": n * 4, "dispatches": 3}))
 
 
+def stream_probe():
+    """HBM stream rates of plain library kernels on 8 GiB buffers: a
+    write-only fill, a read-only reduction and a copy (each timed alone, the
+    minimum of 5), for comparison with the two phases of the reduction."""
+    import torch
+    n = 1 << 31                     # 8 GiB of fp32
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    out = {}
+
+    def rate(name, fn, nbytes):
+        ts = []
+        for _ in range(6):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        ms = min(ts[1:])
+        out[name] = {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1)}
+
+    rate("write (fill_)", lambda: b.fill_(2.0), n * 4)
+    rate("read (sum)", lambda: a.sum(), n * 4)
+    rate("copy (copy_, read + write bytes)", lambda: b.copy_(a), 2 * n * 4)
+    print(json.dumps({"stream_probe_bytes": n * 4, "rates": out}))
+
+
 def sweep(out_path, only=(), execs=("split", "ticket", "launch", "barrier"),
           algs=("dual",)):
     """Every workload x executor x block count, cold caches (a 512 MiB
@@ -198,6 +227,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true")
+    ap.add_argument("--stream-probe", action="store_true",
+                    help="HBM write / read / copy rates of plain kernels")
     ap.add_argument("--sweep", metavar="OUT_JSONL",
                     help="measure every workload, executor and block count")
     ap.add_argument("--only", default="",
@@ -227,6 +258,9 @@ def main():
         sys.exit(2)
     if args.calib_copy:
         calib_copy()
+        return
+    if args.stream_probe:
+        stream_probe()
         return
     if args.sweep:
         sweep(args.sweep, [v for v in args.only.split(",") if v],
