@@ -92,8 +92,8 @@ typedef enum {
  *                     streams y_0 into the other p - 1 outputs.  HBM reads
  *                     and writes share one bus, so separating the two
  *                     directions avoids read/write turnarounds.
- *   AUTO              SPLIT; for calls moving at most 80 MB (2 p m bytes
- *                     per element size) one launch of every work item in
+ *   AUTO              SPLIT; for calls moving at most 40 MB (2 p m times
+ *                     the element size) one launch of every work item in
  *                     round order with the fused write-out instead.
  * The last two run the algorithm's whole round structure, down-phase
  * included (dpar_schedule_rounds gives the number of rounds R):
@@ -282,7 +282,7 @@ const char* dpar_last_error(void);
  *   DPAR_TICKET_BATCH=k     work items claimed per ticket (TICKET)
  *   DPAR_SPLIT_UP=ticket    SPLIT's up-phase on the ticketed persistent
  *                           kernel instead of one launch (comparison)
- *   DPAR_FUSE_BELOW_KB=n    AUTO's single-launch threshold (default 81920)
+ *   DPAR_FUSE_BELOW_KB=n    AUTO's single-launch threshold (default 40960)
  *   DPAR_SPIN_LIMIT=n       grid-barrier watchdog, in polls (default 2^26) */
 
 /* Frees every library-owned device and pinned host buffer (device tables,

@@ -474,9 +474,10 @@ int dpar_block_bounds(const dpar_schedule_t* s, size_t m, int j,
 namespace {
 
 // The device executor for a public one.  AUTO is the split executor, or,
-// for calls moving at most DPAR_FUSE_BELOW_KB (default 80 MB), one launch of
-// every work item in round order with the fused write-out (measured: 2-3 us
-// faster up to 75 MB moved, slower at 157 MB).
+// for calls moving at most DPAR_FUSE_BELOW_KB (default 40 MB), one launch of
+// every work item in round order with the fused write-out (measured: 1-4 us
+// faster up to 40 MB moved; from ~80 MB up it can be slower, e.g. p = 300,
+// m = 2^15, b = 520: 51.7 vs 46.9 us).
 dpar::Exec device_exec(dpar_exec_t exec, int p, uint64_t bytes_moved) {
   switch (exec) {
     case DPAR_EXEC_LAUNCH_PER_ROUND: return dpar::Exec::LAUNCH_PER_ROUND;
@@ -489,7 +490,7 @@ dpar::Exec device_exec(dpar_exec_t exec, int p, uint64_t bytes_moved) {
     default: break;
   }
   if (p < 2 || bytes_moved <= (uint64_t)env_int("DPAR_FUSE_BELOW_KB",
-                                                80 * 1024) * 1024ull)
+                                                40 * 1024) * 1024ull)
     return dpar::Exec::DISPATCH;
   return dpar::Exec::SPLIT;
 }
@@ -509,8 +510,9 @@ struct UnitChoice {
 //         17.9 vs 15.8 ms), or for few short chunks with long chains (a
 //         post-order item costs its p/2-load chain however little it
 //         carries: p = 1152, m = 4096, b = 205: 117 us post-order, 31 level);
-//   SUB   eight subtree walks, then the spines: a whole call (split, ticket)
-//         in fewer than two full chunks per CU with p >= 256 (p = 1152,
+//   SUB   eight subtree walks, then the spines: a whole call (split,
+//         ticket, one fused launch) in fewer than two full chunks per CU
+//         with p >= 256 (p = 1152,
 //         m = 2^16, b = 1: 0.113 vs 0.165 ms); not for per-round executors
 //         or short chunks, where it loses.
 UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s,
@@ -549,7 +551,9 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s,
       return uc;
     }
   }
-  const bool whole_call = ex == dpar::Exec::SPLIT || ex == dpar::Exec::TICKET;
+  const bool whole_call = ex == dpar::Exec::SPLIT ||
+                          ex == dpar::Exec::TICKET ||
+                          ex == dpar::Exec::DISPATCH;
   bool want_sub = whole_call && p >= 256 && all_items < 2 * cus &&
                   s.Q >= 32 * all_items;
   if (forced) want_sub = !std::strcmp(u, "sub");
