@@ -895,8 +895,10 @@ hipError_t occupancy(const void* kfn, int threads, size_t lds, int* out) {
 
 template <class U>
 hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
-                    hipStream_t stream, int num_cus) {
-  const size_t lds = U::lds(prm);
+                    hipStream_t stream, int num_cus, size_t lds_floor) {
+  // a larger request than the work item needs only lowers the number of
+  // workgroups resident per CU (see launch())
+  const size_t lds = U::lds(prm) > lds_floor ? U::lds(prm) : lds_floor;
   const dim3 block(U::kThreads);
   const uint64_t nunits = (uint64_t)prm.b * prm.C;
   // One workgroup per work item: a launch's total thread count must stay
@@ -986,46 +988,48 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
 
 template <class L>
 hipError_t launch_l(Unit unit, int waves, Exec exec, const Tables& tab,
-                    const Params& prm, hipStream_t stream, int num_cus) {
+                    const Params& prm, hipStream_t stream, int num_cus,
+                    size_t lds_floor) {
   const bool fused = exec != Exec::TICKET_SPLIT && exec != Exec::SPLIT &&
                      exec != Exec::ROUNDS && exec != Exec::ROUNDS_BARRIER;
   const Exec ex = exec == Exec::TICKET_SPLIT ? Exec::TICKET
                   : exec == Exec::SPLIT      ? Exec::DISPATCH
                                              : exec;
+#define DPAR_LAUNCH_U(...) \
+  launch_u<__VA_ARGS__>(ex, tab, prm, stream, num_cus, lds_floor)
   if (unit == Unit::LEVEL)
-    return fused ? launch_u<LvUnit<L, true>>(ex, tab, prm, stream, num_cus)
-                 : launch_u<LvUnit<L, false>>(ex, tab, prm, stream, num_cus);
+    return fused ? DPAR_LAUNCH_U(LvUnit<L, true>)
+                 : DPAR_LAUNCH_U(LvUnit<L, false>);
   if (unit == Unit::SUB)
-    return fused ? launch_u<SubUnit<L, true>>(ex, tab, prm, stream, num_cus)
-                 : launch_u<SubUnit<L, false>>(ex, tab, prm, stream, num_cus);
+    return fused ? DPAR_LAUNCH_U(SubUnit<L, true>)
+                 : DPAR_LAUNCH_U(SubUnit<L, false>);
   if (waves == 2)
-    return fused
-               ? launch_u<SeqUnit<L, 2, true>>(ex, tab, prm, stream, num_cus)
-               : launch_u<SeqUnit<L, 2, false>>(ex, tab, prm, stream, num_cus);
-  return fused ? launch_u<SeqUnit<L, 1, true>>(ex, tab, prm, stream, num_cus)
-               : launch_u<SeqUnit<L, 1, false>>(ex, tab, prm, stream, num_cus);
+    return fused ? DPAR_LAUNCH_U(SeqUnit<L, 2, true>)
+                 : DPAR_LAUNCH_U(SeqUnit<L, 2, false>);
+  return fused ? DPAR_LAUNCH_U(SeqUnit<L, 1, true>)
+               : DPAR_LAUNCH_U(SeqUnit<L, 1, false>);
+#undef DPAR_LAUNCH_U
 }
 
 }  // namespace
 
 hipError_t launch(Kind kind, Path path, Unit unit, int waves, Exec exec,
                   const Tables& tab, const Params& prm, hipStream_t stream,
-                  int num_cus) {
+                  int num_cus, size_t lds_floor) {
   const bool vec = path == Path::VEC16;
+#define DPAR_LAUNCH_L(L) \
+  launch_l<L>(unit, waves, exec, tab, prm, stream, num_cus, lds_floor)
   switch (kind) {
     case Kind::I32_SUM:
-      return vec ? launch_l<Lane4<I32Sum>>(unit, waves, exec, tab, prm, stream, num_cus)
-                 : launch_l<Lane1<I32Sum>>(unit, waves, exec, tab, prm, stream, num_cus);
+      return vec ? DPAR_LAUNCH_L(Lane4<I32Sum>) : DPAR_LAUNCH_L(Lane1<I32Sum>);
     case Kind::I32_MAX:
-      return vec ? launch_l<Lane4<I32Max>>(unit, waves, exec, tab, prm, stream, num_cus)
-                 : launch_l<Lane1<I32Max>>(unit, waves, exec, tab, prm, stream, num_cus);
+      return vec ? DPAR_LAUNCH_L(Lane4<I32Max>) : DPAR_LAUNCH_L(Lane1<I32Max>);
     case Kind::F32_SUM:
-      return vec ? launch_l<Lane4<F32Sum>>(unit, waves, exec, tab, prm, stream, num_cus)
-                 : launch_l<Lane1<F32Sum>>(unit, waves, exec, tab, prm, stream, num_cus);
+      return vec ? DPAR_LAUNCH_L(Lane4<F32Sum>) : DPAR_LAUNCH_L(Lane1<F32Sum>);
     case Kind::MAT:
-      return vec ? launch_l<LaneMat16>(unit, waves, exec, tab, prm, stream, num_cus)
-                 : launch_l<LaneMat4>(unit, waves, exec, tab, prm, stream, num_cus);
+      return vec ? DPAR_LAUNCH_L(LaneMat16) : DPAR_LAUNCH_L(LaneMat4);
   }
+#undef DPAR_LAUNCH_L
   return hipErrorInvalidValue;
 }
 

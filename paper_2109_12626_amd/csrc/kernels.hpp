@@ -95,10 +95,12 @@ struct Tables {
 };
 
 // Enqueue one executor run over all b*C chunks of a schedule.
-// `waves` is 1 or 2 (2 needs p >= 2).  Returns the first HIP error.
+// `waves` is 1 or 2 (2 needs p >= 2).  `lds_floor`: bytes of LDS each
+// workgroup requests at least (0: what the work item needs); a larger
+// request caps the workgroups resident per CU.  Returns the first HIP error.
 hipError_t launch(Kind kind, Path path, Unit unit, int waves, Exec exec,
                   const Tables& tab, const Params& prm, hipStream_t stream,
-                  int num_cus);
+                  int num_cus, size_t lds_floor);
 
 // Bytes of dynamic LDS a LEVEL work item needs.
 size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev);
