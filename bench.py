@@ -17,6 +17,8 @@ Prints ONE JSON line.  Extra lines go to stderr.
   python bench.py --calib-copy      # a plain 4 GiB device copy, for the
                                     # rocprofv3 FETCH/WRITE calibration
   python bench.py --sweep OUT.jsonl # every workload, executor, block count
+  python bench.py --stream-probe    # plain fill / sum / copy rates
+  python bench.py --read-probe      # read rates of the up-phase's pattern
 """
 
 import argparse
@@ -129,6 +131,93 @@ def stream_probe():
     print(json.dumps({"stream_probe_bytes": n * 4, "rates": out}))
 
 
+def read_probe():
+    """HBM read rates of the up-phase's access pattern and of plain
+    contiguous reads (libdpar_probe.so, measurement kernels that read and
+    XOR), beside the library's own up-phase on the same box: 19.33 GB read
+    each time, the minimum of 5 timed launches after one untimed one."""
+    import ctypes
+
+    import torch
+
+    from paper_2109_12626_amd import build as pbuild
+    from paper_2109_12626_amd import dpar
+    if not os.path.exists(pbuild.PROBE_LIB):
+        raise RuntimeError(f"{pbuild.PROBE_LIB} is missing: run build() first")
+    lib = ctypes.CDLL(pbuild.PROBE_LIB)
+    vp, ull = ctypes.c_void_p, ctypes.c_ulonglong
+    lib.dpar_probe_rows.argtypes = [vp, ull, ctypes.c_int, ull, ctypes.c_int,
+                                    ctypes.c_int, vp, vp]
+    lib.dpar_probe_tiles.argtypes = [vp, ull, ull, vp, vp]
+    rowb, pad = M * ELEM, 4096
+    total = P * rowb
+    x = torch.ones(P * (rowb + pad) // 4, dtype=torch.float32, device="cuda")
+    sink = torch.zeros(256, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    sv = ctypes.c_void_p(stream.cuda_stream)
+    out = []
+
+    def timed(name, fn, nbytes=total):
+        ts = []
+        for _ in range(6):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            rc = fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if rc != 0:
+                raise RuntimeError(f"{name}: probe returned {rc}")
+            ts.append(e0.elapsed_time(e1))
+        ms = min(ts[1:])
+        out.append({"pattern": name, "ms": round(ms, 4),
+                    "GB/s": round(nbytes / ms / 1e6, 1)})
+        log(json.dumps(out[-1]))
+
+    def rows(p, stride, row_bytes, qpl, waves):
+        return lambda: lib.dpar_probe_rows(x.data_ptr(), stride, p, row_bytes,
+                                           qpl, waves, sink.data_ptr(), sv)
+
+    for qpl, waves in ((1, 2), (2, 2), (4, 2), (1, 8)):
+        timed(f"rows p=1152 x 16 MB, {qpl} KB per row visit, {waves} "
+              "wavefronts per workgroup", rows(P, rowb, rowb, qpl, waves))
+    for waves in (2, 8):
+        timed(f"rows p=1152 x 16 MB, rows 16 MB + 4 KB apart, 1 KB per row "
+              f"visit, {waves} wavefronts", rows(P, rowb + pad, rowb, 1, waves))
+    for p in (18, 36, 144, 576, 4608, 9216):
+        rb = total // p
+        timed(f"rows p={p} x {rb >> 20} MB, 1 KB per row visit, 8 wavefronts",
+              rows(p, rb, rb, 1, 8))
+    for mul in (1, 5, 65537, 1000003):
+        timed(f"16 KB tiles, one short workgroup each, tile order g * {mul} "
+              "mod tiles", lambda: lib.dpar_probe_tiles(
+                  x.data_ptr(), total, mul, sink.data_ptr(), sv))
+
+    # the library's up-phase on the same shape (inputs all 1.0: the values
+    # do not change the time), y_0's write included in the bytes
+    y = torch.empty(P * rowb // 4, dtype=torch.float32, device="cuda")
+    xs = dpar.pointers([x.data_ptr() + i * rowb for i in range(P)])
+    ys = dpar.pointers([y.data_ptr() + i * rowb for i in range(P)])
+    b = dpar.dpar_block_rule(P, M)
+    ups = []
+    for _ in range(6):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        dpar.dpar_set_phase_event(e1)
+        dpar.dpar_allreduce(xs, ys, P, M, "float32", "sum", b, stream)
+        torch.cuda.synchronize()
+        ups.append(e0.elapsed_time(e1))
+    dpar.dpar_check_status(stream)
+    ms = min(ups[1:])
+    out.append({"pattern": f"the library's up-phase (split executor, b={b})",
+                "ms": round(ms, 4), "GB/s": round((total + rowb) / ms / 1e6, 1)})
+    log(json.dumps(out[-1]))
+    print(json.dumps({"read_probe_bytes": total, "rates": out}))
+
+
 def sweep(out_path, only=(), execs=("split", "ticket", "launch", "barrier"),
           algs=("dual",)):
     """Every workload x executor x block count, cold caches (a 512 MiB
@@ -229,6 +318,8 @@ def main():
     ap.add_argument("--calib-copy", action="store_true")
     ap.add_argument("--stream-probe", action="store_true",
                     help="HBM write / read / copy rates of plain kernels")
+    ap.add_argument("--read-probe", action="store_true",
+                    help="HBM read rates of the up-phase's access pattern")
     ap.add_argument("--sweep", metavar="OUT_JSONL",
                     help="measure every workload, executor and block count")
     ap.add_argument("--only", default="",
@@ -261,6 +352,9 @@ def main():
         return
     if args.stream_probe:
         stream_probe()
+        return
+    if args.read_probe:
+        read_probe()
         return
     if args.sweep:
         sweep(args.sweep, [v for v in args.only.split(",") if v],

@@ -283,6 +283,10 @@ const char* dpar_last_error(void);
  *   DPAR_SPLIT_UP=ticket    SPLIT's up-phase on the ticketed persistent
  *                           kernel instead of one launch (comparison)
  *   DPAR_FUSE_BELOW_KB=n    AUTO's single-launch threshold (default 40960)
+ *   DPAR_GROUP_BLOCKS=0     one-launch executors (SPLIT, TICKET, AUTO):
+ *                           one work item per block even when blocks are
+ *                           shorter than half a chunk (default 1: groups of
+ *                           consecutive whole blocks)
  *   DPAR_SEQ_WG_PER_CU=n    SPLIT's post-order up-phase at p >= 256 with
  *                           at least 64 work items per CU: workgroups
  *                           resident per CU (default 4; 0 = as many as fit)

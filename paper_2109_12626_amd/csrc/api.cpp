@@ -506,6 +506,26 @@ dpar::Exec device_exec(dpar_exec_t exec, int p, uint64_t bytes_moved) {
   return dpar::Exec::SPLIT;
 }
 
+// Work items of a one-launch run with groups of grp consecutive blocks.
+uint64_t grouped_units(const dpar::Schedule& s, int grp) {
+  return (((uint64_t)s.b + (uint64_t)grp - 1) / (uint64_t)grp) *
+         (uint64_t)s.C;
+}
+
+// Blocks per work-item group.  The one-launch executors (split, ticket, one
+// fused launch) issue the rounds' work items in round order from one
+// launch, so a work item may carry several consecutive whole blocks: blocks
+// shorter than half a chunk are grouped (plan.hpp block_group), else a
+// wavefront of 64 lanes would carry as few as a handful of quanta.
+// Per-round executors: 1.
+int block_group(dpar::Exec ex, const dpar::Schedule& s) {
+  const bool one_launch = ex == dpar::Exec::SPLIT ||
+                          ex == dpar::Exec::DISPATCH ||
+                          ex == dpar::Exec::TICKET;
+  if (!one_launch || env_int("DPAR_GROUP_BLOCKS", 1) == 0) return 1;
+  return dpar::block_group(s);
+}
+
 struct UnitChoice {
   dpar::Unit unit = dpar::Unit::SEQ;
   int lv_log2t = 0;  // LEVEL: log2 of the chunk capacity in quanta
@@ -526,7 +546,7 @@ struct UnitChoice {
 //         with p >= 256 (p = 1152,
 //         m = 2^16, b = 1: 0.113 vs 0.165 ms); not for per-round executors
 //         or short chunks, where it loses.
-UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s,
+UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
                        dpar::Path path, dpar::Kind kind, int p,
                        const OpsTable& ops, const DeviceState& st) {
   UnitChoice uc;
@@ -537,8 +557,8 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s,
                          ex == dpar::Exec::GRID_BARRIER ||
                          ex == dpar::Exec::ROUNDS ||
                          ex == dpar::Exec::ROUNDS_BARRIER;
-  const uint64_t items = per_round ? (uint64_t)s.C : s.units();
-  const uint64_t all_items = s.units();
+  const uint64_t all_items = grouped_units(s, grp);
+  const uint64_t items = per_round ? (uint64_t)s.C : all_items;
   if (ops.lvl) {
     int tmax = -1;
     for (int lg = 6; lg >= 0; --lg) {
@@ -552,8 +572,10 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s,
                 (p >= 256 && items < 2 * cus && s.Q < 32 * all_items);
     if (forced) want = !std::strcmp(u, "level");
     if (want && tmax >= 0) {
-      // largest block in quanta; chunk capacity T = a power of two
-      const uint64_t maxq = ((s.NL + s.b - 1) / s.b) * (uint64_t)s.lq;
+      // largest block (group of grp blocks) in quanta; chunk capacity T =
+      // a power of two
+      const uint64_t maxq =
+          ((s.NL * (uint64_t)grp + s.b - 1) / s.b) * (uint64_t)s.lq;
       int lg = 0;
       while (lg < tmax && (1ull << lg) < maxq) ++lg;
       uc.unit = dpar::Unit::LEVEL;
@@ -725,10 +747,13 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   prm.qbase = 0;
   prm.b = s.b;
   prm.C = s.C;
+  prm.grp = 1;
   // short work items (few ranks) are claimed several at a time, so that the
   // ticket counter is not the bottleneck; at most 1/2 of a fair share
+  const dpar::Exec ex = device_exec(exec, p, 2ull * p * m * esz);
+  prm.grp = block_group(ex, s);
   {
-    const uint64_t units = s.units();
+    const uint64_t units = grouped_units(s, prm.grp);
     uint64_t k = (512 + (uint64_t)p - 1) / (uint64_t)p;
     const uint64_t fair = units / (2ull * 4 * (uint64_t)st->num_cus);
     if (k > fair) k = fair;
@@ -753,7 +778,6 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   tab.dord = ops->dord;
   tab.doff_host = ops->doff.empty() ? nullptr : ops->doff.data();
 
-  const dpar::Exec ex = device_exec(exec, p, 2ull * p * m * esz);
   // outputs the non-fused up-step writes: y_0 for the split executor (the
   // broadcast pass copies it on), the real root(s) for the round structure
   prm.out0 = 0;
@@ -767,14 +791,15 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   prm.r0 = r0;
   prm.r1 = r1;
 
-  const UnitChoice uc = choose_unit(ex, s, path, kind, p, *ops, *st);
+  const UnitChoice uc = choose_unit(ex, s, prm.grp, path, kind, p, *ops, *st);
   const dpar::Unit unit = uc.unit;
   prm.nlev = ops->height + 1;
   if (unit == dpar::Unit::LEVEL) {
     prm.C = uc.lv_C;
     prm.lv_log2t = uc.lv_log2t;
     prm.batch = 1;
-    if ((uint64_t)prm.b * (uint64_t)prm.C >= (1ull << 31))
+    if (grouped_units(s, prm.grp) / (uint64_t)s.C * (uint64_t)prm.C >=
+        (1ull << 31))
       return fail(DPAR_ERR_UNSUPPORTED, "more than 2^31 work items");
   }
   if (unit == dpar::Unit::SUB) {
@@ -810,7 +835,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   size_t lds_floor = 0;
   if (up == dpar::Exec::SPLIT && unit == dpar::Unit::SEQ &&
       p >= kCapMinRanks &&
-      s.units() >= (uint64_t)kCapMinItemsPerCu * (uint64_t)st->num_cus) {
+      grouped_units(s, prm.grp) >=
+          (uint64_t)kCapMinItemsPerCu * (uint64_t)st->num_cus) {
     const int per_cu = env_int("DPAR_SEQ_WG_PER_CU", kSeqWgPerCu);
     if (per_cu > 0)
       lds_floor = (size_t)st->lds_per_cu / (size_t)(per_cu + 1) + 1024;
@@ -830,6 +856,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     tp.qbase = s.Q * (uint64_t)s.g;
     tp.b = 1;
     tp.C = 1;
+    tp.grp = 1;
     tp.batch = 1;
     e = dpar::launch(kind, dpar::Path::SCALAR, dpar::Unit::SEQ, waves,
                      dpar::Exec::LAUNCH_PER_ROUND, tab, tp, stream,

@@ -177,6 +177,27 @@ struct LaneMat4 {  // one matrix, only 4-byte aligned: four dword accesses
 
 // ------------------------------------------------------------ one work item
 
+// Lines [ls, le) of work item t's blocks and the item's chunk c within them:
+// work item t belongs to group g = t / C, which holds the whole blocks
+// [g G, min(g G + G, b)) (G = prm.grp consecutive blocks; 1 except in the
+// one-launch executors when blocks are shorter than half a chunk); block j
+// is the run of lines [floor(j NL / b), floor((j + 1) NL / b)) of Section
+// 1.1's partition into b blocks.
+__device__ inline void item_lines(const Params& prm, uint64_t t, uint64_t* ls,
+                                  uint64_t* le, uint64_t* c) {
+  const uint64_t g = t / (uint64_t)prm.C;
+  *c = t % (uint64_t)prm.C;
+  const uint64_t j0 = g * (uint64_t)prm.grp;
+  const uint64_t j1 = min(j0 + (uint64_t)prm.grp, (uint64_t)prm.b);
+  *ls = prm.NL * j0 / (uint64_t)prm.b;
+  *le = prm.NL * j1 / (uint64_t)prm.b;
+}
+
+// Work-item groups of a one-launch run (b when every group is one block).
+__device__ __host__ inline uint64_t item_groups(const Params& prm) {
+  return ((uint64_t)prm.b + (uint64_t)prm.grp - 1) / (uint64_t)prm.grp;
+}
+
 // Ranks whose loads are in flight per wavefront.  The host pads the pointer
 // and opcode tables by kTablePad >= 2 * kU entries.
 #ifndef DPAR_KU
@@ -261,11 +282,10 @@ __device__ __forceinline__ void run_unit(const uint64_t* __restrict__ xp,
   const int wave =
       (W == 1) ? 0 : __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 
-  // chunk -> quanta [cs, ce): block j is a run of lines (Section 1.1's
-  // partition into b blocks), cut into C chunks at line boundaries
-  const uint64_t j = t / (uint64_t)prm.C, c = t % (uint64_t)prm.C;
-  const uint64_t ls = prm.NL * j / (uint64_t)prm.b;
-  const uint64_t le = prm.NL * (j + 1) / (uint64_t)prm.b;
+  // chunk -> quanta [cs, ce): the item's blocks are a run of lines, cut
+  // into C chunks at line boundaries
+  uint64_t ls, le, c;
+  item_lines(prm, t, &ls, &le, &c);
   const uint64_t nl = le - ls;
   const uint64_t cls = ls + c * nl / (uint64_t)prm.C;
   const uint64_t cle = ls + (c + 1) * nl / (uint64_t)prm.C;
@@ -369,10 +389,10 @@ __device__ __forceinline__ void run_unit_lv(const uint64_t* __restrict__ xp,
   uint32_t* lvl = reinterpret_cast<uint32_t*>(lds + lay.lvl);
   uint32_t* off = reinterpret_cast<uint32_t*>(lds + lay.off);
 
-  // chunk -> quanta [cs, ce): block j is cut at lines, the chunk at quanta
-  const uint64_t j = t / (uint64_t)prm.C, c = t % (uint64_t)prm.C;
-  const uint64_t ls = prm.NL * j / (uint64_t)prm.b;
-  const uint64_t le = prm.NL * (j + 1) / (uint64_t)prm.b;
+  // chunk -> quanta [cs, ce): the item's blocks are cut at lines, the chunk
+  // at quanta
+  uint64_t ls, le, c;
+  item_lines(prm, t, &ls, &le, &c);
   const uint64_t qs = min(ls * prm.lq, prm.Q);
   const uint64_t qe = min(le * prm.lq, prm.Q);
   const uint64_t n = qe - qs;
@@ -479,9 +499,8 @@ __device__ __forceinline__ void run_unit_sub(const uint64_t* __restrict__ xp,
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 
   // chunk -> quanta [cs, ce), as in run_unit
-  const uint64_t j = t / (uint64_t)prm.C, c = t % (uint64_t)prm.C;
-  const uint64_t ls = prm.NL * j / (uint64_t)prm.b;
-  const uint64_t le = prm.NL * (j + 1) / (uint64_t)prm.b;
+  uint64_t ls, le, c;
+  item_lines(prm, t, &ls, &le, &c);
   const uint64_t nl = le - ls;
   const uint64_t cls = ls + c * nl / (uint64_t)prm.C;
   const uint64_t cle = ls + (c + 1) * nl / (uint64_t)prm.C;
@@ -813,7 +832,7 @@ template <class U>
 __global__ __launch_bounds__(U::kThreads) void k_ticket(DPAR_KARGS) {
   extern __shared__ char lds_raw[];
   __shared__ unsigned s_ticket;
-  const uint64_t nunits = (uint64_t)prm.b * prm.C;
+  const uint64_t nunits = item_groups(prm) * prm.C;
   const uint64_t K = prm.batch;
   // Batch k (work items [k K, k K + K)) belongs to counter k % NC.  A
   // workgroup serves one counter: its first batch is its own index, later
@@ -900,7 +919,7 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
   // workgroups resident per CU (see launch())
   const size_t lds = U::lds(prm) > lds_floor ? U::lds(prm) : lds_floor;
   const dim3 block(U::kThreads);
-  const uint64_t nunits = (uint64_t)prm.b * prm.C;
+  const uint64_t nunits = item_groups(prm) * prm.C;
   // One workgroup per work item: a launch's total thread count must stay
   // below 2^32, so a grid of more than kMaxGrid workgroups goes out as
   // several launches, each given the index of its first item.

@@ -47,7 +47,10 @@ struct Params {
   uint32_t lq;      // quanta per line
   uint64_t qbase;   // first quantum index (the tail unit starts after Q)
   int b;            // blocks = rounds
-  int C;            // chunks per block
+  int C;            // chunks per block (per group of grp blocks)
+  int grp;          // one-launch executors: consecutive whole blocks per
+                    // work-item group (1: every block on its own; more when
+                    // blocks are shorter than half a chunk)
   unsigned batch;   // TICKET: consecutive work items claimed per ticket
   int lv_log2t;     // LEVEL: log2 of the chunk capacity T in quanta
   int nlev;         // LEVEL: H + 1 depth levels

@@ -285,4 +285,12 @@ void block_quanta(const Schedule& s, int j, uint64_t* qs, uint64_t* qe) {
   *qe = std::min<uint64_t>(le * (uint64_t)s.lq, s.Q);
 }
 
+int block_group(const Schedule& s) {
+  const uint64_t L = 64 / (uint64_t)s.lq;  // lines per chunk
+  const uint64_t maxl = (s.NL + (uint64_t)s.b - 1) / (uint64_t)s.b;
+  if (s.NL == 0 || 2 * maxl > L) return 1;
+  const uint64_t g = (uint64_t)s.b * L / s.NL;
+  return (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)s.b));
+}
+
 }  // namespace dpar

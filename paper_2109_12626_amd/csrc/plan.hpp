@@ -130,4 +130,10 @@ Schedule make_schedule(uint64_t m, int b, int g, int lq);
 // Quanta [qs, qe) of block j.
 void block_quanta(const Schedule& s, int j, uint64_t* qs, uint64_t* qe);
 
+// Consecutive whole blocks per work item for executors that issue every
+// round's work items from one launch: 1 when a block fills at least half a
+// chunk (64 quanta), else the largest G <= b with G NL / b <= 64 / lq lines,
+// so that any G consecutive blocks fit one chunk (s.C is then 1).
+int block_group(const Schedule& s);
+
 }  // namespace dpar

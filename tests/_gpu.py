@@ -119,3 +119,8 @@ def env_waves(n):
 def env_unit(u):
     """Work-item evaluation: "seq", "level" or None (the library chooses)."""
     return _Env("DPAR_UNIT", u)
+
+
+def env_group_blocks(on):
+    """Grouping of short blocks in the one-launch executors: 1 or 0."""
+    return _Env("DPAR_GROUP_BLOCKS", 1 if on else 0)

@@ -11,8 +11,8 @@ import torch
 
 import oracle
 import synth
-from tests._gpu import (POISON, assert_all_ranks_equal, env_unit, from_dev,
-                        lib, need_gpu, to_dev)
+from tests._gpu import (POISON, assert_all_ranks_equal, env_group_blocks,
+                        env_unit, from_dev, lib, need_gpu, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -246,3 +246,31 @@ def test_large_p(p, m, exec, alg):
     for b in (1, 3):
         out = from_dev(_run(x, "float32", "sum", b, alg, exec), x)
         assert_all_ranks_equal(out, want, f"{alg}/{exec}/p={p}/b={b}")
+
+
+@pytest.mark.parametrize("exec", ["auto", "split", "ticket"])
+@pytest.mark.parametrize("unit", [None, "seq", "level", "sub"])
+@pytest.mark.parametrize("p,m,b", [(1152, 1 << 16, 817), (300, 4099, 1000),
+                                   (36, 1 << 10, 103), (7, 16, 13),
+                                   (64, 1 << 12, 1024), (129, 5003, 5003)])
+def test_grouped_short_blocks(exec, unit, p, m, b):
+    """Blocks shorter than half a chunk: the one-launch executors give each
+    work item several consecutive whole blocks.  Bit-exact for every work
+    item kind, with grouping off (DPAR_GROUP_BLOCKS=0) as well."""
+    need_gpu()
+    x = _input("normal_f32", 2170 + p, p, m)
+    want = _want(x, "float32", "sum", "dual")
+    for grouped in (True, False):
+        with env_unit(unit), env_group_blocks(grouped):
+            out = from_dev(_run(x, "float32", "sum", b, "dual", exec), x)
+        assert_all_ranks_equal(out, want,
+                               f"{exec}/{unit}/p={p}/m={m}/b={b}/g={grouped}")
+
+
+@pytest.mark.parametrize("exec", ["split", "ticket"])
+def test_grouped_short_blocks_matrix_product(exec):
+    need_gpu()
+    x = _input("uniform_u32_mat", 2177, 64, 1000)
+    want = oracle.allreduce_ltr(x, "u32mat2x2", "matmul")
+    out = from_dev(_run(x, "u32mat2x2", "matmul", 300, "dual", exec), x)
+    assert_all_ranks_equal(out, want, f"matmul grouped {exec}")
