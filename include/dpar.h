@@ -278,7 +278,8 @@ const char* dpar_last_error(void);
  * them changes what a call computes:
  *   DPAR_UNIT=seq|level|sub force the post-order, level or subtree work
  *                           item
- *   DPAR_WAVES=1|2          wavefronts per post-order work item
+ *   DPAR_WAVES=1|2          wavefronts per post-order work item (default
+ *                           1 for p <= 48, else 2)
  *   DPAR_TICKET_BATCH=k     work items claimed per ticket (TICKET)
  *   DPAR_SPLIT_UP=ticket    SPLIT's up-phase on the ticketed persistent
  *                           kernel instead of one launch (comparison)

@@ -12,7 +12,7 @@ import torch
 import oracle
 import synth
 from tests._gpu import (POISON, assert_all_ranks_equal, env_group_blocks,
-                        env_unit, from_dev, lib, need_gpu, to_dev)
+                        env_unit, env_waves, from_dev, lib, need_gpu, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -50,13 +50,16 @@ def _input(dist, seed, p, m, **kw):
 
 @pytest.mark.parametrize("alg", ALGS)
 @pytest.mark.parametrize("exec", EXECS)
-@pytest.mark.parametrize("unit", ["seq", "level"])
+@pytest.mark.parametrize("unit", ["seq1", "seq2", "level"])
 @pytest.mark.parametrize("b", [1, 8, 64])
 def test_fp32_every_alg_and_executor(alg, exec, unit, b):
+    """seq1 / seq2: the post-order item with one wavefront for both trees
+    (the default at p = 36) or one per tree."""
     need_gpu()
     x = _input("normal_f32", 2120, 36, 4099)
     want = _want(x, "float32", "sum", alg)
-    with env_unit(unit):
+    waves = {"seq1": 1, "seq2": 2}.get(unit)
+    with env_unit("seq" if waves else unit), env_waves(waves):
         out = from_dev(_run(x, "float32", "sum", b, alg, exec), x)
     assert_all_ranks_equal(out, want, f"{alg}/{exec}/{unit}/b={b}")
 
