@@ -421,7 +421,11 @@ def main():
     def rate(nb, ms):
         return round(nb / (ms * 1e-3) / 1e9, 2)
 
+    srt = sorted(call_ms)
+    med_ms = (srt[(len(srt) - 1) // 2] + srt[len(srt) // 2]) / 2
     phases = {"call": {"avg_ms": round(avg_ms, 4),
+                       "min_ms": round(srt[0], 4),
+                       "median_ms": round(med_ms, 4),
                        "algorithmic_bytes": int(nbytes),
                        "GB/s": rate(nbytes, avg_ms)}}
     if split:
