@@ -128,10 +128,13 @@ bool make_sub(const Tree& t, const std::vector<uint32_t>& ops, int s,
       const uint32_t slot = ops[v] & OP_DEPTH_MASK;
       if (t.depth[v] - d0 == s) {              // a part: [lo(v), v]
         if ((int)(parts.size() / 3) >= kSubParts) return false;
+        // the walk's slots are the relative depths 0 .. top - slot: a node
+        // reads slot d + 1 only when it has a second child, so never below
+        // the deepest level
         uint32_t top = slot;
         for (int i = t.lo[v]; i <= v; ++i)
           top = std::max<uint32_t>(top, ops[i] & OP_DEPTH_MASK);
-        ns = std::max<int>(ns, (int)(top - slot) + 2);
+        ns = std::max<int>(ns, (int)(top - slot) + 1);
         entries[tr].push_back(0x80000000u | (uint32_t)(parts.size() / 3));
         entries[tr].push_back(ops[v] & ~(uint32_t)(OP_C0 | OP_C1));
         parts.push_back((uint32_t)t.lo[v]);

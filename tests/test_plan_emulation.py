@@ -18,7 +18,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2109_12626_amd", "csrc")
 
 P_LIST = list(range(1, 130)) + [191, 255, 256, 257, 300, 511, 576, 1000,
-                                  1151, 1152]
+                                  1151, 1152, 2049, 4099]
 
 
 @pytest.fixture(scope="module")
