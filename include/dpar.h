@@ -288,6 +288,10 @@ const char* dpar_last_error(void);
  *                           one work item per block even when blocks are
  *                           shorter than half a chunk (default 1: groups of
  *                           consecutive whole blocks)
+ *   DPAR_BCAST_SPAN_KB=n    SPLIT's broadcast pass: y_0 streamed out in
+ *                           spans of at most n KB (at least 8 tiles of 256
+ *                           lanes), each to every output row before the
+ *                           next (default 16384)
  *   DPAR_SEQ_WG_PER_CU=n    SPLIT's post-order up-phase at p >= 256 with
  *                           at least 64 work items per CU: workgroups
  *                           resident per CU (default 4; 0 = as many as fit)

@@ -52,6 +52,10 @@ constexpr int kCapMinRanks = 256;
 constexpr int kCapMinItemsPerCu = 64;
 // Largest p whose post-order work items use one wavefront for both trees.
 constexpr int kOneWaveMaxRanks = 48;
+// Split executor's broadcast pass: y_0 is streamed out in spans of at most
+// this many KB (2 MB per XCD's 4 MB L2; a 32 MB y_0 taken as one span ran at
+// half the speed).
+constexpr int kBcastSpanKB = 16384;
 
 struct OpsTable {
   uint32_t* dev = nullptr;   // opcodes, padded
@@ -884,7 +888,10 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     }
     // y_0 now holds y for the whole chunked part; stream it to y_1..y_{p-1}
     const uint64_t main_bytes = s.Q * (uint64_t)s.g * esz;
-    e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16,
+    int span_kb = env_int("DPAR_BCAST_SPAN_KB", kBcastSpanKB);
+    if (span_kb <= 0) span_kb = kBcastSpanKB;
+    const uint64_t span = (uint64_t)span_kb << 10;
+    e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16, span,
                         stream);
     if (e != hipSuccess) return hip_fail(e, "broadcast launch");
   }

@@ -871,21 +871,24 @@ __global__ __launch_bounds__(U::kThreads) void k_ticket(DPAR_KARGS) {
 }
 
 // Broadcast pass of the split executor: y_0 -> y_1 .. y_{p-1}.  One
-// workgroup per (output row, tile of 256 lanes), the tiles of a row on
-// consecutive workgroups and the rows in order: each thread loads one lane
-// of y_0 (a cache hit: the up-phase has just written y_0, and every row reads
-// it again) and writes it with one streaming store.  Many short workgroups
-// with one store per thread write HBM faster on this part than long-running
-// workgroups with many stores each (measured at the headline size: 7.1 vs
-// 5.7 TB/s).  Works on bytes, whatever the element type.
+// workgroup per (output row, tile of 256 lanes), in the order of plan.hpp
+// bcast_tile: y_0 in spans, every row of a span with its tiles on
+// consecutive workgroups, then the next span.  Each thread loads one lane of
+// y_0 and writes it with one streaming store.  The load is an L2 hit: every
+// XCD reads the same eighth of a span for every row, and a span is sized so
+// that this eighth stays in the XCD's L2 while the stores stream past it
+// (taken as one span, a 32 MB y_0 fell out of L2 and the pass ran at half
+// speed).  Many short workgroups with one store per thread write HBM faster
+// on this part than long-running workgroups with many stores each (measured
+// at p = 1152, m = 2^22 fp32: 7.1 vs 5.7 TB/s).  Works on bytes, whatever
+// the element type.
 template <class T>
 __global__ __launch_bounds__(256) void k_bcast(const uint64_t* __restrict__ yp,
-                                               uint64_t n, uint64_t tiles,
-                                               uint64_t first) {
-  const uint64_t w = first + blockIdx.x;
-  const uint64_t row = 1 + w / tiles;                 // workgroup-uniform
-  const uint64_t lane = (w % tiles) * 256 + threadIdx.x;
-  if (lane >= n) return;
+                                               BcastGrid g, uint64_t first) {
+  uint64_t row, tile;
+  bcast_tile(g, first + blockIdx.x, &row, &tile);     // workgroup-uniform
+  const uint64_t lane = tile * 256 + threadIdx.x;
+  if (lane >= g.n) return;
   const uint64_t off = lane * sizeof(T);
   const T v = *reinterpret_cast<const DPAR_GLOBAL T*>(yp[0] + off);
   __builtin_nontemporal_store(v,
@@ -1064,22 +1067,19 @@ size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev) {
 }
 
 hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
-                     hipStream_t stream) {
-  if (p < 2 || nbytes == 0) return hipSuccess;
-  const uint64_t lane = vec16 ? 16 : 4;
-  const uint64_t n = nbytes / lane;
-  const uint64_t tiles = (n + 255) / 256;
-  const uint64_t total = tiles * (uint64_t)(p - 1);
-  // a launch's thread count stays below 2^32: pieces of at most 2^23 tiles
+                     uint64_t span_bytes, hipStream_t stream) {
+  const BcastGrid g = bcast_grid(nbytes, vec16 ? 16 : 4, p, span_bytes);
+  // a launch's thread count stays below 2^32: pieces of at most 2^23
+  // workgroups (a multiple of 8, so workgroup w stays on XCD w mod 8)
   const uint64_t kMaxGrid = (1ull << 31) / 256;
-  for (uint64_t first = 0; first < total; first += kMaxGrid) {
-    const unsigned g = (unsigned)min(kMaxGrid, total - first);
+  for (uint64_t first = 0; first < g.total; first += kMaxGrid) {
+    const unsigned n = (unsigned)min(kMaxGrid, g.total - first);
     if (vec16)
-      hipLaunchKernelGGL((k_bcast<u32x4>), dim3(g), dim3(256), 0, stream,
-                         tab.yp, n, tiles, first);
+      hipLaunchKernelGGL((k_bcast<u32x4>), dim3(n), dim3(256), 0, stream,
+                         tab.yp, g, first);
     else
-      hipLaunchKernelGGL((k_bcast<uint32_t>), dim3(g), dim3(256), 0, stream,
-                         tab.yp, n, tiles, first);
+      hipLaunchKernelGGL((k_bcast<uint32_t>), dim3(n), dim3(256), 0, stream,
+                         tab.yp, g, first);
   }
   return hipGetLastError();
 }

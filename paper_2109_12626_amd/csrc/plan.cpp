@@ -296,4 +296,21 @@ int block_group(const Schedule& s) {
   return (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)s.b));
 }
 
+BcastGrid bcast_grid(uint64_t nbytes, uint64_t lane_bytes, int p,
+                     uint64_t span_bytes) {
+  BcastGrid g;
+  if (p < 2 || lane_bytes == 0) return g;
+  g.n = nbytes / lane_bytes;
+  g.rows = (uint64_t)(p - 1);
+  const uint64_t tiles = (g.n + 255) / 256;
+  if (tiles == 0) return g;
+  uint64_t tmax = span_bytes / (256 * lane_bytes);
+  tmax = tmax < 8 ? 8 : tmax & ~(uint64_t)7;
+  g.nspan = (tiles + tmax - 1) / tmax;
+  g.ts = (tiles + g.nspan - 1) / g.nspan;
+  if (g.nspan > 1) g.ts = (g.ts + 7) & ~(uint64_t)7;  // still <= tmax
+  g.total = g.nspan * g.rows * g.ts;
+  return g;
+}
+
 }  // namespace dpar

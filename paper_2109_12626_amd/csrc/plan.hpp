@@ -6,6 +6,13 @@
 #include <cstdint>
 #include <vector>
 
+// Helpers that the HIP kernels call as well are compiled for both sides.
+#if defined(__HIPCC__)
+#define DPAR_HOST_DEVICE __host__ __device__
+#else
+#define DPAR_HOST_DEVICE
+#endif
+
 namespace dpar {
 
 // Per-rank opcode consumed by the device round program.  One rank's step in
@@ -135,5 +142,35 @@ void block_quanta(const Schedule& s, int j, uint64_t* qs, uint64_t* qe);
 // chunk (64 quanta), else the largest G <= b with G NL / b <= 64 / lq lines,
 // so that any G consecutive blocks fit one chunk (s.C is then 1).
 int block_group(const Schedule& s);
+
+// Grid of the split executor's broadcast pass (y_0 -> y_1 .. y_{p-1}): one
+// workgroup per (output row, tile of 256 lanes).  The n lanes of y_0 are cut
+// into nspan spans of ts tiles each (equal widths; the last span may end in
+// tiles past y_0's end, which do nothing); every row of one span is written
+// before the next span starts.  With more than one span, ts is a multiple of
+// 8, so that workgroup w, which runs on XCD w mod 8, always finds the same
+// eighth of the span in its XCD's L2.
+struct BcastGrid {
+  uint64_t n = 0;       // lanes of y_0
+  uint64_t ts = 1;      // tiles per span
+  uint64_t nspan = 0;   // spans
+  uint64_t rows = 0;    // output rows p - 1
+  uint64_t total = 0;   // workgroups nspan * rows * ts
+};
+
+// Spans of at most max(span_bytes, 8 tiles) bytes, as few as that allows.
+BcastGrid bcast_grid(uint64_t nbytes, uint64_t lane_bytes, int p,
+                     uint64_t span_bytes);
+
+// Output row (1 .. p-1) and tile of workgroup w < g.total: span
+// w / (rows ts), in it row 1 + (w / ts) mod rows and tile w mod ts.
+DPAR_HOST_DEVICE inline void bcast_tile(const BcastGrid& g, uint64_t w,
+                                        uint64_t* row, uint64_t* tile) {
+  const uint64_t per_span = g.rows * g.ts;
+  const uint64_t span = w / per_span;
+  const uint64_t r = w - span * per_span;
+  *row = 1 + r / g.ts;
+  *tile = span * g.ts + r % g.ts;
+}
 
 }  // namespace dpar

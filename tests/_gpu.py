@@ -124,3 +124,8 @@ def env_unit(u):
 def env_group_blocks(on):
     """Grouping of short blocks in the one-launch executors: 1 or 0."""
     return _Env("DPAR_GROUP_BLOCKS", 1 if on else 0)
+
+
+def env_bcast_span_kb(kb):
+    """Span of y_0 (KB) per pass of the split executor's broadcast."""
+    return _Env("DPAR_BCAST_SPAN_KB", kb)

@@ -15,9 +15,9 @@ import torch
 import oracle
 import synth
 from synth import configs
-from tests._gpu import (POISON, assert_all_ranks_equal, env_unit, env_waves,
-                        from_dev, need_gpu, poisoned_like, resolve_b, run,
-                        to_dev, workload_input)
+from tests._gpu import (POISON, assert_all_ranks_equal, env_bcast_span_kb,
+                        env_unit, env_waves, from_dev, need_gpu,
+                        poisoned_like, resolve_b, run, to_dev, workload_input)
 
 pytestmark = pytest.mark.gpu
 
@@ -103,6 +103,41 @@ def test_level_unit_all_dtypes_and_executors(exec, dtype, op, dist):
         with env_unit("level"):
             out = run(x, dtype, op, b, exec)
         assert_all_ranks_equal(out, _want(x, dtype, op), f"b={b}")
+
+
+@pytest.mark.parametrize("span_kb", [1, 4, 36, 16384])
+@pytest.mark.parametrize("p,m,dtype,op,dist", [
+    (9, 40000, "float32", "sum", "normal_f32"),       # 16-byte lanes
+    (5, 40001, "int32", "max", "uniform_int"),        # + a scalar tail
+    (4, 9999, "u32mat2x2", "matmul", "odd_det_u32_mat"),
+    (3, 123457, "float32", "sum", "normal_f32")])
+def test_split_broadcast_in_spans(span_kb, p, m, dtype, op, dist):
+    """The broadcast pass taken in spans of y_0 (every row of a span, then
+    the next span; 8 tiles at least, padded to equal widths): all outputs
+    equal the oracle's y, whatever the span."""
+    kw = {"lo": -999, "hi": 999} if dist == "uniform_int" else {}
+    x = synth.generate(dist, 900 + p, p, m, **kw)
+    with env_bcast_span_kb(span_kb):
+        out = run(x, dtype, op, 7, "split")
+    assert_all_ranks_equal(out, _want(x, dtype, op), f"span {span_kb} KB")
+
+
+def test_split_broadcast_unaligned_rows_in_spans():
+    """4-byte lanes (rows only 4-byte aligned) with several spans."""
+    p, m = 6, 30001
+    x = synth.generate("normal_f32", 77, p, m)
+    xd = to_dev(np.pad(x, ((0, 0), (1, 0))))
+    yd = poisoned_like(xd)
+    from paper_2109_12626_amd import dpar
+    xs = [t[1:] for t in xd]
+    ys = [t[1:] for t in yd]
+    with env_bcast_span_kb(2):
+        dpar.dpar_allreduce_ex(xs, ys, p, m, "float32", "sum", 5, "split",
+                               torch.cuda.current_stream())
+        dpar.dpar_check_status(torch.cuda.current_stream())
+    out = yd.cpu().numpy()
+    assert_all_ranks_equal(out[:, 1:], _want(x, "float32", "sum"))
+    assert (out[:, 0].view(np.int32) == POISON).all()
 
 
 @pytest.mark.parametrize("exec", EXECS)
