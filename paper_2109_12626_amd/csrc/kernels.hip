@@ -284,13 +284,9 @@ __device__ __forceinline__ void run_unit(const uint64_t* __restrict__ xp,
 
   // chunk -> quanta [cs, ce): the item's blocks are a run of lines, cut
   // into C chunks at line boundaries
-  uint64_t ls, le, c;
-  item_lines(prm, t, &ls, &le, &c);
-  const uint64_t nl = le - ls;
-  const uint64_t cls = ls + c * nl / (uint64_t)prm.C;
-  const uint64_t cle = ls + (c + 1) * nl / (uint64_t)prm.C;
-  const uint64_t cs = min(cls * prm.lq, prm.Q);
-  const uint64_t ce = min(cle * prm.lq, prm.Q);
+  uint64_t cs, ce;
+  item_quanta(prm.NL, (uint64_t)prm.b, (uint64_t)prm.C, (uint64_t)prm.grp,
+              prm.lq, prm.Q, t, &cs, &ce);
   const uint32_t count = (uint32_t)(ce - cs);
   if (count == 0) return;  // uniform; cannot happen for b <= Q
   const uint64_t unit_off = (prm.qbase + cs) * (uint64_t)L::bytes;
@@ -499,13 +495,9 @@ __device__ __forceinline__ void run_unit_sub(const uint64_t* __restrict__ xp,
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 
   // chunk -> quanta [cs, ce), as in run_unit
-  uint64_t ls, le, c;
-  item_lines(prm, t, &ls, &le, &c);
-  const uint64_t nl = le - ls;
-  const uint64_t cls = ls + c * nl / (uint64_t)prm.C;
-  const uint64_t cle = ls + (c + 1) * nl / (uint64_t)prm.C;
-  const uint64_t cs = min(cls * prm.lq, prm.Q);
-  const uint64_t ce = min(cle * prm.lq, prm.Q);
+  uint64_t cs, ce;
+  item_quanta(prm.NL, (uint64_t)prm.b, (uint64_t)prm.C, (uint64_t)prm.grp,
+              prm.lq, prm.Q, t, &cs, &ce);
   const uint32_t count = (uint32_t)(ce - cs);
   if (count == 0) return;  // uniform
   const uint64_t unit_off = (prm.qbase + cs) * (uint64_t)L::bytes;

@@ -308,7 +308,10 @@ BcastGrid bcast_grid(uint64_t nbytes, uint64_t lane_bytes, int p,
   tmax = tmax < 8 ? 8 : tmax & ~(uint64_t)7;
   g.nspan = (tiles + tmax - 1) / tmax;
   g.ts = (tiles + g.nspan - 1) / g.nspan;
-  if (g.nspan > 1) g.ts = (g.ts + 7) & ~(uint64_t)7;  // still <= tmax
+  // a span of 8k tiles gives every XCD the same tiles for every row; only
+  // a y_0 small enough to sit whole in each XCD's L2 goes without padding
+  if (g.nspan > 1 || nbytes > kBcastNoPadBytes)
+    g.ts = (g.ts + 7) & ~(uint64_t)7;  // still <= tmax
   g.total = g.nspan * g.rows * g.ts;
   return g;
 }

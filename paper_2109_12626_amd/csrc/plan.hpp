@@ -143,13 +143,35 @@ void block_quanta(const Schedule& s, int j, uint64_t* qs, uint64_t* qe);
 // so that any G consecutive blocks fit one chunk (s.C is then 1).
 int block_group(const Schedule& s);
 
+// Quanta [*qs, *qe) of work item t of a post-order or subtree run: item t
+// belongs to group g = t / C, which holds the whole blocks [g grp,
+// min(g grp + grp, b)), i.e. the lines [floor(g grp NL / b),
+// floor(min(g grp + grp, b) NL / b)); the group's lines are cut into C
+// chunks at line boundaries and item t is chunk t mod C, clipped at Q
+// quanta.  Items in increasing t cover increasing, disjoint quantum ranges.
+DPAR_HOST_DEVICE inline void item_quanta(uint64_t NL, uint64_t b, uint64_t C,
+                                         uint64_t grp, uint64_t lq,
+                                         uint64_t Q, uint64_t t,
+                                         uint64_t* qs, uint64_t* qe) {
+  const uint64_t g = t / C, c = t % C;
+  const uint64_t j0 = g * grp;
+  const uint64_t j1 = j0 + grp < b ? j0 + grp : b;
+  const uint64_t ls = NL * j0 / b, le = NL * j1 / b;
+  const uint64_t nl = le - ls;
+  const uint64_t cls = ls + c * nl / C, cle = ls + (c + 1) * nl / C;
+  *qs = cls * lq < Q ? cls * lq : Q;
+  *qe = cle * lq < Q ? cle * lq : Q;
+}
+
 // Grid of the split executor's broadcast pass (y_0 -> y_1 .. y_{p-1}): one
 // workgroup per (output row, tile of 256 lanes).  The n lanes of y_0 are cut
 // into nspan spans of ts tiles each (equal widths; the last span may end in
 // tiles past y_0's end, which do nothing); every row of one span is written
-// before the next span starts.  With more than one span, ts is a multiple of
-// 8, so that workgroup w, which runs on XCD w mod 8, always finds the same
-// eighth of the span in its XCD's L2.
+// before the next span starts.  Apart from small y_0, ts is a multiple of 8,
+// so that workgroup w, which runs on XCD w mod 8, always finds the same
+// eighth of the span in its XCD's L2 (with 4095 tiles in a row instead of
+// 4096 every XCD would cycle through all of a 16 MB y_0 and the pass would
+// take half as long again).
 struct BcastGrid {
   uint64_t n = 0;       // lanes of y_0
   uint64_t ts = 1;      // tiles per span
@@ -158,7 +180,10 @@ struct BcastGrid {
   uint64_t total = 0;   // workgroups nspan * rows * ts
 };
 
-// Spans of at most max(span_bytes, 8 tiles) bytes, as few as that allows.
+// Spans of at most max(span_bytes, 8 tiles) bytes, as few as that allows;
+// ts is a multiple of 8 unless y_0 has at most kBcastNoPadBytes (then it
+// stays whole in every XCD's L2 and is not padded).
+constexpr uint64_t kBcastNoPadBytes = 2u << 20;
 BcastGrid bcast_grid(uint64_t nbytes, uint64_t lane_bytes, int p,
                      uint64_t span_bytes);
 

@@ -29,6 +29,9 @@ def _cases():
         (16, 16, 2, 4096),
         (256 * 16 * 9 + 16, 16, 3, 4096),  # 10 tiles, one span of 8 max
         (1 << 30, 16, 2, 16 * MB),
+        (16 * MB - 4096, 16, 1152, 16 * MB),  # 4095 tiles: padded to 4096
+        (2 * MB, 16, 5, 16 * MB),         # whole y_0 fits each L2: no padding
+        (2 * MB + 16, 16, 5, 16 * MB),
     ]
     rng = np.random.default_rng(2110)
     for _ in range(300):
@@ -71,11 +74,14 @@ def test_broadcast_grid_covers_every_output_once(grids, case):
     assert covered == rows * tiles            # every pair exactly once
     assert total == nspan * rows * ts == covered + padded
     budget = max(span // (256 * lane), 8)
-    assert ts <= max(budget & ~7, 8) if nspan > 1 else ts == tiles
     assert nspan == -(-tiles // max(budget & ~7, 8))
-    if nspan > 1:
+    assert ts <= max(budget & ~7, 8)
+    if nspan > 1 or nbytes > 2 * MB:
+        # every XCD (workgroup index mod 8) sees the same tiles in every row
         assert ts % 8 == 0
         assert padded < nspan * 8 * rows      # less than 8 tiles per span
+    else:
+        assert ts == tiles and padded == 0
 
 
 def test_headline_pass_is_one_span(grids):
