@@ -19,6 +19,7 @@ Prints ONE JSON line.  Extra lines go to stderr.
   python bench.py --sweep OUT.jsonl # every workload, executor, block count
   python bench.py --stream-probe    # plain fill / sum / copy rates
   python bench.py --read-probe      # read rates of the up-phase's pattern
+  python bench.py --write-probe     # write rates of broadcast shapes
 """
 
 import argparse
@@ -218,6 +219,90 @@ def read_probe():
     print(json.dumps({"read_probe_bytes": total, "rates": out}))
 
 
+def write_probe():
+    """Write rates of the broadcast pass's shape and of alternatives to it
+    (libdpar_probe.so dpar_probe_bcast): row 0 of a [1152, 2^22] fp32
+    buffer copied into the other 1151 rows, 19.31 GB written each time, the
+    minimum and median of 10 timed launches after two untimed ones, two
+    passes over the variants; then the library's own broadcast pass on the
+    same shape."""
+    import ctypes
+
+    import torch
+
+    from paper_2109_12626_amd import build as pbuild
+    from paper_2109_12626_amd import dpar
+    if not os.path.exists(pbuild.PROBE_LIB):
+        raise RuntimeError(f"{pbuild.PROBE_LIB} is missing: run build() first")
+    lib = ctypes.CDLL(pbuild.PROBE_LIB)
+    lib.dpar_probe_bcast.argtypes = [ctypes.c_void_p, ctypes.c_ulonglong,
+                                     ctypes.c_int, ctypes.c_int,
+                                     ctypes.c_void_p]
+    rowb = M * ELEM
+    y = torch.ones(P, M, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    sv = ctypes.c_void_p(stream.cuda_stream)
+    nbytes = (P - 1) * rowb
+    names = {0: "256 threads, 4 KB tiles, 1 streaming store per thread "
+                "(the library's shape)",
+             1: "as 0, each XCD's tiles from its own eighth of the row",
+             2: "256 threads, 8 KB tiles, 2 stores per thread",
+             3: "256 threads, 4 KB tiles, the tile into 2 rows",
+             4: "128 threads, 2 KB tiles",
+             5: "as 0 with ordinary stores",
+             6: "512 threads, 8 KB tiles"}
+    out = []
+
+    def timed(name, fn):
+        ts = []
+        for k in range(12):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            rc = fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if rc != 0:
+                raise RuntimeError(f"{name}: probe returned {rc}")
+            if k >= 2:
+                ts.append(e0.elapsed_time(e1))
+        ts.sort()
+        rec = {"shape": name, "ms_min": round(ts[0], 4),
+               "ms_median": round(ts[len(ts) // 2], 4),
+               "GB/s": round(nbytes / ts[0] / 1e6, 1)}
+        out.append(rec)
+        log(json.dumps(rec))
+
+    for _ in range(2):
+        for v, name in names.items():
+            timed(name, lambda v=v: lib.dpar_probe_bcast(
+                y.data_ptr(), rowb, P, v, sv))
+    # the library's broadcast pass: the call's second kernel, timed between
+    # the phase event and the end of the call
+    ys = dpar.pointers(dpar.rows(y))
+    ts = []
+    for k in range(12):
+        e1 = torch.cuda.Event(enable_timing=True)
+        e2 = torch.cuda.Event(enable_timing=True)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        dpar.dpar_set_phase_event(e1)
+        dpar.dpar_allreduce(ys, ys, P, M, "float32", "sum", 6532, stream)
+        e2.record(stream)
+        torch.cuda.synchronize()
+        if k >= 2:
+            ts.append(e1.elapsed_time(e2))
+    dpar.dpar_check_status(stream)
+    ts.sort()
+    out.append({"shape": "the library's broadcast pass (split executor, "
+                         "in place)",
+                "ms_min": round(ts[0], 4),
+                "ms_median": round(ts[len(ts) // 2], 4),
+                "GB/s": round(nbytes / ts[0] / 1e6, 1)})
+    log(json.dumps(out[-1]))
+    print(json.dumps({"write_probe_bytes": nbytes, "rates": out}))
+
+
 def sweep(out_path, only=(), execs=("split", "ticket", "launch", "barrier"),
           algs=("dual",)):
     """Every workload x executor x block count, cold caches (a 512 MiB
@@ -318,6 +403,8 @@ def main():
     ap.add_argument("--calib-copy", action="store_true")
     ap.add_argument("--stream-probe", action="store_true",
                     help="HBM write / read / copy rates of plain kernels")
+    ap.add_argument("--write-probe", action="store_true",
+                    help="write rates of broadcast shapes")
     ap.add_argument("--read-probe", action="store_true",
                     help="HBM read rates of the up-phase's access pattern")
     ap.add_argument("--sweep", metavar="OUT_JSONL",
@@ -355,6 +442,9 @@ def main():
         return
     if args.read_probe:
         read_probe()
+        return
+    if args.write_probe:
+        write_probe()
         return
     if args.sweep:
         sweep(args.sweep, [v for v in args.only.split(",") if v],

@@ -1,8 +1,10 @@
-// Read-pattern probes for measurement only; the reduction never calls them.
-// Each kernel reads a region of device memory, XORs what it reads and stores
-// nothing unless the XOR hits a fixed 64-bit pattern (it never does for the
-// probe's inputs, but the compiler cannot drop the loads), so its duration
-// is the time to read that pattern from HBM.  Built as libdpar_probe.so.
+// Read- and write-pattern probes for measurement only; the reduction never
+// calls them.  Each read kernel reads a region of device memory, XORs what it
+// reads and stores nothing unless the XOR hits a fixed 64-bit pattern (it
+// never does for the probe's inputs, but the compiler cannot drop the
+// loads), so its duration is the time to read that pattern from HBM.  The
+// write kernels copy one row into the others in several workgroup shapes.
+// Built as libdpar_probe.so.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -79,6 +81,47 @@ __global__ __launch_bounds__(256) void k_tiles(uint64_t base, uint64_t ntiles,
   sink_if_magic(v[0] ^ v[1] ^ v[2] ^ v[3], sink);
 }
 
+// Broadcast shapes (probe.h dpar_probe_bcast).  TPB threads per workgroup,
+// each storing S lanes of 16 bytes (lane t and t + TPB, ...) into R rows;
+// workgroup w takes row 1 + R (w / ntiles) (and the next R - 1 rows) and tile
+// w mod ntiles of TPB * S lanes; XCDSPLIT: the tile comes from the eighth of
+// the row that belongs to XCD w mod 8.
+template <int TPB, int S, int R, bool XCDSPLIT, bool NT>
+__global__ __launch_bounds__(TPB) void k_bcast_shape(uint64_t base,
+                                                     uint64_t row_bytes,
+                                                     uint64_t ntiles,
+                                                     uint64_t rows) {
+  const uint64_t w = blockIdx.x;
+  uint64_t rg, tile;
+  if (XCDSPLIT) {
+    const uint64_t k = w & 7, q = w >> 3, per = ntiles / 8;
+    rg = q / per;
+    tile = k * per + q % per;
+  } else {
+    rg = w / ntiles;
+    tile = w % ntiles;
+  }
+  const uint64_t lane0 = tile * TPB * S + threadIdx.x;
+  u32x4 v[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s)
+    v[s] = *at<u32x4>(base + (lane0 + (uint64_t)s * TPB) * 16);
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const uint64_t row = 1 + rg * R + r;
+    if (row > rows) break;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      DPAR_GLOBAL u32x4* d = reinterpret_cast<DPAR_GLOBAL u32x4*>(
+          base + row * row_bytes + (lane0 + (uint64_t)s * TPB) * 16);
+      if (NT)
+        __builtin_nontemporal_store(v[s], d);
+      else
+        *d = v[s];
+    }
+  }
+}
+
 uint64_t gcd(uint64_t a, uint64_t b) {
   while (b) {
     const uint64_t t = a % b;
@@ -124,5 +167,33 @@ extern "C" int dpar_probe_tiles(const void* base, unsigned long long nbytes,
   hipLaunchKernelGGL(k_tiles, dim3((unsigned)ntiles), dim3(256), 0, stream,
                      reinterpret_cast<uint64_t>(base), ntiles, (uint64_t)mul,
                      reinterpret_cast<uint64_t>(sink));
+  return hipGetLastError() == hipSuccess ? 0 : -2;
+}
+
+extern "C" int dpar_probe_bcast(void* base, unsigned long long row_bytes,
+                                int p, int variant, hipStream_t stream) {
+  if (!base || p < 2 || row_bytes == 0 || row_bytes % 32768) return -1;
+  const uint64_t rows = (uint64_t)(p - 1);
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const uint64_t rb = row_bytes;
+#define DPAR_SHAPE(TPB, S, R, X, NT)                                        \
+  do {                                                                      \
+    const uint64_t nt = rb / (16ull * TPB * S);                             \
+    const uint64_t grid = nt * ((rows + R - 1) / R);                        \
+    if (grid * TPB >= (1ull << 32)) return -1;                              \
+    hipLaunchKernelGGL((k_bcast_shape<TPB, S, R, X, NT>), dim3((unsigned)grid), \
+                       dim3(TPB), 0, stream, b, rb, nt, rows);              \
+  } while (0)
+  switch (variant) {
+    case 0: DPAR_SHAPE(256, 1, 1, false, true); break;
+    case 1: DPAR_SHAPE(256, 1, 1, true, true); break;
+    case 2: DPAR_SHAPE(256, 2, 1, false, true); break;
+    case 3: DPAR_SHAPE(256, 1, 2, false, true); break;
+    case 4: DPAR_SHAPE(128, 1, 1, false, true); break;
+    case 5: DPAR_SHAPE(256, 1, 1, false, false); break;
+    case 6: DPAR_SHAPE(512, 1, 1, false, true); break;
+    default: return -1;
+  }
+#undef DPAR_SHAPE
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }
