@@ -20,6 +20,7 @@ Prints ONE JSON line.  Extra lines go to stderr.
   python bench.py --stream-probe    # plain fill / sum / copy rates
   python bench.py --read-probe      # read rates of the up-phase's pattern
   python bench.py --write-probe     # write rates of broadcast shapes
+  python bench.py --table2          # the paper's Table 2 counts at p = 288
 """
 
 import argparse
@@ -303,6 +304,77 @@ def write_probe():
     print(json.dumps({"write_probe_bytes": nbytes, "rates": out}))
 
 
+# Per-process counts of the paper's Table 2 (Section 2): int32 elements.
+TABLE2_COUNTS = [0, 1, 2, 8, 15, 21, 25, 87, 150, 212, 250, 875, 1500, 2125,
+                 2500, 8750, 15000, 21250, 25000, 87500, 150000, 212500,
+                 250000, 875000, 1500000, 2125000, 2500000, 4597152, 6694304,
+                 8388608]
+
+
+def table2():
+    """The paper's only experiment, replayed on one GPU: p = 288 virtual
+    ranks (its 36 nodes x 8 processes), int32 SUM, the per-process counts of
+    its Table 2 and its fixed block of 16000 elements (b = ceil(count /
+    16000)).  Columns: the doubly-pipelined dual-root algorithm with the
+    default executor and with the round-structured executor (the paper's
+    b + H rounds, down-phase included), and the single-tree pipelined
+    reduce-then-broadcast (User-Allreduce1) with the same two executors.
+    Each entry: minimum and median of the per-call GPU time (HIP events on
+    the call's stream) over back-to-back calls after warm-up; the paper
+    takes the minimum over repetitions too."""
+    import numpy as np
+    import torch
+
+    from paper_2109_12626_amd import dpar
+    p, blk = 288, 16000
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    cmax = max(TABLE2_COUNTS)
+    g = torch.Generator(device=dev)
+    g.manual_seed(2109)
+    x = torch.randint(-1000, 1001, (p, cmax), dtype=torch.int32, device=dev,
+                      generator=g)
+    y = torch.empty_like(x)
+    xs, ys = dpar.pointers(dpar.rows(x)), dpar.pointers(dpar.rows(y))
+    variants = [("dual", "auto"), ("dual", "rounds"),
+                ("reduce_bcast", "auto"), ("reduce_bcast", "rounds")]
+    out = []
+    for count in TABLE2_COUNTS:
+        b = max(1, -(-count // blk))
+        ref = None
+        rec = {"count": count, "b": b}
+        for alg, ex in variants:
+            def call():
+                dpar.dpar_allreduce_opt(xs, ys, p, count, "int32", "sum", b,
+                                        alg, ex, 0, -1, stream)
+            reps = 20 if count <= 250000 else 8
+            for _ in range(3):
+                call()
+            dpar.dpar_check_status(stream)
+            ts = []
+            for _ in range(reps):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                call()
+                e1.record(stream)
+                e1.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e3)
+            dpar.dpar_check_status(stream)
+            if count:
+                # every algorithm and executor gives the same int32 result
+                got = y[:, :count:max(1, count // 4096)].clone()
+                assert bool((got == got[0]).all()), (count, alg, ex)
+                if ref is None:
+                    ref = got[0]
+                assert torch.equal(ref, got[0]), (count, alg, ex)
+            rec[f"{alg}/{ex}"] = {"us_min": round(min(ts), 2),
+                                  "us_median": round(float(np.median(ts)), 2)}
+        out.append(rec)
+        log(json.dumps(rec))
+    print(json.dumps({"table2_p": p, "block": blk, "rows": out}))
+
+
 def sweep(out_path, only=(), execs=("split", "ticket", "launch", "barrier"),
           algs=("dual",)):
     """Every workload x executor x block count, cold caches (a 512 MiB
@@ -403,6 +475,8 @@ def main():
     ap.add_argument("--calib-copy", action="store_true")
     ap.add_argument("--stream-probe", action="store_true",
                     help="HBM write / read / copy rates of plain kernels")
+    ap.add_argument("--table2", action="store_true",
+                    help="the paper's Table 2 counts at p = 288")
     ap.add_argument("--write-probe", action="store_true",
                     help="write rates of broadcast shapes")
     ap.add_argument("--read-probe", action="store_true",
@@ -445,6 +519,9 @@ def main():
         return
     if args.write_probe:
         write_probe()
+        return
+    if args.table2:
+        table2()
         return
     if args.sweep:
         sweep(args.sweep, [v for v in args.only.split(",") if v],

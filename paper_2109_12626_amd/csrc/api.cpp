@@ -875,8 +875,20 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     tp.C = 1;
     tp.grp = 1;
     tp.batch = 1;
-    e = dpar::launch(kind, dpar::Path::SCALAR, dpar::Unit::SEQ, waves,
-                     dpar::Exec::LAUNCH_PER_ROUND, tab, tp, stream,
+    // at most 3 elements: evaluated level by level (all p loads at once)
+    // where the level table exists; a post-order walk would be a chain of
+    // p / 2 dependent loads (p = 288, 2125 elements: 47 us per call with
+    // the walk)
+    dpar::Tables tt = tab;
+    tt.lvl = ops->lvl;
+    tp.lv_log2t = 2;
+    const bool level =
+        p >= 2 && ops->lvl &&
+        dpar::level_lds_bytes(dpar::Path::SCALAR, kind, p, tp.lv_log2t,
+                              tp.nlev) <= (size_t)st->lds_limit;
+    e = dpar::launch(kind, dpar::Path::SCALAR,
+                     level ? dpar::Unit::LEVEL : dpar::Unit::SEQ, waves,
+                     dpar::Exec::LAUNCH_PER_ROUND, tt, tp, stream,
                      st->num_cus, 0);
     if (e != hipSuccess) return hip_fail(e, "tail launch");
   }

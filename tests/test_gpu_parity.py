@@ -140,6 +140,22 @@ def test_split_broadcast_unaligned_rows_in_spans():
     assert (out[:, 0].view(np.int32) == POISON).all()
 
 
+@pytest.mark.parametrize("exec", ["auto", "split", "ticket", "rounds"])
+@pytest.mark.parametrize("m", [1, 2, 3, 15, 21, 87, 2125, 8750, 21250])
+def test_paper_counts_at_p288(m, exec):
+    """The per-process counts of the paper's Table 2 that leave elements
+    after the last 16-byte quantum, at its 288 processes, with its block of
+    16000 elements: the trailing elements go through their own pass."""
+    p = 288
+    b = max(1, -(-m // 16000))
+    x = synth.generate("uniform_int", 288 + m, p, m, lo=-1000, hi=1000)
+    out = run(x, "int32", "sum", b, exec)
+    assert_all_ranks_equal(out, _want(x, "int32", "sum"), f"m={m} {exec}")
+    xf = synth.generate("normal_f32", 289 + m, p, m)
+    out = run(xf, "float32", "sum", b, exec)
+    assert_all_ranks_equal(out, _want(xf, "float32", "sum"), f"m={m} {exec}")
+
+
 @pytest.mark.parametrize("exec", EXECS)
 def test_m_zero_is_a_noop(exec):
     from paper_2109_12626_amd import dpar

@@ -235,14 +235,16 @@ def test_subtree_unit_chosen_with_a_tail(m):
             assert_all_ranks_equal(out, want, f"auto unit {exec} m={m}")
 
 
-@pytest.mark.parametrize("p,m", [(2049, 257), (4099, 130), (16384, 64)])
+@pytest.mark.parametrize("p,m", [(2049, 257), (4099, 130), (16384, 64),
+                                 (16384, 67)])
 @pytest.mark.parametrize("exec", ["auto", "split", "ticket", "launch",
                                   "rounds"])
 @pytest.mark.parametrize("alg", ["dual", "single"])
 def test_large_p(p, m, exec, alg):
     """Deeper trees (H up to 13): the LDS slot count, the level table (up to
     p = 65534; at 16384 ranks the level item no longer fits in LDS and the
-    library falls back to the post-order item) and the subtree plan."""
+    library falls back to the post-order item, for the elements after the
+    last 16-byte quantum as well) and the subtree plan."""
     need_gpu()
     x = _input("normal_f32", 2160 + p % 97, p, m)
     want = _want(x, "float32", "sum", alg)
