@@ -151,9 +151,10 @@ typedef struct {
 
 /* Block decomposition chosen for a call (Section 1.1: b successive blocks of
  * roughly m/b elements).  A wavefront lane owns one quantum of `quantum`
- * elements (4 = 16 bytes on the vector path for INT32/FLOAT32, else 1).
- * Blocks are cut at multiples of `granularity` elements (128-byte lines on
- * the vector path when m allows b such lines, else one quantum): with
+ * elements: 4 (16 bytes) for INT32/FLOAT32 when every block holds at least
+ * one quantum (m / 4 >= b), else 1; a matrix is one quantum.  Blocks are cut
+ * at multiples of `granularity` elements (lines of 8 quanta, 128 bytes, when
+ * m allows b such lines, else one quantum): with
  * L = ceil(nquanta * quantum / granularity) lines, block j holds lines
  *     [floor(j*L/b), floor((j+1)*L/b)),
  * clipped at nquanta quanta, and the last block also holds the tail_elems
@@ -175,8 +176,10 @@ typedef struct {
 /* Reduction-to-all (Section 1; Algorithm 1).
  *   x, y    HOST arrays of p DEVICE pointers; x[i] and y[i] each address
  *           m elements of dtype (m*16 bytes for DPAR_U32_MAT2X2).  Pointers
- *           must be aligned to 4 bytes; when all 2p are 16-byte aligned the
- *           vector path is used.  The library copies both arrays before
+ *           must be aligned to 4 bytes.  Rows that start on 16-byte
+ *           boundaries are read and written fastest (each 16-byte lane then
+ *           stays within one cache line); other rows take the same path.
+ *           The library copies both arrays before
  *           returning; the caller owns and may free them at once.  The
  *           buffers must stay valid, and x unmodified, until the stream work
  *           completes.
@@ -249,9 +252,11 @@ int dpar_block_rule(int p, size_t m, double alpha, double beta);
  * No device work. */
 int dpar_rounds(int p, int b, int rank);
 
-/* The decomposition dpar_allreduce would use for these arguments when all
- * pointers are 16-byte aligned (aligned != 0) or not.  b == 0 applies the
- * rule.  No device work. */
+/* The decomposition dpar_allreduce would use for these arguments (with any
+ * executor but ROUNDS / ROUNDS_BARRIER, which take one element per lane
+ * when m is not a multiple of 4).  `aligned` is ignored: the decomposition
+ * does not depend on the pointers' alignment.  b == 0 applies the rule.  No
+ * device work. */
 int dpar_schedule_info(int p, size_t m, dpar_dtype_t dtype, int b, int aligned,
                        dpar_schedule_t* out);
 
@@ -288,6 +293,8 @@ const char* dpar_last_error(void);
  *                           one work item per block even when blocks are
  *                           shorter than half a chunk (default 1: groups of
  *                           consecutive whole blocks)
+ *   DPAR_SCALAR=1           one element per lane and the canonical
+ *                           element partition for INT32/FLOAT32 (tests)
  *   DPAR_BCAST_SPAN_KB=n    SPLIT's broadcast pass: y_0 streamed out in
  *                           spans of at most n KB (at least 8 tiles of 256
  *                           lanes), each to every output row before the

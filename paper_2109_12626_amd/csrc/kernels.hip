@@ -38,6 +38,11 @@
 namespace dpar {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// The same 16 bytes in global memory, where a row may start at any 4-byte
+// boundary: gfx950 loads and stores 16 bytes at 4-byte aligned addresses in
+// one instruction (the HSA runtime runs the GPU in unaligned access mode, so
+// the compiler emits global_load/store_dwordx4 for this type as well).
+typedef uint32_t u32x4g __attribute__((ext_vector_type(4), aligned(4)));
 
 // Global-memory pointers (address space 1): lets the compiler emit global_*
 // instructions with a scalar base and a 32-bit per-lane offset instead of
@@ -109,7 +114,7 @@ __device__ inline u32x4 mat_mul(u32x4 a, u32x4 b) {
 // A lane owns one quantum: `bytes` contiguous bytes of every rank row.
 
 template <class E>
-struct Lane4 {  // four scalars, one 16-byte access
+struct Lane4 {  // four scalars, one 16-byte access (4-byte aligned)
   using T = u32x4;
   static constexpr uint32_t bytes = 16;
   __device__ static T ap(T a, T b) {
@@ -121,10 +126,10 @@ struct Lane4 {  // four scalars, one 16-byte access
     return r;
   }
   __device__ static T load(uint64_t row, uint32_t off) {
-    return ld(gptr<T>(row, off));
+    return ld(gptr<u32x4g>(row, off));
   }
   __device__ static void store(uint64_t row, uint32_t off, T v) {
-    st(gptr_w<T>(row, off), v);
+    st(gptr_w<u32x4g>(row, off), (u32x4g)v);
   }
 };
 
@@ -141,37 +146,15 @@ struct Lane1 {  // one scalar
   }
 };
 
-struct LaneMat16 {  // one matrix, 16-byte aligned
+struct LaneMat {  // one matrix, one 16-byte access (4-byte aligned)
   using T = u32x4;
   static constexpr uint32_t bytes = 16;
   __device__ static T ap(T a, T b) { return mat_mul(a, b); }
   __device__ static T load(uint64_t row, uint32_t off) {
-    return ld(gptr<T>(row, off));
+    return ld(gptr<u32x4g>(row, off));
   }
   __device__ static void store(uint64_t row, uint32_t off, T v) {
-    st(gptr_w<T>(row, off), v);
-  }
-};
-
-struct LaneMat4 {  // one matrix, only 4-byte aligned: four dword accesses
-  using T = u32x4;
-  static constexpr uint32_t bytes = 16;
-  __device__ static T ap(T a, T b) { return mat_mul(a, b); }
-  __device__ static T load(uint64_t row, uint32_t off) {
-    const DPAR_GLOBAL uint32_t* q = gptr<uint32_t>(row, off);
-    T v;
-    v.x = q[0];
-    v.y = q[1];
-    v.z = q[2];
-    v.w = q[3];
-    return v;
-  }
-  __device__ static void store(uint64_t row, uint32_t off, T v) {
-    DPAR_GLOBAL uint32_t* q = gptr_w<uint32_t>(row, off);
-    q[0] = v.x;
-    q[1] = v.y;
-    q[2] = v.z;
-    q[3] = v.w;
+    st(gptr_w<u32x4g>(row, off), (u32x4g)v);
   }
 };
 
@@ -886,6 +869,8 @@ __global__ __launch_bounds__(256) void k_bcast(const uint64_t* __restrict__ yp,
   __builtin_nontemporal_store(v,
                               reinterpret_cast<DPAR_GLOBAL T*>(yp[row] + off));
 }
+// (T = u32x4g: 16-byte lanes on rows aligned to 4 bytes; uint32_t: 4-byte
+// lanes)
 
 // ------------------------------------------------------------ host launch
 
@@ -1041,7 +1026,7 @@ hipError_t launch(Kind kind, Path path, Unit unit, int waves, Exec exec,
     case Kind::F32_SUM:
       return vec ? DPAR_LAUNCH_L(Lane4<F32Sum>) : DPAR_LAUNCH_L(Lane1<F32Sum>);
     case Kind::MAT:
-      return vec ? DPAR_LAUNCH_L(LaneMat16) : DPAR_LAUNCH_L(LaneMat4);
+      return DPAR_LAUNCH_L(LaneMat);  // 16-byte lanes on either path
   }
 #undef DPAR_LAUNCH_L
   return hipErrorInvalidValue;
@@ -1067,7 +1052,7 @@ hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
   for (uint64_t first = 0; first < g.total; first += kMaxGrid) {
     const unsigned n = (unsigned)min(kMaxGrid, g.total - first);
     if (vec16)
-      hipLaunchKernelGGL((k_bcast<u32x4>), dim3(n), dim3(256), 0, stream,
+      hipLaunchKernelGGL((k_bcast<u32x4g>), dim3(n), dim3(256), 0, stream,
                          tab.yp, g, first);
     else
       hipLaunchKernelGGL((k_bcast<uint32_t>), dim3(n), dim3(256), 0, stream,

@@ -80,9 +80,14 @@ def test_block_rule_matches_oracle():
 def test_block_decomposition(m, b, dtype, aligned):
     s = dpar.dpar_schedule_info(36, m, dtype, b, aligned)
     assert s.b == b
-    vec4 = aligned and dtype != "u32mat2x2" and m // 4 >= b
+    # 16-byte lanes whenever every block holds a whole quantum, whatever the
+    # alignment (the flag is ignored); a matrix is one quantum
+    vec4 = dtype != "u32mat2x2" and m // 4 >= b
     assert s.quantum == (4 if vec4 else 1)
-    vec = vec4 or (aligned and dtype == "u32mat2x2")
+    vec = vec4 or dtype == "u32mat2x2"
+    other = dpar.dpar_schedule_info(36, m, dtype, b, not aligned)
+    assert [getattr(other, f) for f, _ in other._fields_] == \
+        [getattr(s, f) for f, _ in s._fields_]
     lines = -(-(s.nquanta * s.quantum) // (8 * s.quantum))
     want_g = s.quantum * (8 if vec and lines >= b else 1)
     assert s.granularity == want_g
@@ -104,9 +109,12 @@ def test_block_decomposition(m, b, dtype, aligned):
     assert -(-per_block // s.chunks_per_block) <= 64 + 8
 
 
-def test_scalar_path_matches_canonical_partition():
-    m, b = 1000, 7
-    s = dpar.dpar_schedule_info(9, m, "float32", b, aligned=False)
+@pytest.mark.parametrize("m,b", [(20, 7), (27, 7), (1000, 251), (5, 5)])
+def test_scalar_path_matches_canonical_partition(m, b):
+    # blocks shorter than one quantum of 4 elements: one element per lane
+    # and Section 1.1's partition into b blocks of roughly m / b elements
+    s = dpar.dpar_schedule_info(9, m, "float32", b, aligned=True)
+    assert s.quantum == 1 and s.granularity == 1
     for j in range(b):
         assert dpar.dpar_block_bounds(s, m, j) == oracle.block_bounds(m, b, j)
 

@@ -20,7 +20,7 @@ import torch
 
 import oracle
 from synth import configs
-from tests._gpu import need_gpu, poisoned_like, to_dev, workload_input
+from tests._gpu import _Env, need_gpu, poisoned_like, to_dev, workload_input
 
 pytestmark = pytest.mark.gpu
 
@@ -146,27 +146,34 @@ def test_p1152_fp32_every_alg_and_executor(fp32_full, alg, exec):
                                     ("auto", 1), ("launch", 1)])
 def test_rows_beyond_32_bit_offsets(exec, b):
     """p = 3 rows of 2^31 + 4099 int32 (8.6 GB each, 52 GB in and out): every
-    byte offset past 2^32 goes through 64-bit address arithmetic, and the
-    rows (not 16-byte aligned) take one element per lane, so one launch of
-    all work items (split) or of one round's chunks (b = 1) would need more
-    than 2^32 threads and goes out in pieces.  Checked against the exact
-    wrapped column sum, computed on the device in int64, for every element
-    (a property that holds at any size)."""
+    byte offset past 2^32 goes through 64-bit address arithmetic.  The rows
+    (not 16-byte aligned) are taken one element per lane (DPAR_SCALAR=1), so
+    one launch of all work items (split) or of one round's chunks (b = 1)
+    would need more than 2^32 threads and goes out in pieces; then once
+    more with 16-byte lanes on the misaligned rows.  Checked against the
+    exact wrapped column sum, computed on the device in int64, for every
+    element (a property that holds at any size)."""
     from paper_2109_12626_amd import dpar
     need_gpu()
     p, m = 3, (1 << 31) + 4099
     g = torch.Generator(device="cuda").manual_seed(2170)
     xd = torch.randint(-(1 << 30), 1 << 30, (p, m), dtype=torch.int32,
                        device="cuda", generator=g)
-    yd = poisoned_like(xd)
-    s = torch.cuda.current_stream()
-    dpar.dpar_allreduce_opt(dpar.rows(xd), dpar.rows(yd), p, m, "int32",
-                            "sum", b, "dual", exec, 0, -1, s)
-    dpar.dpar_check_status(s)
     step = 1 << 28
+    wants = []
     for c in range(0, m, step):
         want = xd[:, c:c + step].to(torch.int64).sum(0)
-        want = ((want + 2 ** 31) % 2 ** 32 - 2 ** 31).to(torch.int32)
-        for i in range(p):
-            assert torch.equal(yd[i, c:c + step], want), (exec, i, c)
-    del xd, yd
+        wants.append(((want + 2 ** 31) % 2 ** 32 - 2 ** 31).to(torch.int32))
+    s = torch.cuda.current_stream()
+    for scalar in (1, 0):
+        yd = poisoned_like(xd)
+        with _Env("DPAR_SCALAR", scalar):
+            dpar.dpar_allreduce_opt(dpar.rows(xd), dpar.rows(yd), p, m,
+                                    "int32", "sum", b, "dual", exec, 0, -1, s)
+        dpar.dpar_check_status(s)
+        for k, c in enumerate(range(0, m, step)):
+            for i in range(p):
+                assert torch.equal(yd[i, c:c + step], wants[k]), \
+                    (exec, scalar, i, c)
+        del yd
+    del xd

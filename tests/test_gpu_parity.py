@@ -123,7 +123,8 @@ def test_split_broadcast_in_spans(span_kb, p, m, dtype, op, dist):
 
 
 def test_split_broadcast_unaligned_rows_in_spans():
-    """4-byte lanes (rows only 4-byte aligned) with several spans."""
+    """Rows only 4-byte aligned (16-byte lanes across cache lines) with
+    several spans."""
     p, m = 6, 30001
     x = synth.generate("normal_f32", 77, p, m)
     xd = to_dev(np.pad(x, ((0, 0), (1, 0))))
@@ -178,7 +179,8 @@ def test_b_large_uses_scalar_lanes(m, b):
 
 @pytest.mark.parametrize("offset", [4, 8, 12])
 def test_unaligned_pointers(offset):
-    # rows start 4/8/12 bytes past a 16-byte boundary: scalar lanes
+    # rows start 4/8/12 bytes past a 16-byte boundary: 16-byte lanes that
+    # straddle them
     p, m = 37, 1001
     x = synth.generate("normal_f32", 5, p, m)
     big = torch.zeros((p, m + 8), dtype=torch.float32, device="cuda")
@@ -195,6 +197,28 @@ def test_unaligned_pointers(offset):
     assert_all_ranks_equal(out, _want(x, "float32", "sum"))
     # bytes outside the rows are untouched
     assert torch.isnan(yb[:, :k]).all() and torch.isnan(yb[:, k + m:]).all()
+
+
+@pytest.mark.parametrize("exec", ["auto", "split", "ticket", "launch",
+                                  "barrier", "rounds"])
+@pytest.mark.parametrize("dtype,op,dist", [
+    ("int32", "max", "uniform_int"), ("float32", "sum", "normal_f32"),
+    ("u32mat2x2", "matmul", "odd_det_u32_mat")])
+@pytest.mark.parametrize("scalar", [0, 1])
+def test_rows_of_every_misalignment(exec, dtype, op, dist, scalar):
+    """The rows of one [p, m] tensor with m = 1 mod 4: row i starts 4 i
+    bytes (mod 16) past a 16-byte boundary, so the rows straddle cache lines
+    in every way at once; with 16-byte lanes and with one element per lane
+    (DPAR_SCALAR=1, integer and fp32 only)."""
+    p, m = 23, 4097
+    kw = {"lo": -99, "hi": 99} if dist == "uniform_int" else {}
+    x = synth.generate(dist, 3100 + p, p, m, **kw)
+    from tests._gpu import _Env
+    with _Env("DPAR_SCALAR", scalar):
+        for b in (1, 5, 300):
+            out = run(x, dtype, op, b, exec)
+            assert_all_ranks_equal(out, _want(x, dtype, op),
+                                   f"{exec} b={b} scalar={scalar}")
 
 
 def test_in_place():

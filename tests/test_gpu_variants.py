@@ -115,8 +115,9 @@ def _final_rounds(x, b, alg):
 
 def _unaligned_rows(t, m):
     """Row addresses 4 bytes into each row of a [p, m + 1] int32 tensor:
-    not 16-byte aligned, so the library takes one element per lane and the
-    canonical block partition [floor(j m / b), floor((j + 1) m / b))."""
+    not 16-byte aligned.  With m not a multiple of 4 the round-structured
+    executors take one element per lane and the canonical block partition
+    [floor(j m / b), floor((j + 1) m / b))."""
     return [a + 4 for a in lib().rows(t)]
 
 
