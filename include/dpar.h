@@ -152,7 +152,10 @@ typedef struct {
 /* Block decomposition chosen for a call (Section 1.1: b successive blocks of
  * roughly m/b elements).  A wavefront lane owns one quantum of `quantum`
  * elements: 4 (16 bytes) for INT32/FLOAT32 when every block holds at least
- * one quantum (m / 4 >= b), else 1; a matrix is one quantum.  Blocks are cut
+ * one quantum (m / 4 >= b), else 1; a matrix is one quantum.  Calls with
+ * m mod 4 != 0 that move at most 24 MB (2 p m times the element size) also
+ * take one element per lane: one launch instead of a second one for the
+ * trailing elements.  Blocks are cut
  * at multiples of `granularity` elements (lines of 8 quanta, 128 bytes, when
  * m allows b such lines, else one quantum): with
  * L = ceil(nquanta * quantum / granularity) lines, block j holds lines
@@ -254,7 +257,7 @@ int dpar_rounds(int p, int b, int rank);
 
 /* The decomposition dpar_allreduce would use for these arguments (with any
  * executor but ROUNDS / ROUNDS_BARRIER, which take one element per lane
- * when m is not a multiple of 4).  `aligned` is ignored: the decomposition
+ * whenever m is not a multiple of 4).  `aligned` is ignored: the decomposition
  * does not depend on the pointers' alignment.  b == 0 applies the rule.  No
  * device work. */
 int dpar_schedule_info(int p, size_t m, dpar_dtype_t dtype, int b, int aligned,

@@ -52,6 +52,13 @@ constexpr int kCapMinRanks = 256;
 constexpr int kCapMinItemsPerCu = 64;
 // Largest p whose post-order work items use one wavefront for both trees.
 constexpr int kOneWaveMaxRanks = 48;
+// Calls that leave trailing elements after the last 4-element quantum and
+// move at most this many bytes (2 p m times the element size) take one
+// element per lane in one launch instead of 16-byte lanes plus a launch for
+// the trailing elements (measured, int32 SUM, b = 1: p = 288, m = 8750
+// (20 MB) 20.4 vs 28.1 us; m = 21250 (49 MB) 35.8 vs 32.6 us; p = 1152,
+// m = 2125 (20 MB) 34.7 vs 38.1 us; m = 8750 (81 MB) 66.0 vs 59.0 us).
+constexpr uint64_t kScalarBelowBytes = 24ull << 20;
 // Split executor's broadcast pass: y_0 is streamed out in spans of at most
 // this many KB (2 MB per XCD's 4 MB L2; a 32 MB y_0 taken as one span ran at
 // half the speed).
@@ -434,6 +441,15 @@ int chunk_waves(int p) {
   return w == 1 ? 1 : 2;
 }
 
+// One element per lane (see allreduce_impl).
+static bool one_element_per_lane(int p, size_t m, dpar_dtype_t dtype,
+                                 bool rounds_exec) {
+  if (env_int("DPAR_SCALAR", 0) != 0) return true;
+  if (m % 4 == 0 || dtype == DPAR_U32_MAT2X2) return false;
+  return rounds_exec ||
+         2ull * (uint64_t)p * m * elem_size(dtype) <= kScalarBelowBytes;
+}
+
 // Vector path (16-byte lanes: 4 scalars or one matrix) whenever the blocks
 // hold whole quanta; rows need only the 4-byte alignment every call requires
 // (16-byte accesses at 4-byte aligned addresses: at p = 1152, m = 2^22 int32
@@ -470,7 +486,8 @@ int dpar_schedule_info(int p, size_t m, dpar_dtype_t dtype, int b, int aligned,
   dpar::Schedule s;
   dpar::Path path;
   (void)aligned;  // the decomposition does not depend on alignment
-  choose_schedule(m, dtype, b, false, &s, &path);
+  choose_schedule(m, dtype, b, one_element_per_lane(p, m, dtype, false), &s,
+                  &path);
   const dpar::Tree t = dpar::build_tree(p);
   out->b = s.b;
   out->granularity = s.g * s.lq;
@@ -671,10 +688,12 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
       return fail(DPAR_ERR_INVALID_ARG, "round range [%d, %d) beyond R = %d",
                   r0, r1, R);
   }
-  // the round-structured executors have no separate tail pass: one element
-  // per lane when 4-element quanta would leave one (DPAR_SCALAR=1: always)
-  const bool one_per_lane = (rounds_exec && m % 4 != 0) ||
-                            env_int("DPAR_SCALAR", 0) != 0;
+  // One element per lane when 4-element quanta would leave trailing
+  // elements and either the round-structured executors run (they have no
+  // separate pass for them) or the call is small enough that the launch
+  // that pass needs costs more than the wider lanes save (DPAR_SCALAR=1:
+  // always).
+  const bool one_per_lane = one_element_per_lane(p, m, dtype, rounds_exec);
   dpar::Schedule s;
   dpar::Path path;
   choose_schedule(m, dtype, b, one_per_lane, &s, &path);

@@ -81,8 +81,10 @@ def test_block_decomposition(m, b, dtype, aligned):
     s = dpar.dpar_schedule_info(36, m, dtype, b, aligned)
     assert s.b == b
     # 16-byte lanes whenever every block holds a whole quantum, whatever the
-    # alignment (the flag is ignored); a matrix is one quantum
-    vec4 = dtype != "u32mat2x2" and m // 4 >= b
+    # alignment (the flag is ignored), unless trailing elements remain and
+    # the call moves at most 24 MB; a matrix is one quantum
+    small_tail = m % 4 != 0 and 2 * 36 * m * 4 <= 24 << 20
+    vec4 = dtype != "u32mat2x2" and m // 4 >= b and not small_tail
     assert s.quantum == (4 if vec4 else 1)
     vec = vec4 or dtype == "u32mat2x2"
     other = dpar.dpar_schedule_info(36, m, dtype, b, not aligned)
@@ -107,6 +109,18 @@ def test_block_decomposition(m, b, dtype, aligned):
     # chunks: at most 64 quanta each
     per_block = -(-max(sizes) // s.quantum)
     assert -(-per_block // s.chunks_per_block) <= 64 + 8
+
+
+@pytest.mark.parametrize("p,m,quantum", [
+    (288, 8750, 1), (288, 21250, 4), (288, 21252, 4), (1152, 2125, 1),
+    (1152, 8750, 4), (1152, 2124, 4), (7, 1 << 18 | 1, 1), (2, 1572863, 1),
+    (2, 1572867, 4)])
+def test_small_calls_with_trailing_elements_take_one_element_per_lane(
+        p, m, quantum):
+    # m mod 4 != 0 and at most 24 MB moved: one launch, one element per lane
+    s = dpar.dpar_schedule_info(p, m, "int32", 1, True)
+    assert s.quantum == quantum
+    assert s.tail_elems == (m % 4 if quantum == 4 else 0)
 
 
 @pytest.mark.parametrize("m,b", [(20, 7), (27, 7), (1000, 251), (5, 5)])
