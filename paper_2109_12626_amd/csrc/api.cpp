@@ -660,6 +660,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
       (opt.round_end >= 0 && opt.round_end < opt.round_begin))
     return fail(DPAR_ERR_INVALID_ARG, "bad round range [%d, %d)",
                 opt.round_begin, opt.round_end);
+  bool rows16 = true;  // every output row starts on a 16-byte boundary
   for (int i = 0; i < p; ++i) {
     if (!x[i] || !y[i])
       return fail(DPAR_ERR_INVALID_ARG, "null buffer for rank %d", i);
@@ -667,6 +668,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     if ((a | c) & 3)
       return fail(DPAR_ERR_INVALID_ARG, "rank %d buffer not 4-byte aligned",
                   i);
+    if (c & 15) rows16 = false;
     if (((a | c) >> 48) != 0)
       return fail(DPAR_ERR_UNSUPPORTED, "rank %d address above 2^48", i);
   }
@@ -925,8 +927,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     int span_kb = env_int("DPAR_BCAST_SPAN_KB", kBcastSpanKB);
     if (span_kb <= 0) span_kb = kBcastSpanKB;
     const uint64_t span = (uint64_t)span_kb << 10;
-    e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16, span,
-                        stream);
+    e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16,
+                        rows16, span, stream);
     if (e != hipSuccess) return hip_fail(e, "broadcast launch");
   }
   if (!capturing) {  // a pinned slot is never restaged, so never waited on

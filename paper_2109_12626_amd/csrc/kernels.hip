@@ -869,8 +869,46 @@ __global__ __launch_bounds__(256) void k_bcast(const uint64_t* __restrict__ yp,
   __builtin_nontemporal_store(v,
                               reinterpret_cast<DPAR_GLOBAL T*>(yp[row] + off));
 }
-// (T = u32x4g: 16-byte lanes on rows aligned to 4 bytes; uint32_t: 4-byte
+// (T = u32x4g: 16-byte lanes on 16-byte aligned rows; uint32_t: 4-byte
 // lanes)
+
+// The same pass with 16-byte lanes for output rows that are not all 16-byte
+// aligned.  The stores of row i start at the row's own first 16-byte
+// boundary, h = ((16 - y_i mod 16) mod 16) / 4 dwords in (plan.hpp
+// bcast_row_split), so every store fills 16 aligned bytes; lane l of the
+// row's body copies dwords [h + 4 l, h + 4 l + 4), reading them from y_0 at
+// any 4-byte alignment (an L2 hit).  The h leading and the (up to 3)
+// trailing dwords are copied one dword per thread by the row's tile-0
+// workgroup.  At p = 1152, m = 2^22 with misaligned rows this pass takes
+// 3.3 ms, against 3.7 ms with stores that straddle 16-byte boundaries; on
+// 16-byte aligned rows the plain pass is faster (2.6 against 3.1 ms), so the
+// library picks this one only when some output row needs it.
+__global__ __launch_bounds__(256) void k_bcast16_rows(
+    const uint64_t* __restrict__ yp, BcastGrid g, uint64_t first) {
+  uint64_t row, tile;
+  bcast_tile(g, first + blockIdx.x, &row, &tile);     // workgroup-uniform
+  const uint64_t src = yp[0], dst = yp[row];
+  const uint64_t ndw = g.n * 4;                       // dwords per row
+  uint64_t h, nbody;
+  bcast_row_split(dst, ndw, &h, &nbody);
+  const uint64_t lane = tile * 256 + threadIdx.x;
+  if (lane < nbody) {
+    const uint64_t off = (h + 4 * lane) * 4;
+    const u32x4g v = *reinterpret_cast<const DPAR_GLOBAL u32x4g*>(src + off);
+    __builtin_nontemporal_store((u32x4)v,
+                                reinterpret_cast<DPAR_GLOBAL u32x4*>(dst + off));
+  }
+  if (tile == 0 && threadIdx.x < 8) {
+    const uint64_t t = threadIdx.x;
+    const uint64_t k = t < 4 ? t : h + 4 * nbody + (t - 4);
+    if (t < 4 ? t < h : k < ndw) {
+      const uint32_t v =
+          *reinterpret_cast<const DPAR_GLOBAL uint32_t*>(src + 4 * k);
+      __builtin_nontemporal_store(
+          v, reinterpret_cast<DPAR_GLOBAL uint32_t*>(dst + 4 * k));
+    }
+  }
+}
 
 // ------------------------------------------------------------ host launch
 
@@ -1044,15 +1082,18 @@ size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev) {
 }
 
 hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
-                     uint64_t span_bytes, hipStream_t stream) {
+                     bool rows16, uint64_t span_bytes, hipStream_t stream) {
   const BcastGrid g = bcast_grid(nbytes, vec16 ? 16 : 4, p, span_bytes);
   // a launch's thread count stays below 2^32: pieces of at most 2^23
   // workgroups (a multiple of 8, so workgroup w stays on XCD w mod 8)
   const uint64_t kMaxGrid = (1ull << 31) / 256;
   for (uint64_t first = 0; first < g.total; first += kMaxGrid) {
     const unsigned n = (unsigned)min(kMaxGrid, g.total - first);
-    if (vec16)
+    if (vec16 && rows16)
       hipLaunchKernelGGL((k_bcast<u32x4g>), dim3(n), dim3(256), 0, stream,
+                         tab.yp, g, first);
+    else if (vec16)
+      hipLaunchKernelGGL(k_bcast16_rows, dim3(n), dim3(256), 0, stream,
                          tab.yp, g, first);
     else
       hipLaunchKernelGGL((k_bcast<uint32_t>), dim3(n), dim3(256), 0, stream,

@@ -5,14 +5,53 @@
 // workgroups whose tile lies past y_0's end, and bad the workgroups that hit
 // a pair already written or a row outside 1 .. p-1.  Test infrastructure.
 #include <cstdio>
+#include <cstdlib>
+#include <string>
 #include <vector>
 
 #include "plan.hpp"
 
+static void split(unsigned long long dst, unsigned long long ndw) {
+  uint64_t h, nbody;
+  dpar::bcast_row_split(dst, ndw, &h, &nbody);
+  std::vector<int> seen(ndw, 0);
+  uint64_t twice = 0, outside = 0, misaligned = 0;
+  auto put = [&](uint64_t k) {
+    if (k >= ndw) {
+      ++outside;
+      return;
+    }
+    if (seen[k]++) ++twice;
+  };
+  for (uint64_t l = 0; l < nbody; ++l) {   // body: one 16-byte store each
+    if ((dst + 4 * (h + 4 * l)) & 15) ++misaligned;
+    for (uint64_t d = 0; d < 4; ++d) put(h + 4 * l + d);
+  }
+  for (uint64_t t = 0; t < 8; ++t) {        // the tile-0 workgroup's dwords
+    const uint64_t k = t < 4 ? t : h + 4 * nbody + (t - 4);
+    if (t < 4 ? t < h : k < ndw) put(k);
+  }
+  uint64_t covered = 0;
+  for (uint64_t k = 0; k < ndw; ++k) covered += seen[k] != 0;
+  std::printf("%llu %llu %llu %llu %llu %llu\n", (unsigned long long)h,
+              (unsigned long long)nbody, (unsigned long long)covered,
+              (unsigned long long)twice, (unsigned long long)outside,
+              (unsigned long long)misaligned);
+}
+
 int main() {
-  unsigned long long nbytes, lane, span;
-  int p;
-  while (std::scanf("%llu %llu %d %llu", &nbytes, &lane, &p, &span) == 4) {
+  char tag[32];
+  while (std::scanf("%31s", tag) == 1) {
+    if (std::string(tag) == "split") {
+      unsigned long long dst, ndw;
+      if (std::scanf("%llu %llu", &dst, &ndw) != 2) return 1;
+      split(dst, ndw);
+      continue;
+    }
+    const unsigned long long nbytes = std::strtoull(tag, nullptr, 10);
+    unsigned long long lane, span;
+    int p;
+    if (std::scanf("%llu %d %llu", &lane, &p, &span) != 3) return 1;
     const dpar::BcastGrid g = dpar::bcast_grid(nbytes, lane, p, span);
     const uint64_t tiles = (g.n + 255) / 256;
     std::vector<unsigned char> seen(g.rows * tiles, 0);

@@ -47,7 +47,7 @@ CASES = _cases()
 
 
 @pytest.fixture(scope="module")
-def grids(tmp_path_factory):
+def checker(tmp_path_factory):
     gxx = shutil.which("g++")
     if gxx is None:
         pytest.skip("g++ not available")
@@ -56,8 +56,13 @@ def grids(tmp_path_factory):
                     os.path.join(ROOT, "tests", "cpp", "bcast_check.cpp"),
                     os.path.join(CSRC, "plan.cpp"), "-o", str(exe)],
                    check=True)
+    return str(exe)
+
+
+@pytest.fixture(scope="module")
+def grids(checker):
     text = "\n".join(" ".join(map(str, c)) for c in CASES)
-    res = subprocess.run([str(exe)], input=text, capture_output=True,
+    res = subprocess.run([checker], input=text, capture_output=True,
                          text=True, check=True)
     rows = [tuple(map(int, line.split())) for line in res.stdout.splitlines()]
     assert len(rows) == len(CASES)
@@ -89,3 +94,32 @@ def test_headline_pass_is_one_span(grids):
     4096 tiles; at m = 2^23 as two."""
     assert grids[(16 * MB, 16, 1152, 16 * MB)][1:3] == (4096, 1)
     assert grids[(32 * MB, 16, 1152, 16 * MB)][1:3] == (4096, 2)
+
+
+# rows of ndw = 4 n dwords (the pass copies the n 16-byte lanes of y_0)
+SPLITS = [(base + d, ndw) for base in (0, 1 << 40) for d in (0, 4, 8, 12)
+          for ndw in (4, 8, 12, 16, 1020, 1024, 1028, 4 << 20)]
+
+
+@pytest.fixture(scope="module")
+def splits(checker):
+    text = "\n".join(f"split {d} {n}" for d, n in SPLITS)
+    res = subprocess.run([checker], input=text, capture_output=True,
+                         text=True, check=True)
+    rows = [tuple(map(int, line.split())) for line in res.stdout.splitlines()]
+    assert len(rows) == len(SPLITS)
+    return dict(zip(SPLITS, rows))
+
+
+@pytest.mark.parametrize("case", SPLITS, ids=lambda c: f"{c[0]}-{c[1]}")
+def test_row_split_writes_every_dword_once_with_aligned_stores(splits, case):
+    """Rows off 16-byte boundaries are written as leading dwords up to the
+    row's first 16-byte boundary, aligned 16-byte stores, and at most 3
+    trailing dwords: every dword of the row once, nothing outside."""
+    dst, ndw = case
+    h, nbody, covered, twice, outside, misaligned = splits[case]
+    assert h == min(((16 - dst % 16) % 16) // 4, ndw)
+    assert covered == ndw and twice == 0 and outside == 0
+    assert misaligned == 0
+    assert 0 <= ndw - h - 4 * nbody <= 3
+    assert nbody <= ndw // 4          # body lanes inside the row's grid

@@ -221,6 +221,51 @@ def test_rows_of_every_misalignment(exec, dtype, op, dist, scalar):
                                    f"{exec} b={b} scalar={scalar}")
 
 
+@pytest.mark.parametrize("span_kb", [4, 16384])
+@pytest.mark.parametrize("offset", [4, 8, 12])
+@pytest.mark.parametrize("dtype,op,dist", [
+    ("int32", "sum", "uniform_int"), ("float32", "sum", "normal_f32"),
+    ("u32mat2x2", "matmul", "odd_det_u32_mat")])
+def test_split_with_output_rows_off_16_byte_boundaries(span_kb, offset, dtype,
+                                                       op, dist):
+    """16-byte lanes on rows 4, 8 or 12 bytes past a 16-byte boundary (m a
+    multiple of 4, so no trailing elements): the broadcast pass shifts each
+    row's stores to the row's own 16-byte boundaries and copies the leading
+    and trailing dwords one by one.  Nothing outside the rows is touched."""
+    p, m = 9, 6000
+    kw = {"lo": -999, "hi": 999} if dist == "uniform_int" else {}
+    x = synth.generate(dist, 700 + offset, p, m, **kw)
+    words = 4 if dtype == "u32mat2x2" else 1
+    k = offset // 4
+    xi = np.ascontiguousarray(x).view(np.int32).reshape(p, m * words)
+    big = torch.zeros((p, m * words + 8), dtype=torch.int32, device="cuda")
+    big[:, k:k + m * words] = torch.from_numpy(xi).cuda()
+    yb = torch.full_like(big, POISON)
+    from paper_2109_12626_amd import dpar
+    xs = [a + offset for a in dpar.rows(big)]
+    ys = [a + offset for a in dpar.rows(yb)]
+    s = torch.cuda.current_stream()
+    with env_bcast_span_kb(span_kb):
+        dpar.dpar_allreduce_ex(xs, ys, p, m, dtype, op, 5, "split", s)
+    dpar.dpar_check_status(s)
+    got = yb.cpu().numpy()
+    out = got[:, k:k + m * words].copy().view(x.dtype).reshape(x.shape)
+    assert_all_ranks_equal(out, _want(x, dtype, op), f"offset {offset}")
+    assert (got[:, :k] == POISON).all() and (got[:, k + m * words:] == POISON).all()
+
+
+@pytest.mark.parametrize("exec", ["auto", "split"])
+def test_large_call_with_rows_of_every_misalignment(exec):
+    """One [4, 2^20 + 1] fp32 tensor: its rows start 0, 4, 8 and 12 bytes
+    past a 16-byte boundary and the call moves 33.5 MB, so it takes 16-byte
+    lanes plus a pass for the trailing element, and the broadcast shifts
+    every row's stores to its own boundaries."""
+    p, m = 4, (1 << 20) + 1
+    x = synth.generate("normal_f32", 4242, p, m)
+    out = run(x, "float32", "sum", 0, exec)
+    assert_all_ranks_equal(out, _want(x, "float32", "sum"), exec)
+
+
 def test_in_place():
     p, m = 64, 4099
     x = synth.generate("normal_f32", 9, p, m)
