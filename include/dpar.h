@@ -17,6 +17,9 @@
  *   - Device work is enqueued on the caller's stream and is asynchronous with
  *     respect to the host.
  *   - Nothing is written to any output on an argument error.
+ * The header is C99 and C++; like every HIP host program built without
+ * hipcc, a C or C++ consumer defines __HIP_PLATFORM_AMD__ for HIP's runtime
+ * header (e.g. gcc -D__HIP_PLATFORM_AMD__ -I/opt/rocm/include ... -ldpar).
  */
 #ifndef DPAR_H
 #define DPAR_H

@@ -25,6 +25,31 @@ def _declared():
     return sorted(set(re.findall(r"\b(dpar_[a-z_]+)\s*\(", text)))
 
 
+def test_plain_c_program_uses_the_abi(tmp_path):
+    """tests/cpp/c_consumer.c, compiled as C99 with gcc against the header
+    and linked to libdpar.so, calls the entry points that need no device and
+    gets the documented results (the boundary is a C ABI, not only a Python
+    one).  HIP's host headers need __HIP_PLATFORM_AMD__ outside hipcc."""
+    import shutil
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not available")
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    libdir = os.path.dirname(dpar.LIB_PATH)
+    exe = tmp_path / "c_consumer"
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Werror",
+                    "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+                    "-I", os.path.join(rocm, "include"),
+                    os.path.join(ROOT, "tests", "cpp", "c_consumer.c"),
+                    "-L", libdir, "-ldpar", f"-Wl,-rpath,{libdir}",
+                    "-o", str(exe)], check=True)
+    res = subprocess.run([str(exe)], capture_output=True, text=True)
+    lines = res.stdout.split("\n")
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert not [ln for ln in lines if ln.startswith("FAIL")]
+    assert sum(ln.startswith("ok ") for ln in lines) == 12
+
+
 def test_library_exports_every_declared_function():
     names = _declared()
     assert "dpar_allreduce" in names and len(names) >= 9
