@@ -64,14 +64,20 @@ def run(x, dtype, op, b, exec="auto", y=None, x_ptrs=None, y_ptrs=None,
 
 
 def assert_all_ranks_equal(out, want, what=""):
-    p = out.shape[0]
-    for i in range(p):
-        if not np.array_equal(out[i], want):
-            bad = np.argwhere(out[i] != want)
-            raise AssertionError(
-                f"{what} rank {i}: {len(bad)} elements differ, first at "
-                f"{bad[0].tolist()}: got {out[i][tuple(bad[0])]} want "
-                f"{want[tuple(bad[0])]}")
+    """Every rank's output equals want bit for bit (for fp32 that includes
+    the sign of zero)."""
+    o = np.ascontiguousarray(out).view(np.uint32)
+    w = np.ascontiguousarray(want).view(np.uint32)
+    assert o.shape[1:] == w.shape, (what, o.shape, w.shape)
+    eq = (o == w[None]).reshape(o.shape[0], -1).all(axis=1)
+    if eq.all():
+        return
+    i = int(np.argmin(eq))
+    bad = np.argwhere(o[i] != w)
+    raise AssertionError(
+        f"{what} rank {i}: {len(bad)} elements differ, first at "
+        f"{bad[0].tolist()}: got {out[i][tuple(bad[0])]} want "
+        f"{want[tuple(bad[0])]}")
 
 
 def workload_input(w, m=None, p=None):
