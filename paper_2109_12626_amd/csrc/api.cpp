@@ -660,7 +660,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
       (opt.round_end >= 0 && opt.round_end < opt.round_begin))
     return fail(DPAR_ERR_INVALID_ARG, "bad round range [%d, %d)",
                 opt.round_begin, opt.round_end);
-  bool rows16 = true;  // every output row starts on a 16-byte boundary
+  bool rows16 = true;   // every output row starts on a 16-byte boundary
+  bool xrows16 = true;  // every input row does
   for (int i = 0; i < p; ++i) {
     if (!x[i] || !y[i])
       return fail(DPAR_ERR_INVALID_ARG, "null buffer for rank %d", i);
@@ -669,6 +670,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
       return fail(DPAR_ERR_INVALID_ARG, "rank %d buffer not 4-byte aligned",
                   i);
     if (c & 15) rows16 = false;
+    if (a & 15) xrows16 = false;
     if (((a | c) >> 48) != 0)
       return fail(DPAR_ERR_UNSUPPORTED, "rank %d address above 2^48", i);
   }
@@ -883,6 +885,10 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
       lds_floor = (size_t)st->lds_per_cu / (size_t)(per_cu + 1) + 1024;
     if (lds_floor > (size_t)st->lds_limit) lds_floor = 0;
   }
+  // the split up-phase on input rows off 16-byte boundaries: each XCD takes
+  // a contiguous run of work items (plan.hpp xcd_run_index)
+  if (up == dpar::Exec::SPLIT && path == dpar::Path::VEC16 && !xrows16)
+    prm.xcd_runs = 1;
   hipError_t e = dpar::launch(kind, path, unit, waves, up, tab, prm, stream,
                               st->num_cus, lds_floor);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
@@ -899,6 +905,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     tp.C = 1;
     tp.grp = 1;
     tp.batch = 1;
+    tp.xcd_runs = 0;
     // at most 3 elements: evaluated level by level (all p loads at once)
     // where the level table exists; a post-order walk would be a chain of
     // p / 2 dependent loads (p = 288, 2125 elements: 47 us per call with

@@ -630,8 +630,10 @@ template <class U>
 __global__ __launch_bounds__(U::kThreads) void k_round(DPAR_KARGS, int round,
                                                       uint64_t first) {
   extern __shared__ char lds_raw[];
-  U::run(xp, yp, ops, lvl, prm,
-         (uint64_t)round * prm.C + first + blockIdx.x, lds_raw);
+  // in launch order, or each XCD a contiguous run of the launch's items
+  const uint64_t w =
+      prm.xcd_runs ? xcd_run_index(blockIdx.x, gridDim.x) : blockIdx.x;
+  U::run(xp, yp, ops, lvl, prm, (uint64_t)round * prm.C + first + w, lds_raw);
 }
 
 __device__ inline void grid_barrier(const Params& prm) {

@@ -71,6 +71,9 @@ struct Params {
   int dheight;          // ROUNDS: height of the real tree(s) (the kernel
                         // form of one tree with p <= 2 is lower)
   int r0, r1;           // ROUNDS: run rounds [r0, r1)
+  int xcd_runs;         // k_round: each XCD takes a contiguous run of the
+                        // launch's work items (else consecutive items go
+                        // to consecutive XCDs)
 };
 
 // Quanta per down-step piece: 64 lanes x 4 quanta per lane.
