@@ -875,16 +875,19 @@ __global__ __launch_bounds__(256) void k_bcast(const uint64_t* __restrict__ yp,
 // lanes)
 
 // The same pass with 16-byte lanes for output rows that are not all 16-byte
-// aligned.  The stores of row i start at the row's own first 16-byte
-// boundary, h = ((16 - y_i mod 16) mod 16) / 4 dwords in (plan.hpp
-// bcast_row_split), so every store fills 16 aligned bytes; lane l of the
-// row's body copies dwords [h + 4 l, h + 4 l + 4), reading them from y_0 at
-// any 4-byte alignment (an L2 hit).  The h leading and the (up to 3)
-// trailing dwords are copied one dword per thread by the row's tile-0
-// workgroup.  At p = 1152, m = 2^22 with misaligned rows this pass takes
-// 3.3 ms, against 3.7 ms with stores that straddle 16-byte boundaries; on
-// 16-byte aligned rows the plain pass is faster (2.6 against 3.1 ms), so the
-// library picks this one only when some output row needs it.
+// aligned.  The body of row i starts at the row's own first 4 KB boundary,
+// h dwords in (plan.hpp bcast_row_split), so that every store fills 16
+// aligned bytes and every workgroup's tile is whole cache lines of one
+// page; lane l of the body copies dwords [h + 4 l, h + 4 l + 4), reading
+// them from y_0 at any 4-byte alignment (an L2 hit).  The row's tile-0
+// workgroup also copies the h leading and the (up to 3) trailing dwords,
+// one dword per thread.  At p = 1152, m = 2^22 with rows 4 bytes off a
+// 16-byte boundary this pass takes 3.0 ms, against 3.7 ms with stores that
+// straddle 16-byte boundaries, 3.3 ms with the body shifted to the next
+// 16-byte boundary and 3.06 ms to the next 128-byte line (tiles straddling
+// cache lines leave partial lines to two workgroups); on 16-byte aligned
+// rows the plain pass is faster (2.6 against 3.1 ms), so the library picks
+// this one only when some output row needs it.
 __global__ __launch_bounds__(256) void k_bcast16_rows(
     const uint64_t* __restrict__ yp, BcastGrid g, uint64_t first) {
   uint64_t row, tile;
@@ -900,15 +903,14 @@ __global__ __launch_bounds__(256) void k_bcast16_rows(
     __builtin_nontemporal_store((u32x4)v,
                                 reinterpret_cast<DPAR_GLOBAL u32x4*>(dst + off));
   }
-  if (tile == 0 && threadIdx.x < 8) {
-    const uint64_t t = threadIdx.x;
-    const uint64_t k = t < 4 ? t : h + 4 * nbody + (t - 4);
-    if (t < 4 ? t < h : k < ndw) {
-      const uint32_t v =
-          *reinterpret_cast<const DPAR_GLOBAL uint32_t*>(src + 4 * k);
-      __builtin_nontemporal_store(
-          v, reinterpret_cast<DPAR_GLOBAL uint32_t*>(dst + 4 * k));
-    }
+  if (tile == 0) {
+    const DPAR_GLOBAL uint32_t* a =
+        reinterpret_cast<const DPAR_GLOBAL uint32_t*>(src);
+    DPAR_GLOBAL uint32_t* d = reinterpret_cast<DPAR_GLOBAL uint32_t*>(dst);
+    for (uint64_t k = threadIdx.x; k < h; k += 256)    // leading dwords
+      __builtin_nontemporal_store(a[k], d + k);
+    const uint64_t k = h + 4 * nbody + threadIdx.x;    // trailing dwords
+    if (threadIdx.x < 4 && k < ndw) __builtin_nontemporal_store(a[k], d + k);
   }
 }
 

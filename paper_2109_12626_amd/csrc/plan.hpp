@@ -211,15 +211,16 @@ DPAR_HOST_DEVICE inline void bcast_tile(const BcastGrid& g, uint64_t w,
   *tile = span * g.ts + r % g.ts;
 }
 
-// Row split of the broadcast for rows that do not start on a 16-byte
-// boundary: a row of ndw dwords (a multiple of 4: the pass copies whole
-// 16-byte lanes of y_0) at byte address dst (4-byte aligned) is written as
-// h leading dwords (up to the first 16-byte boundary), nbody aligned 16-byte
-// quanta [h + 4 l, h + 4 l + 4) for l < nbody, and the ndw - h - 4 nbody (at
-// most 3) trailing dwords.
+// Row split of the broadcast for output rows that do not all start on
+// 16-byte boundaries: a row of ndw dwords (a multiple of 4: the pass copies
+// whole 16-byte lanes of y_0) at byte address dst (4-byte aligned) is
+// written as h leading dwords, up to the row's first 4 KB boundary, then
+// nbody 16-byte quanta [h + 4 l, h + 4 l + 4) for l < nbody, which start on
+// that boundary, so that every workgroup's 4 KB tile is whole cache lines
+// of one page, and then the ndw - h - 4 nbody (at most 3) trailing dwords.
 DPAR_HOST_DEVICE inline void bcast_row_split(uint64_t dst, uint64_t ndw,
                                              uint64_t* h, uint64_t* nbody) {
-  const uint64_t lead = ((16 - (dst & 15)) & 15) >> 2;
+  const uint64_t lead = ((4096 - (dst & 4095)) & 4095) >> 2;
   *h = lead < ndw ? lead : ndw;
   *nbody = (ndw - *h) >> 2;
 }

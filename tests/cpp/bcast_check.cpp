@@ -25,12 +25,12 @@ static void split(unsigned long long dst, unsigned long long ndw) {
   };
   for (uint64_t l = 0; l < nbody; ++l) {   // body: one 16-byte store each
     if ((dst + 4 * (h + 4 * l)) & 15) ++misaligned;
+    if (l % 256 == 0 && ((dst + 4 * (h + 4 * l)) & 4095)) ++misaligned;
     for (uint64_t d = 0; d < 4; ++d) put(h + 4 * l + d);
   }
-  for (uint64_t t = 0; t < 8; ++t) {        // the tile-0 workgroup's dwords
-    const uint64_t k = t < 4 ? t : h + 4 * nbody + (t - 4);
-    if (t < 4 ? t < h : k < ndw) put(k);
-  }
+  for (uint64_t k = 0; k < h; ++k) put(k);  // the tile-0 workgroup's dwords
+  for (uint64_t t = 0; t < 4; ++t)
+    if (h + 4 * nbody + t < ndw) put(h + 4 * nbody + t);
   uint64_t covered = 0;
   for (uint64_t k = 0; k < ndw; ++k) covered += seen[k] != 0;
   std::printf("%llu %llu %llu %llu %llu %llu\n", (unsigned long long)h,

@@ -97,8 +97,9 @@ def test_headline_pass_is_one_span(grids):
 
 
 # rows of ndw = 4 n dwords (the pass copies the n 16-byte lanes of y_0)
-SPLITS = [(base + d, ndw) for base in (0, 1 << 40) for d in (0, 4, 8, 12)
-          for ndw in (4, 8, 12, 16, 1020, 1024, 1028, 4 << 20)]
+SPLITS = [(base + d, ndw) for base in (0, 1 << 40, 4096 * 7 + 128)
+          for d in (0, 4, 8, 12, 132, 4092)
+          for ndw in (4, 8, 12, 16, 1020, 1024, 1028, 4096, 4 << 20)]
 
 
 @pytest.fixture(scope="module")
@@ -114,11 +115,12 @@ def splits(checker):
 @pytest.mark.parametrize("case", SPLITS, ids=lambda c: f"{c[0]}-{c[1]}")
 def test_row_split_writes_every_dword_once_with_aligned_stores(splits, case):
     """Rows off 16-byte boundaries are written as leading dwords up to the
-    row's first 16-byte boundary, aligned 16-byte stores, and at most 3
-    trailing dwords: every dword of the row once, nothing outside."""
+    row's first 4 KB boundary, 16-byte stores from there (each workgroup's
+    4 KB tile starting on a 4 KB boundary), and at most 3 trailing dwords:
+    every dword of the row once, nothing outside."""
     dst, ndw = case
     h, nbody, covered, twice, outside, misaligned = splits[case]
-    assert h == min(((16 - dst % 16) % 16) // 4, ndw)
+    assert h == min(((4096 - dst % 4096) % 4096) // 4, ndw)
     assert covered == ndw and twice == 0 and outside == 0
     assert misaligned == 0
     assert 0 <= ndw - h - 4 * nbody <= 3
