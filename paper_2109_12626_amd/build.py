@@ -29,19 +29,25 @@ def _run(cmd):
     subprocess.run(cmd, check=True)
 
 
-def build(verbose=True, out=None, defines=()):
+def build(verbose=True, out=None, defines=(), host_sanitize=False):
     """Compiles libdpar.so (or ``out``); ``defines`` are extra -D flags for
-    kernel experiments."""
+    kernel experiments.  ``host_sanitize``: the host C++ (plan.cpp, api.cpp
+    and the host side of the launches) built with AddressSanitizer and
+    UndefinedBehaviorSanitizer, for CPU runs of the no-device entry points
+    (needs ``out``; load it with libasan and libubsan preloaded)."""
+    if host_sanitize and out is None:
+        raise ValueError("a sanitized build needs its own output path")
     build_dir = BUILD if out is None else os.path.dirname(out) + "/_obj"
     os.makedirs(build_dir, exist_ok=True)
     inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC,
            "-I", os.path.join(ROCM, "include")]
     hipcc = os.path.join(ROCM, "bin", "hipcc")
     objs = []
+    san = ["-fsanitize=address,undefined", "-g"] if host_sanitize else []
     for src in ("plan.cpp", "api.cpp"):
         obj = os.path.join(build_dir, src + ".o")
-        _run(["g++"] + HOST_FLAGS + inc + ["-c", os.path.join(CSRC, src),
-                                           "-o", obj])
+        _run(["g++"] + HOST_FLAGS + san + inc +
+             ["-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     obj = os.path.join(build_dir, "kernels.hip.o")
     _run([hipcc] + HIP_FLAGS + [f"-D{d}" for d in defines] + inc
@@ -49,8 +55,10 @@ def build(verbose=True, out=None, defines=()):
     objs.append(obj)
     lib = LIB if out is None else out
     tmp = lib + ".tmp"
-    _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp]
-         + objs + ["-Wl,-soname,libdpar.so"])
+    link_san = (["-Xarch_host", "-fsanitize=address",
+                 "-Xarch_host", "-fsanitize=undefined"] if host_sanitize else [])
+    _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}"] + link_san
+         + ["-o", tmp] + objs + ["-Wl,-soname,libdpar.so"])
     os.replace(tmp, lib)
     if out is None:
         build_probe(build_dir, inc)
