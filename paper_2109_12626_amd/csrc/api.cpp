@@ -848,6 +848,21 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   if (unit == dpar::Unit::SUB) {
     tab.lvl = ops->sub;
     prm.nslots = ops->sub_ns;
+    // One launch of subtree work items has fewer than two per CU, all
+    // resident at once, so its items need not follow the blocks: the
+    // columns are cut into whole chunks of 64 quanta, as with b = 1 (at
+    // p = 1152, m = 2^16, b = 817: 256 items instead of 273 groups of three
+    // blocks, 0.079 -> 0.063 ms for the up-phase).  Element-wise, so the
+    // result does not depend on the cut.
+    if (ex == dpar::Exec::SPLIT || ex == dpar::Exec::DISPATCH ||
+        ex == dpar::Exec::TICKET) {
+      const dpar::Schedule s1 = dpar::make_schedule(m, 1, s.g, 8);
+      prm.b = 1;
+      prm.NL = s1.NL;
+      prm.lq = (uint32_t)s1.lq;
+      prm.C = s1.C;
+      prm.grp = 1;
+    }
   }
   // round-structured down-step: two ranks per wavefront per work item, the
   // largest block in pieces of kDownPiece quanta
