@@ -597,11 +597,20 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
                          ex == dpar::Exec::ROUNDS_BARRIER;
   const uint64_t all_items = grouped_units(s, grp);
   const uint64_t items = per_round ? (uint64_t)s.C : all_items;
+  const bool whole_call = ex == dpar::Exec::SPLIT ||
+                          ex == dpar::Exec::TICKET ||
+                          ex == dpar::Exec::DISPATCH;
+  const size_t lane_bytes =
+      (path == dpar::Path::VEC16 || kind == dpar::Kind::MAT) ? 16 : 4;
+  bool want_sub = whole_call && p >= 256 && all_items < 2 * cus &&
+                  s.Q >= 32 * all_items && ops.sub &&
+                  dpar::sub_lds_bytes(lane_bytes, ops.sub_ns) <=
+                      (size_t)st.lds_limit - dpar::kStaticLdsReserve;
   if (ops.lvl) {
     int tmax = -1;
     for (int lg = 6; lg >= 0; --lg) {
       if (dpar::level_lds_bytes(path, kind, p, lg, ops.height + 1) <=
-          (size_t)st.lds_limit) {
+          (size_t)st.lds_limit - dpar::kStaticLdsReserve) {
         tmax = lg;
         break;
       }
@@ -616,23 +625,28 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
           ((s.NL * (uint64_t)grp + s.b - 1) / s.b) * (uint64_t)s.lq;
       int lg = 0;
       while (lg < tmax && (1ull << lg) < maxq) ++lg;
-      uc.unit = dpar::Unit::LEVEL;
-      uc.lv_log2t = lg;
-      uc.lv_C = (int)((maxq + (1ull << lg) - 1) >> lg);
-      return uc;
+      const int lv_C = (int)((maxq + (1ull << lg) - 1) >> lg);
+      // At large p a level item holds only a few quanta of each row; when
+      // that takes more than two level items per CU and the subtree item
+      // can take the call, it is faster (p = 2304, m = 2^14, b = 1:
+      // 1024 level items 0.200 ms, 64 subtree items 0.116 ms; p = 4608:
+      // 0.494 vs 0.213 ms; p = 1152 keeps level items: 512 of them,
+      // 0.054 vs 0.068 ms).
+      const uint64_t groups =
+          per_round ? 1 : ((uint64_t)s.b + (uint64_t)grp - 1) / (uint64_t)grp;
+      const bool crowded = groups * (uint64_t)lv_C > 2 * cus;
+      if (forced || !(crowded && want_sub)) {
+        uc.unit = dpar::Unit::LEVEL;
+        uc.lv_log2t = lg;
+        uc.lv_C = lv_C;
+        return uc;
+      }
     }
   }
-  const bool whole_call = ex == dpar::Exec::SPLIT ||
-                          ex == dpar::Exec::TICKET ||
-                          ex == dpar::Exec::DISPATCH;
-  bool want_sub = whole_call && p >= 256 && all_items < 2 * cus &&
-                  s.Q >= 32 * all_items;
-  if (forced) want_sub = !std::strcmp(u, "sub");
-  const size_t lane_bytes =
-      (path == dpar::Path::VEC16 || kind == dpar::Kind::MAT) ? 16 : 4;
-  if (want_sub && ops.sub &&
-      dpar::sub_lds_bytes(lane_bytes, ops.sub_ns) <= (size_t)st.lds_limit)
-    uc.unit = dpar::Unit::SUB;
+  if (forced) want_sub = !std::strcmp(u, "sub") && ops.sub &&
+                         dpar::sub_lds_bytes(lane_bytes, ops.sub_ns) <=
+                             (size_t)st.lds_limit - dpar::kStaticLdsReserve;
+  if (want_sub) uc.unit = dpar::Unit::SUB;
   return uc;
 }
 
@@ -931,7 +945,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     const bool level =
         p >= 2 && ops->lvl &&
         dpar::level_lds_bytes(dpar::Path::SCALAR, kind, p, tp.lv_log2t,
-                              tp.nlev) <= (size_t)st->lds_limit;
+                              tp.nlev) <=
+            (size_t)st->lds_limit - dpar::kStaticLdsReserve;
     e = dpar::launch(kind, dpar::Path::SCALAR,
                      level ? dpar::Unit::LEVEL : dpar::Unit::SEQ, waves,
                      dpar::Exec::LAUNCH_PER_ROUND, tt, tp, stream,

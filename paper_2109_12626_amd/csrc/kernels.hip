@@ -1018,7 +1018,8 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
     return hipLaunchCooperativeKernel(kfn, dim3((unsigned)grid), block, args,
                                       (unsigned)lds, stream);
   }
-  if (per_cu < 1) per_cu = 1;
+  // no workgroup fits (dynamic plus static LDS beyond a CU's): never launch
+  if (per_cu < 1) return hipErrorInvalidConfiguration;
   uint64_t grid = (uint64_t)per_cu * num_cus;
   const uint64_t batches = (nunits + prm.batch - 1) / prm.batch;
   if (grid > batches) grid = batches;

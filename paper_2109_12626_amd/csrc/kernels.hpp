@@ -108,6 +108,14 @@ hipError_t launch(Kind kind, Path path, Unit unit, int waves, Exec exec,
                   const Tables& tab, const Params& prm, hipStream_t stream,
                   int num_cus, size_t lds_floor);
 
+// LDS a work item's dynamic request must leave free for the kernels' own
+// static LDS (the ticket executor's claim word): the host compares
+// requests with the device limit minus this.  (A subtree plan needing
+// exactly the 160 KB limit once went to the ticket kernel, whose claim word
+// then did not fit; the launch ran with an invalid LDS allocation and
+// faulted.)
+constexpr size_t kStaticLdsReserve = 256;
+
 // Bytes of dynamic LDS a LEVEL work item needs.
 size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev);
 
