@@ -582,8 +582,9 @@ struct UnitChoice {
 //   SUB   eight subtree walks, then the spines: a whole call (split,
 //         ticket, one fused launch) in fewer than two full chunks per CU
 //         with p >= 256 (p = 1152,
-//         m = 2^16, b = 1: 0.113 vs 0.165 ms); not for per-round executors
-//         or short chunks, where it loses.
+//         m = 2^16, b = 1: 0.113 vs 0.165 ms), and in place of LEVEL at
+//         p >= 256 when the level plan needs more than two items per CU; not
+//         for per-round executors or short chunks, where it loses.
 UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
                        dpar::Path path, dpar::Kind kind, int p,
                        const OpsTable& ops, const DeviceState& st) {
@@ -804,12 +805,11 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   prm.qbase = 0;
   prm.b = s.b;
   prm.C = s.C;
-  prm.grp = 1;
-  // short work items (few ranks) are claimed several at a time, so that the
-  // ticket counter is not the bottleneck; at most 1/2 of a fair share
   const dpar::Exec ex = device_exec(exec, p, 2ull * p * m * esz);
   prm.grp = block_group(ex, s);
   {
+    // short work items (few ranks) are claimed several at a time, so that
+    // the ticket counter is not the bottleneck; at most 1/2 of a fair share
     const uint64_t units = grouped_units(s, prm.grp);
     uint64_t k = (512 + (uint64_t)p - 1) / (uint64_t)p;
     const uint64_t fair = units / (2ull * 4 * (uint64_t)st->num_cus);
