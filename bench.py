@@ -21,6 +21,7 @@ Prints ONE JSON line.  Extra lines go to stderr.
   python bench.py --read-probe      # read rates of the up-phase's pattern
   python bench.py --write-probe     # write rates of broadcast shapes
   python bench.py --table2          # the paper's Table 2 counts at p = 288
+  python bench.py --copy-compare    # calls beside a device copy of their bytes
 """
 
 import argparse
@@ -375,6 +376,77 @@ def table2():
     print(json.dumps({"table2_p": p, "block": blk, "rows": out}))
 
 
+COPY_COMPARE = [  # p, m, dtype, op
+    (36, 1 << 20, "int32", "sum"),
+    (64, 1 << 18, "u32mat2x2", "matmul"),
+    (1152, 1 << 16, "int32", "sum"),
+    (1152, 1 << 16, "int32", "max"),
+    (1152, 1 << 18, "float32", "sum"),
+    (1152, 1 << 22, "float32", "sum"),
+]
+
+
+def copy_compare():
+    """The library's call (default executor, b from the sqrt(m log2 p)
+    rule) beside a plain device copy of the same bytes (torch's copy_ of the
+    [p, m] input into the [p, m] output: p*m*e read, p*m*e written, as the
+    call moves).  Both back to back on warm caches, the minimum and median of
+    20 timed calls after 3 untimed ones."""
+    import numpy as np
+    import torch
+
+    from paper_2109_12626_amd import dpar
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(2109)
+    out = []
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        ts = []
+        for _ in range(20):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return min(ts), float(np.median(ts))
+
+    for p, m, dt, op in COPY_COMPARE:
+        words = m * (4 if dt == "u32mat2x2" else 1)
+        if dt == "float32":
+            x = torch.randn(p, words, device=dev, generator=g)
+        else:
+            x = torch.randint(-2 ** 31, 2 ** 31 - 1, (p, words),
+                              dtype=torch.int32, device=dev, generator=g)
+        y = torch.empty_like(x)
+        xs, ys = dpar.pointers(dpar.rows(x)), dpar.pointers(dpar.rows(y))
+        b = dpar.dpar_block_rule(p, m)
+        nbytes = 2 * x.numel() * 4
+
+        def call():
+            dpar.dpar_allreduce(xs, ys, p, m, dt, op, b, stream)
+        lib_t = timed(call)
+        dpar.dpar_check_status(stream)
+        assert bool((y[:, :4096] == y[0, :4096]).all()), (p, m, dt, op)
+        copy_t = timed(lambda: y.copy_(x))
+        rec = {"p": p, "m": m, "dtype": dt, "op": op, "b": b,
+               "bytes": nbytes,
+               "call_ms": [round(lib_t[0], 4), round(lib_t[1], 4)],
+               "copy_ms": [round(copy_t[0], 4), round(copy_t[1], 4)],
+               "call_GBs": round(nbytes / lib_t[0] / 1e6, 1),
+               "copy_GBs": round(nbytes / copy_t[0] / 1e6, 1)}
+        out.append(rec)
+        log(json.dumps(rec))
+        del x, y
+        torch.cuda.empty_cache()
+    print(json.dumps({"copy_compare": out}))
+
+
 def sweep(out_path, only=(), execs=("split", "ticket", "launch", "barrier"),
           algs=("dual",)):
     """Every workload x executor x block count, cold caches (a 512 MiB
@@ -481,6 +553,8 @@ def main():
                     help="write rates of broadcast shapes")
     ap.add_argument("--read-probe", action="store_true",
                     help="HBM read rates of the up-phase's access pattern")
+    ap.add_argument("--copy-compare", action="store_true",
+                    help="calls beside a plain device copy of their bytes")
     ap.add_argument("--sweep", metavar="OUT_JSONL",
                     help="measure every workload, executor and block count")
     ap.add_argument("--only", default="",
@@ -522,6 +596,9 @@ def main():
         return
     if args.table2:
         table2()
+        return
+    if args.copy_compare:
+        copy_compare()
         return
     if args.sweep:
         sweep(args.sweep, [v for v in args.only.split(",") if v],
