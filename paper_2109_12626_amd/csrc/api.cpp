@@ -50,6 +50,8 @@ constexpr int kStageSlots = 8;
 constexpr int kSeqWgPerCu = 4;
 constexpr int kCapMinRanks = 256;
 constexpr int kCapMinItemsPerCu = 64;
+// Ticket executor: rank loads per claimed batch of work items.
+constexpr uint64_t kTicketRankLoads = 1024;
 // Largest p whose post-order work items use one wavefront for both trees.
 constexpr int kOneWaveMaxRanks = 48;
 // Calls that leave trailing elements after the last 4-element quantum and
@@ -808,11 +810,17 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   const dpar::Exec ex = device_exec(exec, p, 2ull * p * m * esz);
   prm.grp = block_group(ex, s);
   {
-    // short work items (few ranks) are claimed several at a time, so that
-    // the ticket counter is not the bottleneck; at most 1/2 of a fair share
+    // Work items per ticket: a claim is an atomic at device scope, whose
+    // round trip costs about as much as a short work item, so items of few
+    // ranks are claimed several at a time (about kTicketRankLoads rank loads
+    // per claim), leaving at least two batches per CU (measured, ticket
+    // executor, b = 1: p = 36, m = 2^20 int32 0.224 / 0.144 / 0.103 /
+    // 0.140 ms with 1 / 2 / 8 / 16 items per claim; p = 64, m = 2^18
+    // matrices 0.283 / 0.208 / 0.179 / 0.195 ms; p = 1152, m = 2^16 one item
+    // 0.120 ms, two 0.156 ms).
     const uint64_t units = grouped_units(s, prm.grp);
-    uint64_t k = (512 + (uint64_t)p - 1) / (uint64_t)p;
-    const uint64_t fair = units / (2ull * 4 * (uint64_t)st->num_cus);
+    uint64_t k = (kTicketRankLoads + (uint64_t)p - 1) / (uint64_t)p;
+    const uint64_t fair = units / (2ull * (uint64_t)st->num_cus);
     if (k > fair) k = fair;
     if (k < 1) k = 1;
     prm.batch = (unsigned)env_int("DPAR_TICKET_BATCH", (int)k);

@@ -236,6 +236,22 @@ def test_subtree_unit_chosen_with_a_tail(m):
             assert_all_ranks_equal(out, want, f"auto unit {exec} m={m}")
 
 
+@pytest.mark.parametrize("p,m", [(2304, 1 << 14), (4608, 1 << 14),
+                                 (4608, (1 << 13) + 3), (1152, 1 << 14)])
+def test_unit_rule_at_large_p(p, m):
+    """The library's own work-item choice where a level plan would need
+    more than two items per CU (p = 2304 and 4608: subtree items) and where
+    it would not (p = 1152: level items), for the block rule and b = 1."""
+    need_gpu()
+    x = _input("normal_f32", 2131 + p, p, m)
+    want = _want(x, "float32", "sum", "dual")
+    with env_unit(None):
+        for b in (1, 0):
+            for exec in ("auto", "split", "ticket"):
+                out = from_dev(_run(x, "float32", "sum", b, "dual", exec), x)
+                assert_all_ranks_equal(out, want, f"{exec}/p={p}/m={m}/b={b}")
+
+
 _LARGE_P = {}
 
 
