@@ -252,6 +252,22 @@ def test_unit_rule_at_large_p(p, m):
                 assert_all_ranks_equal(out, want, f"{exec}/p={p}/m={m}/b={b}")
 
 
+@pytest.mark.parametrize("k", [None, 1, 3, 8, 64])
+@pytest.mark.parametrize("p,m,b", [(36, 70001, 7), (64, 20483, 1),
+                                   (300, 9001, 13)])
+def test_ticket_batches(k, p, m, b):
+    """The ticket executor with several work items per claim, including
+    batch counts that do not divide the number of items: every item is
+    evaluated exactly once whatever the batch."""
+    need_gpu()
+    from tests._gpu import _Env
+    x = _input("normal_f32", 2133 + p, p, m)
+    want = _want(x, "float32", "sum", "dual")
+    with _Env("DPAR_TICKET_BATCH", k):
+        out = from_dev(_run(x, "float32", "sum", b, "dual", "ticket"), x)
+    assert_all_ranks_equal(out, want, f"ticket k={k} p={p} m={m} b={b}")
+
+
 _LARGE_P = {}
 
 
