@@ -289,6 +289,8 @@ const char* dpar_last_error(void);
  * them changes what a call computes:
  *   DPAR_UNIT=seq|level|sub force the post-order, level or subtree work
  *                           item
+ *   DPAR_LEVEL_LOG2T=k      level work items of 2^k quanta (at most what
+ *                           fits in LDS)
  *   DPAR_WAVES=1|2          wavefronts per post-order work item (default
  *                           1 for p <= 48, else 2)
  *   DPAR_TICKET_BATCH=k     work items claimed per ticket (TICKET)

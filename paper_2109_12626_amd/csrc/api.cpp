@@ -50,6 +50,8 @@ constexpr int kStageSlots = 8;
 constexpr int kSeqWgPerCu = 4;
 constexpr int kCapMinRanks = 256;
 constexpr int kCapMinItemsPerCu = 64;
+// Level work item: loads in flight at once (1024 threads, 8 loads each).
+constexpr uint64_t kLvLoadsInFlight = 1024 * 8;
 // Ticket executor: rank loads per claimed batch of work items.
 constexpr uint64_t kTicketRankLoads = 1024;
 // Largest p whose post-order work items use one wavefront for both trees.
@@ -626,18 +628,33 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
       // a power of two
       const uint64_t maxq =
           ((s.NL * (uint64_t)grp + s.b - 1) / s.b) * (uint64_t)s.lq;
-      int lg = 0;
-      while (lg < tmax && (1ull << lg) < maxq) ++lg;
-      const int lv_C = (int)((maxq + (1ull << lg) - 1) >> lg);
+      // the largest chunk that fits LDS and the block (group)
+      int lg_max = 0;
+      while (lg_max < tmax && (1ull << lg_max) < maxq) ++lg_max;
+      auto chunks = [&](int l) { return (maxq + (1ull << l) - 1) >> l; };
+      const uint64_t groups =
+          per_round ? 1 : ((uint64_t)s.b + (uint64_t)grp - 1) / (uint64_t)grp;
       // At large p a level item holds only a few quanta of each row; when
       // that takes more than two level items per CU and the subtree item
       // can take the call, it is faster (p = 2304, m = 2^14, b = 1:
       // 1024 level items 0.200 ms, 64 subtree items 0.116 ms; p = 4608:
       // 0.494 vs 0.213 ms; p = 1152 keeps level items: 512 of them,
       // 0.054 vs 0.068 ms).
-      const uint64_t groups =
-          per_round ? 1 : ((uint64_t)s.b + (uint64_t)grp - 1) / (uint64_t)grp;
-      const bool crowded = groups * (uint64_t)lv_C > 2 * cus;
+      const bool crowded = groups * chunks(lg_max) > 2 * cus;
+      // Chunk used: the largest whose p * T loads are all in flight at once
+      // (1024 threads with kLvBatch loads each), larger only while the items
+      // outnumber the CUs.  Measured, int32 SUM, one fused launch: p = 288,
+      // m = 875: T = 64 (the largest that fits) 19.4 us, T = 16 14.5 us;
+      // m = 25: 15.5 vs 14.2 us; p = 1152, m = 16, b = 13: 19.7 vs
+      // 15.3 us; p = 1152, m = 4096: T = 2 (512 items) 41.2 us, T = 4
+      // 20.6 us.
+      int lg = 0;
+      while (lg < lg_max && ((uint64_t)p << (lg + 1)) <= kLvLoadsInFlight)
+        ++lg;
+      while (lg < lg_max && groups * chunks(lg) > cus) ++lg;
+      const int forced_lg = env_int("DPAR_LEVEL_LOG2T", -1);
+      if (forced_lg >= 0) lg = std::min(forced_lg, tmax);
+      const int lv_C = (int)chunks(lg);
       if (forced || !(crowded && want_sub)) {
         uc.unit = dpar::Unit::LEVEL;
         uc.lv_log2t = lg;
