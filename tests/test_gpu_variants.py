@@ -268,6 +268,25 @@ def test_ticket_batches(k, p, m, b):
     assert_all_ranks_equal(out, want, f"ticket k={k} p={p} m={m} b={b}")
 
 
+@pytest.mark.parametrize("p,m,b", [(288, 875, 1), (1152, 16, 13),
+                                   (300, 4099, 3), (97, 2501, 2)])
+def test_level_chunk_sizes(p, m, b):
+    """Level work items of every chunk size from 1 to 64 quanta (forced),
+    the library's own choice included: bit-identical fp32 results."""
+    need_gpu()
+    from tests._gpu import _Env
+    x = _input("normal_f32", 2135 + p, p, m)
+    want = _want(x, "float32", "sum", "dual")
+    with env_unit("level"):
+        for lg in (None, 0, 1, 2, 3, 4, 5, 6):
+            with _Env("DPAR_LEVEL_LOG2T", lg):
+                for exec in ("auto", "ticket", "launch"):
+                    out = from_dev(_run(x, "float32", "sum", b, "dual", exec),
+                                   x)
+                    assert_all_ranks_equal(out, want,
+                                           f"lg={lg} {exec} p={p} m={m}")
+
+
 _LARGE_P = {}
 
 
