@@ -88,3 +88,46 @@ def test_random_combination(k):
             np.all(t[off + m * words:] == POISON), (str(c), i)
     got = np.stack(rows).view(x.dtype).reshape(x.shape)
     assert_all_ranks_equal(got, want, str(c))
+
+
+def _large_case(k):
+    r = np.random.default_rng(9500 + k)
+    p = int(r.integers(257, 5001))
+    dtype, op, dist = PAIRS[int(r.integers(len(PAIRS)))]
+    words = 4 if dtype == "u32mat2x2" else 1
+    # at most 2^22 words of input, so that each case stays small
+    m = int(r.integers(1, max(2, min(20000, (1 << 22) // (p * words)))))
+    b = int(r.choice([0, 1, 2, int(r.integers(1, m + 1))]))
+    return dict(p=p, m=m, b=min(b, m), dtype=dtype, op=op, dist=dist,
+                alg=ALGS[int(r.integers(3))],
+                exec=["auto", "split", "ticket", "launch"][int(r.integers(4))],
+                unit=UNITS[int(r.integers(len(UNITS)))], seed=2600 + k)
+
+
+@pytest.mark.parametrize("k", range(40))
+def test_random_large_p(k):
+    """Seeded random calls at p = 257 .. 5000 (deeper trees, the subtree
+    and level work items and their chunk choices): bit for bit against the
+    oracle, with the library's own choices and with forced work items."""
+    need_gpu()
+    dpar = lib()
+    c = _large_case(k)
+    p, m = c["p"], c["m"]
+    kw = {"lo": -50, "hi": 50} if c["dist"] == "uniform_int" else {}
+    x = synth.generate(c["dist"], c["seed"], p, m, **kw)
+    trees = oracle.build_trees(p) if c["alg"] == "dual" else \
+        oracle.build_trees(p, layout="single")
+    want = oracle.allreduce_tree(x, c["dtype"], c["op"], trees=trees)
+    a = np.ascontiguousarray(x)
+    if a.dtype == np.uint32:
+        a = a.view(np.int32)
+    xd = torch.from_numpy(a).cuda()
+    yd = torch.full_like(xd, POISON)
+    s = torch.cuda.current_stream()
+    with env_unit(c["unit"]):
+        dpar.dpar_allreduce_opt(dpar.rows(xd), dpar.rows(yd), p, m,
+                                c["dtype"], c["op"], c["b"], c["alg"],
+                                c["exec"], 0, -1, s)
+    dpar.dpar_check_status(s)
+    got = yd.cpu().numpy().view(x.dtype).reshape(x.shape)
+    assert_all_ranks_equal(got, want, str(c))
