@@ -291,6 +291,9 @@ const char* dpar_last_error(void);
  *                           item
  *   DPAR_LEVEL_LOG2T=k      level work items of 2^k quanta (at most what
  *                           fits in LDS)
+ *   DPAR_SUB_DEEP=0|1       subtree work items with 8 or 16 loads in flight
+ *                           per wavefront (default 16 from p = 1024 on when
+ *                           the call has at most one item per CU)
  *   DPAR_WAVES=1|2          wavefronts per post-order work item (default
  *                           1 for p <= 48, else 2)
  *   DPAR_TICKET_BATCH=k     work items claimed per ticket (TICKET)

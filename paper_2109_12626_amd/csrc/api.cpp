@@ -50,6 +50,8 @@ constexpr int kStageSlots = 8;
 constexpr int kSeqWgPerCu = 4;
 constexpr int kCapMinRanks = 256;
 constexpr int kCapMinItemsPerCu = 64;
+// Subtree work items: the deep load pipeline from this many ranks on.
+constexpr int kSubDeepMinRanks = 1024;
 // Level work item: loads in flight at once (1024 threads, 8 loads each).
 constexpr uint64_t kLvLoadsInFlight = 1024 * 8;
 // Ticket executor: rank loads per claimed batch of work items.
@@ -902,6 +904,18 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
       prm.C = s1.C;
       prm.grp = 1;
     }
+    // Long parts and at most one item per CU: a deeper load pipeline per
+    // wavefront shortens the chains (its registers leave room for one
+    // subtree workgroup per CU instead of two).  Measured, int32 SUM, split:
+    // p = 2304, m = 2^14: 0.112 -> 0.101 ms; p = 4608, m = 2^14: 0.210 ->
+    // 0.188 ms; p = 1152, m = 2^14, b = 207: 0.064 -> 0.060 ms; with 384
+    // items at p = 1152 (residency halved) 5% slower, at p <= 576 1-3%.
+    const uint64_t sub_items =
+        ((uint64_t)prm.b + (uint64_t)prm.grp - 1) / (uint64_t)prm.grp *
+        (uint64_t)prm.C;
+    prm.sub_deep = env_int("DPAR_SUB_DEEP",
+                           p >= kSubDeepMinRanks &&
+                               sub_items <= (uint64_t)st->num_cus);
   }
   // round-structured down-step: two ranks per wavefront per work item, the
   // largest block in pieces of kDownPiece quanta

@@ -188,6 +188,10 @@ __device__ __host__ inline uint64_t item_groups(const Params& prm) {
 #endif
 constexpr int kU = DPAR_KU;
 static_assert(2 * kU <= kTablePad, "tables are padded for 2 * kU reads");
+// The subtree work item's deep variant (Params::sub_deep): 16 loads in flight
+// per wavefront, for calls whose items all run at once, one per CU.
+constexpr int kUDeep = 16;
+static_assert(2 * kUDeep <= kTablePad, "tables are padded for 2 * kU reads");
 
 // Up-step of one chunk over the ranks [r0, r1) in post-order (Algorithm 1's
 // "Y <- t (.) Y" with the first child's block, then with the second
@@ -200,7 +204,7 @@ static_assert(2 * kU <= kTablePad, "tables are padded for 2 * kU reads");
 // entries, so reading kU entries ahead stays inside them; ranks past r1
 // re-read row r1 - 1 (cache hits) and are not processed.  Returns the value
 // of the last rank walked.
-template <class L>
+template <class L, int KU = kU>
 __device__ __forceinline__ typename L::T walk(const uint64_t* __restrict__ xp,
                                               const uint32_t* __restrict__ ops,
                                               int r0, int r1,
@@ -221,27 +225,27 @@ __device__ __forceinline__ typename L::T walk(const uint64_t* __restrict__ xp,
     last = v;
   };
   const uint64_t last_row = xp[r1 - 1] + unit_off;
-  T buf[kU];
+  T buf[KU];
 #pragma unroll
-  for (int k = 0; k < kU; ++k) {
+  for (int k = 0; k < KU; ++k) {
     const uint64_t row = xp[r0 + k] + unit_off;
     buf[k] = L::load(r0 + k < r1 ? row : last_row, lane_off);
     // keep the loads in slot order: the wait before consuming slot k then
     // only needs the oldest load, in the prologue and in the loop alike
     __builtin_amdgcn_sched_barrier(0);
   }
-  for (int rb = r0; rb < r1; rb += kU) {
-    uint64_t next_row[kU];
-    uint32_t op[kU];
+  for (int rb = r0; rb < r1; rb += KU) {
+    uint64_t next_row[KU];
+    uint32_t op[KU];
 #pragma unroll
-    for (int k = 0; k < kU; ++k) {
-      next_row[k] = xp[rb + kU + k] + unit_off;
+    for (int k = 0; k < KU; ++k) {
+      next_row[k] = xp[rb + KU + k] + unit_off;
       op[k] = ops[rb + k];
     }
 #pragma unroll
-    for (int k = 0; k < kU; ++k) {
+    for (int k = 0; k < KU; ++k) {
       const T v = buf[k];
-      buf[k] = L::load(rb + kU + k < r1 ? next_row[k] : last_row, lane_off);
+      buf[k] = L::load(rb + KU + k < r1 ? next_row[k] : last_row, lane_off);
       __builtin_amdgcn_sched_barrier(0);
       if (rb + k < r1) step(v, op[k]);
     }
@@ -466,7 +470,7 @@ size_t sub_lds_bytes(size_t lane_bytes, int ns) {
 //
 // LDS: slots [kSubParts][NS][64] | part values [kSubParts][64] | spine
 // blocks [2][kSubSpineRanks][64].
-template <class L, bool FUSED>
+template <class L, bool FUSED, int KU>
 __device__ __forceinline__ void run_unit_sub(const uint64_t* __restrict__ xp,
                                              const uint64_t* __restrict__ yp,
                                              const uint32_t* __restrict__ ops,
@@ -510,7 +514,7 @@ __device__ __forceinline__ void run_unit_sub(const uint64_t* __restrict__ xp,
     const int base = (int)parts[3 * wave + 2];
     T cur = T{};
     pval[(size_t)wave * 64 + lane] =
-        walk<L>(xp, ops, lo, hi + 1, unit_off, lane_off, my, base, cur);
+        walk<L, KU>(xp, ops, lo, hi + 1, unit_off, lane_off, my, base, cur);
   }
   if (wave < 2) {
 #pragma unroll
@@ -585,7 +589,7 @@ struct SeqUnit {
   }
 };
 
-template <class L, bool FUSED>
+template <class L, bool FUSED, int KU = kU>
 struct SubUnit {
   using Lane = L;
   static constexpr int kThreads = 64 * kSubParts;
@@ -594,8 +598,8 @@ struct SubUnit {
                              const uint32_t* __restrict__ ops,
                              const uint32_t* __restrict__ lvl,
                              const Params& prm, uint64_t t, char* lds) {
-    run_unit_sub<L, FUSED>(xp, yp, ops, lvl, prm, t,
-                           reinterpret_cast<typename L::T*>(lds));
+    run_unit_sub<L, FUSED, KU>(xp, yp, ops, lvl, prm, t,
+                               reinterpret_cast<typename L::T*>(lds));
   }
   static size_t lds(const Params& prm) {
     return sub_lds_bytes(sizeof(typename L::T), prm.nslots);
@@ -1042,9 +1046,13 @@ hipError_t launch_l(Unit unit, int waves, Exec exec, const Tables& tab,
   if (unit == Unit::LEVEL)
     return fused ? DPAR_LAUNCH_U(LvUnit<L, true>)
                  : DPAR_LAUNCH_U(LvUnit<L, false>);
-  if (unit == Unit::SUB)
+  if (unit == Unit::SUB) {
+    if (prm.sub_deep)
+      return fused ? DPAR_LAUNCH_U(SubUnit<L, true, kUDeep>)
+                   : DPAR_LAUNCH_U(SubUnit<L, false, kUDeep>);
     return fused ? DPAR_LAUNCH_U(SubUnit<L, true>)
                  : DPAR_LAUNCH_U(SubUnit<L, false>);
+  }
   if (waves == 2)
     return fused ? DPAR_LAUNCH_U(SeqUnit<L, 2, true>)
                  : DPAR_LAUNCH_U(SeqUnit<L, 2, false>);

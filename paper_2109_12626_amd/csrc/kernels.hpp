@@ -74,6 +74,9 @@ struct Params {
   int xcd_runs;         // k_round: each XCD takes a contiguous run of the
                         // launch's work items (else consecutive items go
                         // to consecutive XCDs)
+  int sub_deep;         // SUB: the parts are walked with 16 loads in flight
+                        // per wavefront instead of 8 (host-side choice of
+                        // the kernel)
 };
 
 // Quanta per down-step piece: 64 lanes x 4 quanta per lane.

@@ -287,6 +287,22 @@ def test_level_chunk_sizes(p, m, b):
                                            f"lg={lg} {exec} p={p} m={m}")
 
 
+@pytest.mark.parametrize("deep", [0, 1])
+@pytest.mark.parametrize("p,m,b", [(1152, 16387, 1), (2304, 8192, 3),
+                                   (300, 5001, 2), (4099, 4096, 1)])
+def test_subtree_unit_load_depths(deep, p, m, b):
+    """Subtree work items with 8 and with 16 loads in flight per wavefront
+    (forced either way), including a ragged m: bit-identical fp32."""
+    need_gpu()
+    from tests._gpu import _Env
+    x = _input("normal_f32", 2137 + p, p, m)
+    want = _want(x, "float32", "sum", "dual")
+    with env_unit("sub"), _Env("DPAR_SUB_DEEP", deep):
+        for exec in ("split", "ticket", "auto"):
+            out = from_dev(_run(x, "float32", "sum", b, "dual", exec), x)
+            assert_all_ranks_equal(out, want, f"deep={deep} {exec} p={p}")
+
+
 _LARGE_P = {}
 
 
