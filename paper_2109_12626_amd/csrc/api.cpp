@@ -586,11 +586,12 @@ struct UnitChoice {
 //         post-order item costs its p/2-load chain however little it
 //         carries: p = 1152, m = 4096, b = 205: 117 us post-order, 31 level);
 //   SUB   eight subtree walks, then the spines: a whole call (split,
-//         ticket, one fused launch) in fewer than two full chunks per CU
-//         with p >= 256 (p = 1152,
-//         m = 2^16, b = 1: 0.113 vs 0.165 ms), and in place of LEVEL at
-//         p >= 256 when the level plan needs more than two items per CU; not
-//         for per-round executors or short chunks, where it loses.
+//         ticket, one fused launch) in at most two full chunks per CU
+//         with p >= 256 (p = 1152, m = 2^16, b = 1: 0.113 vs 0.165 ms;
+//         two per CU, p = 1152, m = 2^17: 0.240 vs 0.260 ms), and in
+//         place of LEVEL at p >= 256 when the level plan needs more than
+//         two items per CU; not for per-round executors or short chunks,
+//         where it loses.
 UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
                        dpar::Path path, dpar::Kind kind, int p,
                        const OpsTable& ops, const DeviceState& st) {
@@ -609,8 +610,10 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
                           ex == dpar::Exec::DISPATCH;
   const size_t lane_bytes =
       (path == dpar::Path::VEC16 || kind == dpar::Kind::MAT) ? 16 : 4;
-  bool want_sub = whole_call && p >= 256 && all_items < 2 * cus &&
-                  s.Q >= 32 * all_items && ops.sub &&
+  // a one-launch subtree run cuts the columns into whole chunks of 64
+  // quanta, whatever the blocks (see allreduce_impl): count those
+  const uint64_t sub_items = (s.Q + 63) / 64;
+  bool want_sub = whole_call && p >= 256 && sub_items <= 2 * cus && ops.sub &&
                   dpar::sub_lds_bytes(lane_bytes, ops.sub_ns) <=
                       (size_t)st.lds_limit - dpar::kStaticLdsReserve;
   if (ops.lvl) {
