@@ -17,9 +17,6 @@ Prints ONE JSON line.  Extra lines go to stderr.
   python bench.py --calib-copy      # a plain 4 GiB device copy, for the
                                     # rocprofv3 FETCH/WRITE calibration
   python bench.py --sweep OUT.jsonl # every workload, executor, block count
-  python bench.py --stream-probe    # plain fill / sum / copy rates
-  python bench.py --read-probe      # read rates of the up-phase's pattern
-  python bench.py --write-probe     # write rates of broadcast shapes
   python bench.py --table2          # the paper's Table 2 counts at p = 288
   python bench.py --copy-compare    # calls beside a device copy of their bytes
 """
@@ -103,206 +100,6 @@ def calib_copy():
         b.copy_(a)
     torch.cuda.synchronize()
     print(json.dumps({"calib_copy_bytes": n * 4, "dispatches": 3}))
-
-
-def stream_probe():
-    """HBM stream rates of plain library kernels on 8 GiB buffers: a
-    write-only fill, a read-only reduction and a copy (each timed alone, the
-    minimum of 5), for comparison with the two phases of the reduction."""
-    import torch
-    n = 1 << 31                     # 8 GiB of fp32
-    a = torch.ones(n, dtype=torch.float32, device="cuda")
-    b = torch.empty_like(a)
-    out = {}
-
-    def rate(name, fn, nbytes):
-        ts = []
-        for _ in range(6):
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record()
-            fn()
-            e1.record()
-            torch.cuda.synchronize()
-            ts.append(e0.elapsed_time(e1))
-        ms = min(ts[1:])
-        out[name] = {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1)}
-
-    rate("write (fill_)", lambda: b.fill_(2.0), n * 4)
-    rate("read (sum)", lambda: a.sum(), n * 4)
-    rate("copy (copy_, read + write bytes)", lambda: b.copy_(a), 2 * n * 4)
-    print(json.dumps({"stream_probe_bytes": n * 4, "rates": out}))
-
-
-def read_probe():
-    """HBM read rates of the up-phase's access pattern and of plain
-    contiguous reads (libdpar_probe.so, measurement kernels that read and
-    XOR), beside the library's own up-phase on the same box: 19.33 GB read
-    each time, the minimum of 5 timed launches after one untimed one."""
-    import ctypes
-
-    import torch
-
-    from paper_2109_12626_amd import build as pbuild
-    from paper_2109_12626_amd import dpar
-    if not os.path.exists(pbuild.PROBE_LIB):
-        raise RuntimeError(f"{pbuild.PROBE_LIB} is missing: run build() first")
-    lib = ctypes.CDLL(pbuild.PROBE_LIB)
-    vp, ull = ctypes.c_void_p, ctypes.c_ulonglong
-    lib.dpar_probe_rows.argtypes = [vp, ull, ctypes.c_int, ull, ctypes.c_int,
-                                    ctypes.c_int, vp, vp]
-    lib.dpar_probe_tiles.argtypes = [vp, ull, ull, vp, vp]
-    rowb, pad = M * ELEM, 4096
-    total = P * rowb
-    x = torch.ones(P * (rowb + pad) // 4, dtype=torch.float32, device="cuda")
-    sink = torch.zeros(256, dtype=torch.float32, device="cuda")
-    stream = torch.cuda.current_stream()
-    sv = ctypes.c_void_p(stream.cuda_stream)
-    out = []
-
-    def timed(name, fn, nbytes=total):
-        ts = []
-        for _ in range(6):
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            rc = fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            if rc != 0:
-                raise RuntimeError(f"{name}: probe returned {rc}")
-            ts.append(e0.elapsed_time(e1))
-        ms = min(ts[1:])
-        out.append({"pattern": name, "ms": round(ms, 4),
-                    "GB/s": round(nbytes / ms / 1e6, 1)})
-        log(json.dumps(out[-1]))
-
-    def rows(p, stride, row_bytes, qpl, waves):
-        return lambda: lib.dpar_probe_rows(x.data_ptr(), stride, p, row_bytes,
-                                           qpl, waves, sink.data_ptr(), sv)
-
-    for qpl, waves in ((1, 2), (2, 2), (4, 2), (1, 8)):
-        timed(f"rows p=1152 x 16 MB, {qpl} KB per row visit, {waves} "
-              "wavefronts per workgroup", rows(P, rowb, rowb, qpl, waves))
-    for waves in (2, 8):
-        timed(f"rows p=1152 x 16 MB, rows 16 MB + 4 KB apart, 1 KB per row "
-              f"visit, {waves} wavefronts", rows(P, rowb + pad, rowb, 1, waves))
-    for p in (18, 36, 144, 576, 4608, 9216):
-        rb = total // p
-        timed(f"rows p={p} x {rb >> 20} MB, 1 KB per row visit, 8 wavefronts",
-              rows(p, rb, rb, 1, 8))
-    for mul in (1, 5, 65537, 1000003):
-        timed(f"16 KB tiles, one short workgroup each, tile order g * {mul} "
-              "mod tiles", lambda: lib.dpar_probe_tiles(
-                  x.data_ptr(), total, mul, sink.data_ptr(), sv))
-
-    # the library's up-phase on the same shape (inputs all 1.0: the values
-    # do not change the time), y_0's write included in the bytes
-    y = torch.empty(P * rowb // 4, dtype=torch.float32, device="cuda")
-    xs = dpar.pointers([x.data_ptr() + i * rowb for i in range(P)])
-    ys = dpar.pointers([y.data_ptr() + i * rowb for i in range(P)])
-    b = dpar.dpar_block_rule(P, M)
-    ups = []
-    for _ in range(6):
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        dpar.dpar_set_phase_event(e1)
-        dpar.dpar_allreduce(xs, ys, P, M, "float32", "sum", b, stream)
-        torch.cuda.synchronize()
-        ups.append(e0.elapsed_time(e1))
-    dpar.dpar_check_status(stream)
-    ms = min(ups[1:])
-    out.append({"pattern": f"the library's up-phase (split executor, b={b})",
-                "ms": round(ms, 4), "GB/s": round((total + rowb) / ms / 1e6, 1)})
-    log(json.dumps(out[-1]))
-    print(json.dumps({"read_probe_bytes": total, "rates": out}))
-
-
-def write_probe():
-    """Write rates of the broadcast pass's shape and of alternatives to it
-    (libdpar_probe.so dpar_probe_bcast): row 0 of a [1152, 2^22] fp32
-    buffer copied into the other 1151 rows, 19.31 GB written each time, the
-    minimum and median of 10 timed launches after two untimed ones, two
-    passes over the variants; then the library's own broadcast pass on the
-    same shape."""
-    import ctypes
-
-    import torch
-
-    from paper_2109_12626_amd import build as pbuild
-    from paper_2109_12626_amd import dpar
-    if not os.path.exists(pbuild.PROBE_LIB):
-        raise RuntimeError(f"{pbuild.PROBE_LIB} is missing: run build() first")
-    lib = ctypes.CDLL(pbuild.PROBE_LIB)
-    lib.dpar_probe_bcast.argtypes = [ctypes.c_void_p, ctypes.c_ulonglong,
-                                     ctypes.c_int, ctypes.c_int,
-                                     ctypes.c_void_p]
-    rowb = M * ELEM
-    y = torch.ones(P, M, dtype=torch.float32, device="cuda")
-    stream = torch.cuda.current_stream()
-    sv = ctypes.c_void_p(stream.cuda_stream)
-    nbytes = (P - 1) * rowb
-    names = {0: "256 threads, 4 KB tiles, 1 streaming store per thread "
-                "(the library's shape)",
-             1: "as 0, each XCD's tiles from its own eighth of the row",
-             2: "256 threads, 8 KB tiles, 2 stores per thread",
-             3: "256 threads, 4 KB tiles, the tile into 2 rows",
-             4: "128 threads, 2 KB tiles",
-             5: "as 0 with ordinary stores",
-             6: "512 threads, 8 KB tiles"}
-    out = []
-
-    def timed(name, fn):
-        ts = []
-        for k in range(12):
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            rc = fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            if rc != 0:
-                raise RuntimeError(f"{name}: probe returned {rc}")
-            if k >= 2:
-                ts.append(e0.elapsed_time(e1))
-        ts.sort()
-        rec = {"shape": name, "ms_min": round(ts[0], 4),
-               "ms_median": round(ts[len(ts) // 2], 4),
-               "GB/s": round(nbytes / ts[0] / 1e6, 1)}
-        out.append(rec)
-        log(json.dumps(rec))
-
-    for _ in range(2):
-        for v, name in names.items():
-            timed(name, lambda v=v: lib.dpar_probe_bcast(
-                y.data_ptr(), rowb, P, v, sv))
-    # the library's broadcast pass: the call's second kernel, timed between
-    # the phase event and the end of the call
-    ys = dpar.pointers(dpar.rows(y))
-    ts = []
-    for k in range(12):
-        e1 = torch.cuda.Event(enable_timing=True)
-        e2 = torch.cuda.Event(enable_timing=True)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        dpar.dpar_set_phase_event(e1)
-        dpar.dpar_allreduce(ys, ys, P, M, "float32", "sum", 6532, stream)
-        e2.record(stream)
-        torch.cuda.synchronize()
-        if k >= 2:
-            ts.append(e1.elapsed_time(e2))
-    dpar.dpar_check_status(stream)
-    ts.sort()
-    out.append({"shape": "the library's broadcast pass (split executor, "
-                         "in place)",
-                "ms_min": round(ts[0], 4),
-                "ms_median": round(ts[len(ts) // 2], 4),
-                "GB/s": round(nbytes / ts[0] / 1e6, 1)})
-    log(json.dumps(out[-1]))
-    print(json.dumps({"write_probe_bytes": nbytes, "rates": out}))
 
 
 # Per-process counts of the paper's Table 2 (Section 2): int32 elements.
@@ -545,14 +342,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true")
-    ap.add_argument("--stream-probe", action="store_true",
-                    help="HBM write / read / copy rates of plain kernels")
     ap.add_argument("--table2", action="store_true",
                     help="the paper's Table 2 counts at p = 288")
-    ap.add_argument("--write-probe", action="store_true",
-                    help="write rates of broadcast shapes")
-    ap.add_argument("--read-probe", action="store_true",
-                    help="HBM read rates of the up-phase's access pattern")
     ap.add_argument("--copy-compare", action="store_true",
                     help="calls beside a plain device copy of their bytes")
     ap.add_argument("--sweep", metavar="OUT_JSONL",
@@ -584,15 +375,6 @@ def main():
         sys.exit(2)
     if args.calib_copy:
         calib_copy()
-        return
-    if args.stream_probe:
-        stream_probe()
-        return
-    if args.read_probe:
-        read_probe()
-        return
-    if args.write_probe:
-        write_probe()
         return
     if args.table2:
         table2()

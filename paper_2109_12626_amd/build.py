@@ -60,25 +60,7 @@ def build(verbose=True, out=None, defines=(), host_sanitize=False):
     _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}"] + link_san
          + ["-o", tmp] + objs + ["-Wl,-soname,libdpar.so"])
     os.replace(tmp, lib)
-    if out is None:
-        build_probe(build_dir, inc)
     return lib
-
-
-PROBE_LIB = os.path.join(HERE, "libdpar_probe.so")
-
-
-def build_probe(build_dir, inc):
-    """libdpar_probe.so: the read-pattern measurement kernels that
-    ``bench.py --read-probe`` times (not used by the reduction)."""
-    hipcc = os.path.join(ROCM, "bin", "hipcc")
-    obj = os.path.join(build_dir, "probe.hip.o")
-    _run([hipcc] + HIP_FLAGS + inc
-         + ["-c", os.path.join(CSRC, "probe.hip"), "-o", obj])
-    tmp = PROBE_LIB + ".tmp"
-    _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp,
-          obj, "-Wl,-soname,libdpar_probe.so"])
-    os.replace(tmp, PROBE_LIB)
 
 
 if __name__ == "__main__":

@@ -312,39 +312,3 @@ def test_work_item_limit_is_checked_before_narrowing():
     ys = [A + (2 << 41), A + (3 << 41)]
     assert _err(dpar.dpar_allreduce_ex, xs, ys, 2, 1 << 39, "int32", "sum", 1,
                 "split") == dpar.DPAR_ERR_UNSUPPORTED
-
-
-def test_probe_library_exports_and_checks_arguments():
-    """The measurement library behind ``bench.py --read-probe`` and
-    ``--write-probe``: every probe is exported and rejects invalid shapes
-    before touching the device."""
-    import ctypes
-    from paper_2109_12626_amd import build as pbuild
-    text = open(os.path.join(ROOT, "paper_2109_12626_amd", "csrc",
-                             "probe.h")).read()
-    text = re.sub(r"//[^\n]*", "", text)
-    names = sorted(set(re.findall(r"\b(dpar_probe_[a-z_]+)\s*\(", text)))
-    assert names == ["dpar_probe_bcast", "dpar_probe_rows", "dpar_probe_tiles"]
-    L = ctypes.CDLL(pbuild.PROBE_LIB)
-    vp, ull, ci = ctypes.c_void_p, ctypes.c_ulonglong, ctypes.c_int
-    L.dpar_probe_rows.argtypes = [vp, ull, ci, ull, ci, ci, vp, vp]
-    L.dpar_probe_tiles.argtypes = [vp, ull, ull, vp, vp]
-    fake = 1 << 40      # never dereferenced: every case fails its checks
-    rows = L.dpar_probe_rows
-    assert rows(None, 4096, 4, 4096, 1, 2, fake, None) == -1       # no base
-    assert rows(fake, 4096, 1, 4096, 1, 2, fake, None) == -1       # p < waves
-    assert rows(fake, 2048, 4, 4096, 1, 2, fake, None) == -1       # row > stride
-    assert rows(fake, 4096, 4, 3072, 2, 2, fake, None) == -1       # not whole chunks
-    assert rows(fake, 4096, 4, 4096, 2, 8, fake, None) == -1       # no such variant
-    assert rows(fake, 1 << 36, 4, 1 << 36, 1, 2, fake, None) == -1  # grid too big
-    tiles = L.dpar_probe_tiles
-    assert tiles(fake, 16384 * 6, 3, fake, None) == -1            # not coprime
-    assert tiles(fake, 16385, 1, fake, None) == -1                # not whole tiles
-    assert tiles(fake, 16384, 1, None, None) == -1                # no sink
-    L.dpar_probe_bcast.argtypes = [vp, ull, ci, ci, vp]
-    bc = L.dpar_probe_bcast
-    assert bc(None, 32768, 4, 0, None) == -1                      # no base
-    assert bc(fake, 32768, 1, 0, None) == -1                      # p < 2
-    assert bc(fake, 16384, 4, 0, None) == -1                      # not 32 KB rows
-    assert bc(fake, 32768, 4, 7, None) == -1                      # no such variant
-    assert bc(fake, 1 << 34, 1 << 20, 4, None) == -1              # grid too big
