@@ -111,11 +111,18 @@ typedef enum {
  *                     becomes final in round j + d_i (REDUCE_BCAST: j for
  *                     the root, b + j + d_i - 1 otherwise).
  *   ROUNDS_BARRIER    the same rounds in one persistent (co-resident) launch
- *                     with a device-wide barrier between rounds.  A barrier
- *                     that gives up (DPAR_ERR_TIMEOUT) leaves this
- *                     executor's outputs undefined.
+ *                     with a device-wide barrier between rounds.
  * These two read each rank's block from its parent's output, so their HBM
  * traffic is about 1.5 times the others'.
+ * Every wait at a device-wide barrier is bounded (DPAR_SPIN_LIMIT polls).  A
+ * wait that gives up ends the waiting of the rest of that call (its later
+ * barriers pass at once), sets a device-wide report flag that
+ * dpar_check_status returns as DPAR_ERR_TIMEOUT, and leaves the outputs of a
+ * ROUNDS_BARRIER call undefined; a GRID_BARRIER call's outputs are still
+ * complete, since its work items are independent and the barrier only
+ * orders the rounds.  Each call of these two executors starts from barrier
+ * words of its own, zeroed before its launch, so a wait that gave up never
+ * affects another call.
  * GRID_BARRIER and ROUNDS_BARRIER need every workgroup of their grid resident
  * at once (a cooperative launch sized to that): do not run them while other
  * work occupies the GPU, e.g. on a concurrent stream.  The other executors
@@ -270,9 +277,10 @@ int dpar_schedule_info(int p, size_t m, dpar_dtype_t dtype, int b, int aligned,
 int dpar_block_bounds(const dpar_schedule_t* s, size_t m, int j, size_t* start,
                       size_t* end);
 
-/* Waits for the stream, then reports a grid-barrier watchdog expiry recorded
- * by an earlier GRID_BARRIER call on this device (DPAR_ERR_TIMEOUT, flag
- * cleared) or a pending HIP error. */
+/* Waits for the stream, then reports a grid-barrier wait that gave up in an
+ * earlier GRID_BARRIER or ROUNDS_BARRIER call on this device since the last
+ * report (DPAR_ERR_TIMEOUT, returned once: the flag is cleared), or a pending
+ * HIP error. */
 int dpar_check_status(hipStream_t stream);
 
 /* Profiling aid: records `ev` on the call's stream between the up-phase and

@@ -34,8 +34,9 @@ independent columns):
 Parity status: every function here is pinned by ``tests/test_oracle_*.py``
 (hand-derived worked examples, closed forms, brute force, the error bound of
 recursive summation and the independent Algorithm-1 simulation).  The
-``wbal`` tree shape is an experiment only and is "parity unpinned" beyond its
-p=9 structure.
+``wbal`` tree shape (an experiment only) is pinned by its p=9 structure, a
+hand-derived fp32 value and the invariants that fix it for every p up to 257
+and larger sizes up to 2000.
 """
 
 from .trees import Trees, build_trees, heap_postorder_tree

@@ -1,40 +1,51 @@
-"""Literal rendezvous simulation of Algorithm 1 (Section 1.1).
+"""Round-by-round simulation of the doubly-pipelined dual-root schedule
+(Section 1.1), stated per tree edge.
 
 Oracle module: test infrastructure only.
 
-Every virtual rank runs the per-processor program of Algorithm 1 as a Python
-generator on its own pipelining array Y (initialised to x_i) and a temporary
-t.  Each communication step is a telephone-model bidirectional exchange: the
-rank yields (partner, kind, round, block it sends) and is resumed with the
-block the partner sent.  A scheduler pairs the k-th exchange of A with B with
-the k-th exchange of B with A (the order MPI's Sendrecv matching would
-impose) and checks that both sides are in the same round and agree on the
-kind of step.  Nothing is reordered: a rank only advances when its partner
-is ready.
+What Section 1.1 defines, restated as traffic on the edges of the trees:
 
-Per round j = 0 .. b + d_i the program is:
+* Rank i keeps an array Y of the b blocks, starting as x_i.  Its depth is
+  d_i (roots 0, children one deeper than their parent).
+* In round j every tree edge (parent q, child c) carries one bidirectional
+  exchange.  Upwards goes the child's block j, which by then holds the
+  product over the child's whole subtree for that block; the parent folds it
+  into its own block j from the left (first child's block first, then the
+  second child's), so that S(q) = S(c1) (.) (S(c0) (.) x_q).  Downwards goes
+  the parent's block j - d_c, which holds the final result y for that block:
+  it reached the parent one round earlier.  The child stores it.
+* In round j the two roots exchange block j, once both hold their tree's
+  product for it, and both end with y[j] = S(root A) (.) S(root B) (the
+  lower-numbered root computes mine (.) received, the other received (.)
+  mine).
+* Blocks outside [0, b) are empty: an exchange that would move only empty
+  blocks carries nothing (Section 1.3 sends and receives zero-element blocks
+  and stops after the last real one), and is skipped with
+  ``skip_void=True``.
 
-1. with child0: send Y[j - (d_i + 1)], receive t, then Y[j] <- t (.) Y[j];
-2. with child1: the same;
-3. a root exchanges Y[j] with its dual and combines, the lower-numbered root
-   as Y[j] (.) t and the higher one as t (.) Y[j]; any other rank sends Y[j]
-   to its parent and receives Y[j - d_i] from it.
+A rank takes its exchanges of a round in the order first child, second
+child, then parent (or dual), and its exchanges with a partner are
+rendezvous: the simulation processes a round edge by edge from the deepest
+edges up, then the root pair, so every block sent up is complete when it
+leaves, and every block sent down was made final in an earlier round (this
+is checked).  An exchange happens when both ends reach it; a rank whose
+partner never takes part (it has stopped, or is itself stuck) waits forever
+and takes no further step, and the run ends in a DeadlockError naming every
+waiting rank.
 
-Blocks outside [0, b) are the paper's zero-element virtual blocks.  With
-``skip_void=True`` an exchange in which both the sent and the received block
-are virtual is not performed (Section 1.3: the implementation sends and
-receives zero-element blocks and stops after the last non-empty block from
-the parent, so such exchanges carry nothing).  With ``skip_void=False`` the
-loop bound is taken literally and every exchange is attempted; the scheduler
-then reports the deadlock this causes.
+``skip_void=False`` has every rank attempt an exchange on each of its edges
+in every round j = 0 .. b + d_i, empty or not, as a loop bound of b + d_i
+rounds taken literally would: a deepest leaf then attempts round b + d_i
+with a parent whose rounds ended one earlier, and waits forever.
+``fail=(rank, round)`` stops one rank at the start of that round.
 
-``fail=(rank, round)`` stops one rank at the start of that round, to show
-which ranks the blocking exchanges leave stuck.
+The result is a round-by-round schedule, independent of the recursive
+evaluation in ``reduce.allreduce_tree``; the tests compare the two bit for
+bit.
 """
 
-from collections import deque
 from dataclasses import dataclass, field
-from typing import Dict, List, Optional
+from typing import Dict, List
 
 from .blocks import block_bounds
 from .ops import combine
@@ -42,8 +53,8 @@ from .trees import build_trees
 
 
 class DeadlockError(RuntimeError):
-    """Raised when no pending exchange can be paired.  ``blocked`` maps each
-    stuck rank to (partner, kind, round)."""
+    """Raised when some rank waits for an exchange its partner never takes
+    part in.  ``blocked`` maps each waiting rank to (partner, kind, round)."""
 
     def __init__(self, blocked):
         self.blocked = blocked
@@ -52,32 +63,22 @@ class DeadlockError(RuntimeError):
 
 
 class ProtocolError(RuntimeError):
-    pass
-
-
-@dataclass
-class _Req:
-    partner: int
-    kind: str            # "child", "parent" or "dual" (the step's role)
-    round: int
-    send_j: int          # index of the block sent (may be virtual)
-    recv_j: int          # index of the block expected back
-    payload: object      # array or None for a virtual block
+    """The schedule would move a block that is not ready."""
 
 
 @dataclass
 class Trace:
     """What the simulation recorded, per rank.  ``final_round[i][k]`` is the
     round in which block k of rank i took its final value y[k]: for a
-    non-root the round of the parent exchange that delivered it, for a root
-    the round in which it finished Y[k] (after the dual exchange, if any)."""
+    non-root the round in which it came down from the parent, for a root the
+    round in which it finished Y[k] (after the dual exchange, if any)."""
     active_rounds: Dict[int, List[int]] = field(default_factory=dict)
     exchanges: Dict[int, int] = field(default_factory=dict)
     ops_per_round: Dict[int, Dict[int, int]] = field(default_factory=dict)
     steps_per_round: Dict[int, Dict[int, int]] = field(default_factory=dict)
     final_round: Dict[int, Dict[int, int]] = field(default_factory=dict)
-    # per rank, every exchange in order: (round, kind, partner, block sent,
-    # block received), a block index None where it is virtual
+    # per rank, every exchange in the order the rank takes them: (round,
+    # kind, partner, block sent, block received), None for an empty block
     exchange_log: Dict[int, List[tuple]] = field(default_factory=dict)
 
     def span(self, i: int) -> int:
@@ -91,131 +92,131 @@ class Trace:
 
 def simulate(x, dtype: str, op: str, b: int, trees=None,
              skip_void: bool = True, fail=None):
-    """Run Algorithm 1 for all ranks.  Returns (Y, trace) where Y[i] is rank
+    """Run the schedule for all ranks.  Returns (Y, trace) where Y[i] is rank
     i's final array."""
-    rows = [x[i].copy() for i in range(len(x))]
-    p = len(rows)
-    m = rows[0].shape[0]
+    Y = [x[i].copy() for i in range(len(x))]
+    p = len(Y)
+    m = Y[0].shape[0]
     t = trees if trees is not None else build_trees(p)
     if not (0 < b <= max(m, 1)):
         raise ValueError("need 0 < b <= m")
     trace = Trace()
+    H = t.height
+    by_depth = [[] for _ in range(H + 1)]
+    for i in range(p):
+        by_depth[t.depth[i]].append(i)
 
     def blk(j):
         return block_bounds(m, b, j)
 
-    def note(i, j, ops, steps):
+    def real(j):
+        return blk(j) is not None
+
+    def last_round(i):
+        # the rounds a rank's loop runs through: j = 0 .. b + d_i
+        return b + t.depth[i]
+
+    # how far each rank got: ranks that stopped or wait forever take no
+    # further step
+    stopped = set()
+    blocked = {}
+    # blocks of Y[i] that hold their final value, with the round they did
+    final = {i: {} for i in range(p)}
+    # log entries with the rank's own step order inside a round
+    steps = {i: [] for i in range(p)}
+
+    def note(i, j, step, kind, partner, sent, recv, ops):
+        steps[i].append((j, step, kind, partner,
+                         sent if real(sent) else None,
+                         recv if real(recv) else None))
         ar = trace.active_rounds.setdefault(i, [])
         if not ar or ar[-1] != j:
             ar.append(j)
-        trace.exchanges[i] = trace.exchanges.get(i, 0) + steps
+        trace.exchanges[i] = trace.exchanges.get(i, 0) + 1
         o = trace.ops_per_round.setdefault(i, {})
         o[j] = o.get(j, 0) + ops
         s = trace.steps_per_round.setdefault(i, {})
-        s[j] = s.get(j, 0) + steps
+        s[j] = s.get(j, 0) + 1
 
-    def take(Y, j):
-        bb = blk(j)
-        return None if bb is None else Y[bb[0]:bb[1]].copy()
+    def can_step(i, j):
+        return i not in stopped and i not in blocked
 
-    def log(i, j, kind, partner, s_j, r_j):
-        trace.exchange_log.setdefault(i, []).append(
-            (j, kind, partner, s_j if blk(s_j) is not None else None,
-             r_j if blk(r_j) is not None else None))
+    def attempts(i, j, void):
+        """Does rank i take part in this round's exchange on an edge?"""
+        if j > last_round(i):
+            return False
+        return not (skip_void and void)
 
-    def program(i):
-        Y = rows[i]                                    # Y <- x_i
-        d = t.depth[i]
-        for j in range(0, b + d + 1):
-            if fail is not None and fail == (i, j):
-                return
-            for c in (t.child0[i], t.child1[i]):
-                if c is None:
-                    continue
-                s_j, r_j = j - (d + 1), j
-                if skip_void and blk(s_j) is None and blk(r_j) is None:
-                    continue
-                got = yield _Req(c, "child", j, s_j, r_j, take(Y, s_j))
-                log(i, j, "child", c, s_j, r_j)
-                bb = blk(r_j)
+    def rendezvous(a, b_, j, kind_a, kind_b, void):
+        """Both ends of an edge in round j: True if the exchange happens;
+        otherwise an end that waits for it is marked blocked."""
+        wa = attempts(a, j, void) and can_step(a, j)
+        wb = attempts(b_, j, void) and can_step(b_, j)
+        if wa and wb:
+            return True
+        if wa and attempts(a, j, void):
+            blocked[a] = (b_, kind_a, j)
+        if wb and attempts(b_, j, void):
+            blocked[b_] = (a, kind_b, j)
+        return False
+
+    rounds = b + H + 1
+    for j in range(rounds):
+        if fail is not None and fail[1] == j:
+            stopped.add(fail[0])
+        # child-to-parent and parent-to-child traffic, deepest edges first;
+        # at each parent the first child's edge before the second child's
+        for d in range(H, 0, -1):
+            for q in by_depth[d - 1]:
+                for step, c in ((0, t.child0[q]), (1, t.child1[q])):
+                    if c is None:
+                        continue
+                    up, down = j, j - t.depth[c]
+                    void = not real(up) and not real(down)
+                    if not rendezvous(c, q, j, "parent", "child", void):
+                        continue
+                    ops = 0
+                    if real(up):
+                        s, e = blk(up)
+                        Y[q][s:e] = combine(dtype, op, Y[c][s:e], Y[q][s:e])
+                        ops = 1
+                    if real(down):
+                        if final[q].get(down, j) >= j:
+                            raise ProtocolError(
+                                f"round {j}: rank {q} sends block {down} to "
+                                f"rank {c} before it is final")
+                        s, e = blk(down)
+                        Y[c][s:e] = Y[q][s:e]
+                        final[c][down] = j
+                    note(q, j, step, "child", c, down, up, ops)
+                    note(c, j, 2, "parent", q, up, down, 0)
+        # the roots: block j is now their tree's product
+        if len(t.roots) == 2:
+            ra, rb = t.roots
+            void = not real(j)
+            if rendezvous(ra, rb, j, "dual", "dual", void):
                 ops = 0
-                if bb is not None:
-                    Y[bb[0]:bb[1]] = combine(dtype, op, got, Y[bb[0]:bb[1]])
+                if real(j):
+                    s, e = blk(j)
+                    ta, tb = Y[ra][s:e].copy(), Y[rb][s:e].copy()
+                    Y[ra][s:e] = combine(dtype, op, ta, tb)   # mine (.) got
+                    Y[rb][s:e] = combine(dtype, op, ta, tb)   # got (.) mine
+                    final[ra][j] = final[rb][j] = j
                     ops = 1
-                note(i, j, ops, 1)
-            if t.parent[i] is None:
-                q = t.dual[i]
-                if q is None:
-                    # a root without a dual has Y[j] complete now
-                    if blk(j) is not None:
-                        trace.final_round.setdefault(i, {})[j] = j
-                    continue
-                if skip_void and blk(j) is None:
-                    continue
-                got = yield _Req(q, "dual", j, j, j, take(Y, j))
-                log(i, j, "dual", q, j, j)
-                bb = blk(j)
-                ops = 0
-                if bb is not None:
-                    mine = Y[bb[0]:bb[1]]
-                    Y[bb[0]:bb[1]] = (combine(dtype, op, mine, got) if i < q
-                                      else combine(dtype, op, got, mine))
-                    ops = 1
-                    trace.final_round.setdefault(i, {})[j] = j
-                note(i, j, ops, 1)
-            else:
-                s_j, r_j = j, j - d
-                if skip_void and blk(s_j) is None and blk(r_j) is None:
-                    continue
-                got = yield _Req(t.parent[i], "parent", j, s_j, r_j,
-                                take(Y, s_j))
-                log(i, j, "parent", t.parent[i], s_j, r_j)
-                bb = blk(r_j)
-                if bb is not None:
-                    Y[bb[0]:bb[1]] = got
-                    trace.final_round.setdefault(i, {})[r_j] = j
-                note(i, j, 0, 1)
+                note(ra, j, 2, "dual", rb, j, j, ops)
+                note(rb, j, 2, "dual", ra, j, j, ops)
+        else:
+            r = t.roots[0]
+            if real(j) and can_step(r, j):
+                final[r][j] = j
 
-    gens = {i: program(i) for i in range(p)}
-    pending: Dict[int, Optional[_Req]] = {}
-
-    def advance(i, value):
-        try:
-            pending[i] = gens[i].send(value)
-        except StopIteration:
-            pending.pop(i, None)
-
+    if blocked:
+        raise DeadlockError(blocked)
     for i in range(p):
-        advance(i, None)
-
-    ready = deque(range(p))
-    while ready:
-        i = ready.popleft()
-        req = pending.get(i)
-        if req is None:
-            continue
-        other = pending.get(req.partner)
-        if other is None or other.partner != i:
-            continue
-        pair = {req.kind, other.kind}
-        if req.round != other.round or pair not in ({"child", "parent"},
-                                                     {"dual"}):
-            raise ProtocolError(
-                f"ranks {i} and {req.partner} disagree: {req.kind}@{req.round}"
-                f" vs {other.kind}@{other.round}")
-        if req.send_j != other.recv_j or other.send_j != req.recv_j:
-            raise ProtocolError(
-                f"ranks {i} and {req.partner} exchange mismatched blocks in "
-                f"round {req.round}")
-        q = req.partner
-        a, bpay = req.payload, other.payload
-        advance(i, bpay)
-        advance(q, a)
-        ready.append(i)
-        ready.append(q)
-
-    if pending:
-        raise DeadlockError({i: (r.partner, r.kind, r.round)
-                             for i, r in pending.items()})
-    return rows, trace
-
+        for (j, _, kind, partner, sent, recv) in sorted(
+                steps[i], key=lambda e: (e[0], e[1])):
+            trace.exchange_log.setdefault(i, []).append(
+                (j, kind, partner, sent, recv))
+        if final[i]:
+            trace.final_round[i] = dict(final[i])
+    return Y, trace

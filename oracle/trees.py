@@ -22,8 +22,8 @@ the text leaves room (each listed in the design notes):
   d_i as the depth and needs children one level below their parent.
 
 A second shape, ``wbal`` (recursive weight-balanced split, lower subtree gets
-ceil((n-1)/2)), is provided for experiments only; it is parity unpinned
-except for its p=9 structure.
+ceil((n-1)/2)), is provided for experiments only; its pins are the p=9
+structure, one hand-derived fp32 value and the size invariants that fix it.
 
 ``layout="single"`` builds one heap-shaped post-order tree over all p ranks
 instead (root p-1, no dual): the single-tree alternative discussed in

@@ -852,6 +852,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   prm.done = slot_base + (size_t)dpar::kTicketCounters * kCounterStride;
   prm.bar_count = line + 0;
   prm.bar_gen = line + 1;
+  prm.bar_quit = line + 2;
   prm.err = st->counters + (size_t)kCounterSlots * kLinesPerSlot *
                                kCounterStride;
   prm.spin_limit = spin_limit();
@@ -960,6 +961,15 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // a contiguous run of work items (plan.hpp xcd_run_index)
   if (up == dpar::Exec::SPLIT && path == dpar::Path::VEC16 && !xrows16)
     prm.xcd_runs = 1;
+  // The cooperative executors start from zeroed barrier words (arrivals,
+  // generation, give-up): a call whose wait gave up may leave them out of
+  // step, and its counter slot comes round again kCounterSlots calls later.
+  // (These executors are refused under capture, so no graph records this.)
+  if (ex == dpar::Exec::GRID_BARRIER || ex == dpar::Exec::ROUNDS_BARRIER) {
+    const hipError_t ez =
+        hipMemsetAsync(line, 0, kCounterStride * sizeof(unsigned), stream);
+    if (ez != hipSuccess) return hip_fail(ez, "hipMemsetAsync barrier words");
+  }
   hipError_t e = dpar::launch(kind, path, unit, waves, up, tab, prm, stream,
                               st->num_cus, lds_floor);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
@@ -1056,14 +1066,14 @@ int dpar_check_status(hipStream_t stream) {
   e = hipMemcpy(&flag, errw, sizeof flag, hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
   if (flag) {
-    // a barrier gave up: clear the flag and every barrier counter
-    const size_t words =
-        ((size_t)kCounterSlots * kLinesPerSlot + 1) * kCounterStride;
-    e = hipMemset(st->counters, 0, words * sizeof(unsigned));
+    // a barrier wait gave up: report it once (each call zeroes its own
+    // barrier words, so only the report word is cleared here)
+    e = hipMemset(errw, 0, sizeof(unsigned));
     if (e != hipSuccess) return hip_fail(e, "hipMemset");
-    return fail(DPAR_ERR_TIMEOUT, "a grid-barrier wait exceeded its spin "
-                                  "limit; results of that call are unordered "
-                                  "but complete");
+    return fail(DPAR_ERR_TIMEOUT,
+                "a grid-barrier wait exceeded its spin limit: a GRID_BARRIER "
+                "call's outputs are complete (its rounds ran unordered), a "
+                "ROUNDS_BARRIER call's outputs are undefined");
   }
   return DPAR_SUCCESS;
 }

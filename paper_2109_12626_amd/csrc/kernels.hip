@@ -653,9 +653,10 @@ __device__ inline void grid_barrier(const Params& prm) {
                          __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_fetch_add(prm.bar_gen, 1u, __ATOMIC_RELEASE,
                              __HIP_MEMORY_SCOPE_AGENT);
-    } else if (__hip_atomic_load(prm.err, __ATOMIC_RELAXED,
+    } else if (__hip_atomic_load(prm.bar_quit, __ATOMIC_RELAXED,
                                  __HIP_MEMORY_SCOPE_AGENT) == 0) {
-      // (once a wait has given up, later barriers of the call do not wait)
+      // (once a wait of this call has given up, its later barriers do not
+      // wait; the word belongs to this call alone)
       // Poll with relaxed loads: on this multi-XCD part an agent-scope
       // acquire invalidates the XCD's L2, and polling with it from many
       // workgroups would keep every L2 invalidating under the workgroups
@@ -665,6 +666,7 @@ __device__ inline void grid_barrier(const Params& prm) {
                                __HIP_MEMORY_SCOPE_AGENT) == g) {
         __builtin_amdgcn_s_sleep(2);
         if (++spins > prm.spin_limit) {  // watchdog: give up, report
+          atomicOr(prm.bar_quit, 1u);
           atomicOr(prm.err, 1u);
           break;
         }

@@ -58,9 +58,12 @@ struct Params {
                         // words apart; each reset by the last WG it served
   unsigned* done;       // TICKET: per-counter count of WGs finished, same
                         // layout as `ticket`
-  unsigned* bar_count;  // GRID_BARRIER: arrivals
-  unsigned* bar_gen;    // GRID_BARRIER: generation
-  unsigned* err;        // bit 0: a barrier wait gave up
+  unsigned* bar_count;  // GRID_BARRIER, ROUNDS_BARRIER: arrivals
+  unsigned* bar_gen;    // generation
+  unsigned* bar_quit;   // nonzero once a wait of this call gave up (the
+                        // host zeroes the three words before each call)
+  unsigned* err;        // device-wide report: bit 0 set when any barrier
+                        // wait gave up (cleared by the host's status check)
   unsigned long long spin_limit;
   int out0, out1;       // non-fused up-step: ranks whose outputs receive y
                         // (out1 < 0: none)

@@ -3,13 +3,14 @@ in the launch configuration the benchmark times (block count from the
 sqrt(m log2 p) rule, the default split executor), and with every algorithm
 and executor at that size.
 
-* Sampled columns (the first and last chunks, every column around a few
-  block boundaries, and random ones) are compared with the CPU oracle for
-  every rank, bit for bit.
-* Every column of every rank is checked against properties that hold at any
-  size: all p outputs are identical; int32 SUM and MAX equal the exact
-  column sum (wrapped) and maximum; fp32 SUM lies within the recursive
-  summation bound of the exact sum.
+* fp32 SUM: every one of the 2^22 columns of y_0 is compared bit for bit
+  with the CPU oracle's full evaluation in the trees' association (a few
+  seconds of numpy per tree layout), and every rank's row with y_0 on the
+  device; the result also lies within the recursive summation bound of the
+  exact sum.
+* int32 SUM and MAX: every column equals the exact column sum (wrapped) and
+  maximum, the plain definition that the exactly associative operators
+  reach; sampled columns are also compared with the oracle's evaluation.
 """
 
 import gc
@@ -68,10 +69,54 @@ def _cleanup():
     torch.cuda.empty_cache()
 
 
-def test_p1152_fp32_sum_full_size():
+def _check_all_columns(yd, want, what=""):
+    """y_0 equals the oracle's y in every column, bit for bit (rows 1..p-1
+    are compared with y_0 on the device by _check_rows_identical)."""
+    got = yd[0].cpu().numpy()
+    g = got.view(np.uint32)
+    wv = np.ascontiguousarray(want).view(np.uint32)
+    bad = np.flatnonzero(g != wv)
+    assert bad.size == 0, (
+        f"{what}: {bad.size} of {g.size} columns differ from the oracle, "
+        f"first at {bad[0]}: got {got[bad[0]]!r} want {want[bad[0]]!r}")
+
+
+@pytest.fixture(scope="module")
+def fp32_full():
+    """The headline input on the host and the device, and the oracle's full
+    y for each tree layout (computed once, on first use)."""
+    need_gpu()
     w = configs.P1152_F32
-    x, xd, yd, b = _run_full(w, "sum")
-    _check_sampled(x, yd, b, "float32", "sum", 1)
+    x = workload_input(w)
+    xd = to_dev(x)
+    wants = {}
+
+    def want(layout):
+        if layout not in wants:
+            trees = (oracle.build_trees(w.p) if layout == "dual" else
+                     oracle.build_trees(w.p, layout="single"))
+            wants[layout] = oracle.allreduce_tree(x, w.dtype, "sum",
+                                                  trees=trees)
+        return wants[layout]
+
+    yield w, x, xd, want
+    del xd
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def test_p1152_fp32_sum_full_size(fp32_full):
+    """The benchmark's call (default executor, the rule's b = 6532): all
+    4,194,304 columns against the oracle, all 1152 rows identical."""
+    from paper_2109_12626_amd import dpar
+    w, x, xd, want = fp32_full
+    b = oracle.block_rule_lit(w.p, w.m)
+    yd = poisoned_like(xd)
+    s = torch.cuda.current_stream()
+    dpar.dpar_allreduce(dpar.rows(xd), dpar.rows(yd), w.p, w.m, w.dtype,
+                        "sum", b, s)
+    dpar.dpar_check_status(s)
+    _check_all_columns(yd, want("dual"), "default call")
     _check_rows_identical(yd)
     # every column within the recursive-summation bound of the exact sum:
     # at most 2 (H + 1) + 1 additions on any input's path, H = 9
@@ -88,6 +133,7 @@ def test_p1152_fp32_sum_full_size():
         # fp64 summation of 1152 terms is exact to ~1e-13 relative, far
         # below the fp32 bound
         assert bool((err <= gamma * mag + 1e-30).all()), f"columns from {c}"
+    del yd, y0
 
 
 @pytest.mark.parametrize("op", ["sum", "max"])
@@ -108,36 +154,23 @@ def test_p1152_int32_full_size(op):
         assert torch.equal(y0[c:c + step], want), f"columns from {c}"
 
 
-@pytest.fixture(scope="module")
-def fp32_full():
-    need_gpu()
-    w = configs.P1152_F32
-    x = workload_input(w)
-    xd = to_dev(x)
-    yield w, x, xd
-    del xd
-    gc.collect()
-    torch.cuda.empty_cache()
-
-
 @pytest.mark.parametrize("alg", ["dual", "single", "reduce_bcast"])
 @pytest.mark.parametrize("exec", ["split", "ticket", "launch", "barrier",
                                   "rounds", "rounds_barrier"])
 def test_p1152_fp32_every_alg_and_executor(fp32_full, alg, exec):
     """The headline shape through every algorithm and executor at the rule's
-    b: sampled columns bit-exact against the oracle's tree(s), every rank's
-    row identical to rank 0's."""
+    b: every column bit-exact against the oracle's tree(s), every rank's row
+    identical to rank 0's."""
     from paper_2109_12626_amd import dpar
-    w, x, xd = fp32_full
+    w, x, xd, want = fp32_full
     b = oracle.block_rule_lit(w.p, w.m)
     yd = poisoned_like(xd)
     s = torch.cuda.current_stream()
     dpar.dpar_allreduce_opt(dpar.rows(xd), dpar.rows(yd), w.p, w.m, w.dtype,
                             "sum", b, alg, exec, 0, -1, s)
     dpar.dpar_check_status(s)
-    trees = (oracle.build_trees(w.p) if alg == "dual" else
-             oracle.build_trees(w.p, layout="single"))
-    _check_sampled(x, yd, b, "float32", "sum", 3, trees=trees)
+    _check_all_columns(yd, want("dual" if alg == "dual" else "single"),
+                       f"{alg}/{exec}")
     _check_rows_identical(yd)
     del yd
 

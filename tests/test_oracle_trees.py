@@ -209,3 +209,67 @@ def test_depth2_subtree_sizes_of_576():
     t = build_trees(1152)
     roots = sorted(i for i in range(576) if t.depth[i] == 2)
     assert [r - t.lo[r] + 1 for r in roots] == [192, 127, 127, 127]
+
+
+def _subtree_size(t, i):
+    return i - t.lo[i] + 1
+
+
+@pytest.mark.parametrize("p", list(range(1, 258)) + [300, 511, 576, 1000,
+                                                      1151, 1152, 1999, 2000])
+@pytest.mark.parametrize("layout", ["dual", "single"])
+def test_wbal_invariants(p, layout):
+    """The weight-balanced shape (the alternative reading of "as balanced
+    and complete as possible", kept for experiments), pinned by the
+    properties that define it, which together fix the tree: every subtree is
+    a contiguous post-order rank range [lo_i, i] ending at its root; of the
+    s - 1 ranks below a root of an s-rank subtree, the lower ceil((s-1)/2)
+    form the second child's subtree, the rest the first child's (i - 1); a
+    two-rank subtree has one child; depth grows by one per level; the height
+    of an n-rank tree is floor(log2 n)."""
+    t = build_trees(p, shape="wbal", layout=layout)
+    n_a = (p + 1) // 2 if layout == "dual" else p
+    spans = [(0, n_a), (n_a, p - n_a)]
+    for first, n in spans:
+        if n == 0:
+            continue
+        root = first + n - 1
+        assert t.parent[root] is None and t.depth[root] == 0
+        assert t.lo[root] == first
+        walk = []
+        _postorder_walk(t, root, walk)
+        assert walk == list(range(first, first + n))
+        assert max(t.depth[first:first + n]) == int(math.floor(math.log2(n)))
+    assert t.roots == [root for root in
+                       [f + n - 1 for f, n in spans if n > 0]]
+    for i in range(p):
+        s = _subtree_size(t, i)
+        c0, c1 = t.child0[i], t.child1[i]
+        below = s - 1
+        low, high = (below + 1) // 2, below // 2
+        if below == 0:
+            assert c0 is None and c1 is None
+            continue
+        assert c0 == i - 1 and t.parent[c0] == i
+        assert t.depth[c0] == t.depth[i] + 1
+        if high == 0:          # one rank below: a single (first) child
+            assert c1 is None and _subtree_size(t, c0) == 1
+            continue
+        assert c1 is not None and t.parent[c1] == i
+        assert t.depth[c1] == t.depth[i] + 1
+        assert t.lo[i] == t.lo[c1]
+        assert _subtree_size(t, c1) == low          # second child: lower part
+        assert _subtree_size(t, c0) == high
+        assert t.lo[c0] == c1 + 1
+
+
+def test_wbal_p1152_differs_from_heap():
+    """At p = 1152 the two readings give different trees (576 = 2^9 + 64:
+    the heap's left-filled last level is unbalanced by weight)."""
+    h = build_trees(1152)
+    w = build_trees(1152, shape="wbal")
+    assert h.child1[575] != w.child1[575]
+    assert [_subtree_size(w, w.child1[575]), _subtree_size(w, 574)] == \
+        [288, 287]
+    assert [_subtree_size(h, h.child1[575]), _subtree_size(h, 574)] == \
+        [320, 255]
