@@ -321,7 +321,11 @@ const char* dpar_last_error(void);
  *   DPAR_SEQ_WG_PER_CU=n    SPLIT's post-order up-phase at p >= 256 with
  *                           at least 64 work items per CU: workgroups
  *                           resident per CU (default 4; 0 = as many as fit)
- *   DPAR_SPIN_LIMIT=n       grid-barrier watchdog, in polls (default 2^26) */
+ *   DPAR_SPIN_LIMIT=n       grid-barrier watchdog, in polls (default 2^26)
+ *   DPAR_LOG=1              print each call's plan on stderr: p, m, dtype,
+ *                           operator, algorithm, tree height H, b, lane
+ *                           width, decomposition, executor, work-item kind,
+ *                           work items */
 
 /* Frees every library-owned device and pinned host buffer (device tables,
  * counters, staging).  The library re-creates them lazily on the next call.

@@ -675,6 +675,53 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
   return uc;
 }
 
+const char* exec_name(dpar::Exec e) {
+  switch (e) {
+    case dpar::Exec::LAUNCH_PER_ROUND: return "launch_per_round";
+    case dpar::Exec::GRID_BARRIER: return "grid_barrier";
+    case dpar::Exec::TICKET: return "ticket";
+    case dpar::Exec::SPLIT: return "split";
+    case dpar::Exec::DISPATCH: return "one_launch_fused";
+    case dpar::Exec::TICKET_SPLIT: return "split(ticket up-phase)";
+    case dpar::Exec::ROUNDS: return "rounds";
+    case dpar::Exec::ROUNDS_BARRIER: return "rounds_barrier";
+  }
+  return "?";
+}
+
+const char* unit_name(dpar::Unit u) {
+  return u == dpar::Unit::LEVEL ? "level" : u == dpar::Unit::SUB ? "subtree"
+                                                                  : "postorder";
+}
+
+// DPAR_LOG=1: one line per call on stderr with the plan it runs (tree
+// height, block count, decomposition, executor, work item), for diagnosis.
+void log_plan(int p, size_t m, dpar_dtype_t dtype, dpar_op_t op,
+              dpar_alg_t alg, bool rule_b, const dpar::Schedule& s,
+              dpar::Path path, dpar::Exec ex, dpar::Unit unit, int waves,
+              const dpar::Params& prm, int height) {
+  static const char* dts[] = {"int32", "float32", "u32mat2x2"};
+  static const char* opn[] = {"sum", "max", "matmul"};
+  static const char* algs[] = {"dual_root", "single_tree", "reduce_bcast"};
+  const uint64_t items = ((uint64_t)prm.b + (uint64_t)prm.grp - 1) /
+                         (uint64_t)prm.grp * (uint64_t)prm.C;
+  std::fprintf(stderr,
+               "dpar: p=%d m=%zu %s %s alg=%s H=%d b=%d%s lanes=%s "
+               "quantum=%d line_quanta=%d tail=%llu exec=%s unit=%s "
+               "waves=%d chunks_per_block=%d blocks_per_item=%d items=%llu",
+               p, m, dts[(int)dtype], opn[(int)op], algs[(int)alg], height,
+               s.b, rule_b ? " (rule)" : "",
+               path == dpar::Path::VEC16 ? "16B" : "4B", s.g, s.lq,
+               (unsigned long long)s.tail, exec_name(ex), unit_name(unit),
+               waves, prm.C, prm.grp, (unsigned long long)items);
+  if (unit == dpar::Unit::LEVEL)
+    std::fprintf(stderr, " level_chunk_quanta=%d", 1 << prm.lv_log2t);
+  if (unit == dpar::Unit::SUB)
+    std::fprintf(stderr, " sub_deep=%d", prm.sub_deep);
+  if (ex == dpar::Exec::TICKET) std::fprintf(stderr, " batch=%u", prm.batch);
+  std::fprintf(stderr, "\n");
+}
+
 int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
                    dpar_dtype_t dtype, dpar_op_t op, int b,
                    const dpar_options_t& opt, hipStream_t stream) {
@@ -714,6 +761,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
       return fail(DPAR_ERR_UNSUPPORTED, "rank %d address above 2^48", i);
   }
   if (m == 0) return DPAR_SUCCESS;
+  const bool rule_b = b == 0;
   if (b == 0) b = (int)dpar::block_rule(p, m, 0.0, 0.0);
   if ((size_t)b > m)
     return fail(DPAR_ERR_INVALID_ARG, "b = %d exceeds m = %zu", b, m);
@@ -961,6 +1009,9 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // a contiguous run of work items (plan.hpp xcd_run_index)
   if (up == dpar::Exec::SPLIT && path == dpar::Path::VEC16 && !xrows16)
     prm.xcd_runs = 1;
+  if (env_int("DPAR_LOG", 0) != 0)
+    log_plan(p, m, dtype, op, alg, rule_b, s, path, up, unit, waves, prm,
+             ops->real_height);
   // The cooperative executors start from zeroed barrier words (arrivals,
   // generation, give-up): a call whose wait gave up may leave them out of
   // step, and its counter slot comes round again kCounterSlots calls later.

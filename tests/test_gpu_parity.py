@@ -3,9 +3,8 @@ by element, on seeded inputs.  Integer and matrix results must be bit-exact;
 fp32 SUM must also be bit-exact, because the kernels apply the additions in
 exactly the tree order the oracle follows (Algorithm 1's association).
 
-Small and mid-size cases compare every element of every rank's output.
-Full-size workloads compare sampled columns with the oracle and check
-properties that hold at any size for every column.
+Small and mid-size cases compare every element of every rank's output (the
+full-size workloads are in test_gpu_fullsize.py).
 """
 
 import numpy as np
@@ -389,3 +388,20 @@ def test_p1152_fp32_reduced_size_every_element(unit):
         with env_unit(unit):
             out = run(x, "float32", "sum", resolve_b("rule", w.p, m), exec)
         assert_all_ranks_equal(out, _want(x, "float32", "sum"), exec)
+
+
+def test_plan_log_names_the_plan(capfd):
+    """DPAR_LOG=1 prints the plan of each call on stderr (diagnostics only:
+    the result is unchanged)."""
+    from tests._gpu import _Env
+    w = configs.P7_SMALL
+    x = workload_input(w)
+    with _Env("DPAR_LOG", 1):
+        out = run(x, "int32", "sum", 0, "split")
+    err = capfd.readouterr().err
+    line = next(v for v in err.splitlines() if v.startswith("dpar: "))
+    b = oracle.block_rule_lit(w.p, w.m)
+    for part in (f"p={w.p}", f"m={w.m}", "int32 sum", "alg=dual_root",
+                 "H=2", f"b={b} (rule)", "exec=split", "items="):
+        assert part in line, (part, line)
+    assert_all_ranks_equal(out, _want(x, "int32", "sum"), "logged call")
