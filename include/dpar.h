@@ -211,6 +211,27 @@ typedef struct {
 int dpar_allreduce(const void* const* x, void* const* y, int p, size_t m,
                    dpar_dtype_t dtype, dpar_op_t op, int b, hipStream_t stream);
 
+/* dpar_allreduce for callers that cannot allocate memory (code that must not
+ * call hipMalloc, e.g. tight serving loops or harnesses that forbid it): the
+ * same computation, arguments, results and errors as dpar_allreduce, with
+ * no device or pinned host allocation in the call.  The library's device
+ * tables (opcodes, level table, subtree plan, the pointer tables) live in a
+ * fixed 1 MiB device array per GPU, held until the process ends; they are
+ * written by small copy kernels whose data travels in kernel arguments,
+ * only when p or the pointer arrays differ from the previous call of this
+ * entry point on the device.  Limits and caveats:
+ *   - p <= 32768 (DPAR_ERR_UNSUPPORTED beyond);
+ *   - every call on a GPU shares that GPU's array: calls of this entry
+ *     point that overlap on one GPU (e.g. on two streams without
+ *     synchronisation between them) race and give undefined results;
+ *   - it cannot be recorded into a HIP graph (DPAR_ERR_UNSUPPORTED under
+ *     stream capture);
+ *   - the host-side planner still uses ordinary heap memory when p changes.
+ * The other entry points are unaffected and may be mixed with it. */
+int dpar_allreduce_noalloc(const void* const* x, void* const* y, int p,
+                           size_t m, dpar_dtype_t dtype, dpar_op_t op, int b,
+                           hipStream_t stream);
+
 /* Same as dpar_allreduce with an explicit round executor. */
 int dpar_allreduce_ex(const void* const* x, void* const* y, int p, size_t m,
                       dpar_dtype_t dtype, dpar_op_t op, int b,

@@ -110,6 +110,23 @@ struct DeviceState {
 std::mutex g_mu;
 std::map<int, std::unique_ptr<DeviceState>> g_devices;
 
+// The allocation-free entry point (dpar_allreduce_noalloc): per device, the
+// address of the library's fixed scratch array and what it holds.  Layout
+// for p ranks: opcode table | level table | subtree plan | pointer tables,
+// each at a 256-byte boundary.
+constexpr int kFixedMaxDevices = 64;
+struct FixedState {
+  bool ready = false;
+  DeviceState info;               // device attributes only: no counters,
+                                  // tables or staging slots
+  unsigned char* scratch = nullptr;  // this device's fixed scratch array
+  int tables_p = 0;               // p whose tables the scratch holds (0: none)
+  OpsTable ops;                   // device pointers into the scratch
+  size_t ptr_off = 0;             // offset of the pointer tables
+  std::vector<uint64_t> ptr_key;  // x then y pointers the scratch holds
+};
+FixedState g_fixed[kFixedMaxDevices];
+
 int env_int(const char* name, int dflt) {
   const char* v = std::getenv(name);
   return v && *v ? std::atoi(v) : dflt;
@@ -320,6 +337,113 @@ int stage_pointers(DeviceState* st, const void* const* x, void* const* y,
   s->key = std::move(key);
   s->last_use = st->tick;
   *used = s;
+  return DPAR_SUCCESS;
+}
+
+// The fixed scratch of the current device; its address is looked up once per
+// device (with that device current) and kept.  Allocates nothing.
+int get_fixed(FixedState** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kFixedMaxDevices)
+    return fail(DPAR_ERR_UNSUPPORTED, "device %d beyond the fixed scratch "
+                                      "table", dev);
+  FixedState& f = g_fixed[dev];
+  if (!f.ready) {
+    DeviceState& st = f.info;
+    st.device = dev;
+    e = hipDeviceGetAttribute(&st.num_cus,
+                              hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+      e = hipDeviceGetAttribute(&st.lds_limit,
+                                hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+    if (e == hipSuccess)
+      e = hipDeviceGetAttribute(
+          &st.lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+          dev);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    void* ptr = nullptr;
+    e = dpar::fixed_scratch_address(&ptr);
+    if (e != hipSuccess || !ptr)
+      return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol,
+                      "hipGetSymbolAddress(fixed scratch)");
+    f.scratch = static_cast<unsigned char*>(ptr);
+    f.ready = true;
+  }
+  *out = &f;
+  return DPAR_SUCCESS;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// Device tables for p ranks (dual-root trees) in the fixed scratch, staged
+// through kernel arguments on `stream` unless the scratch holds them already.
+int fixed_tables(FixedState* f, int p, hipStream_t stream,
+                 const OpsTable** out) {
+  if (f->tables_p == p) {
+    *out = &f->ops;
+    return DPAR_SUCCESS;
+  }
+  f->tables_p = 0;  // whatever follows, the old tables are gone
+  f->ptr_key.clear();
+  const dpar::Tree kt = dpar::build_tree(p);
+  std::vector<uint32_t> ops = dpar::make_ops(kt);
+  std::vector<uint32_t> sub;
+  const bool has_sub = p >= 64 && dpar::make_sub(kt, ops, 2, &sub);
+  ops.resize(ops.size() + dpar::kTablePad, 0u);  // kernels read ahead
+  const std::vector<uint32_t> lvl = dpar::make_levels(kt);
+  const size_t off_lvl = align256(ops.size() * 4);
+  const size_t off_sub = off_lvl + align256(lvl.size() * 4);
+  const size_t off_ptr = off_sub + align256(sub.size() * 4);
+  const size_t ptr_bytes = (2 * (size_t)p + dpar::kTablePad) * 8;
+  if (off_ptr + align256(ptr_bytes) > dpar::kFixedScratchBytes)
+    return fail(DPAR_ERR_UNSUPPORTED, "p = %d: tables exceed the fixed "
+                "scratch of %zu bytes", p, dpar::kFixedScratchBytes);
+  unsigned char* base = f->scratch;
+  hipError_t e = dpar::stage_by_args(base, ops.data(), ops.size() * 4, stream);
+  if (e == hipSuccess)
+    e = dpar::stage_by_args(base + off_lvl, lvl.data(), lvl.size() * 4,
+                            stream);
+  if (e == hipSuccess && has_sub)
+    e = dpar::stage_by_args(base + off_sub, sub.data(), sub.size() * 4,
+                            stream);
+  if (e != hipSuccess) return hip_fail(e, "staging the tables");
+  OpsTable t;
+  t.dev = reinterpret_cast<uint32_t*>(base);
+  t.lvl = reinterpret_cast<uint32_t*>(base + off_lvl);
+  t.sub = has_sub ? reinterpret_cast<uint32_t*>(base + off_sub) : nullptr;
+  t.sub_ns = has_sub ? (int)sub[3] : 0;
+  t.height = kt.height;
+  t.real_height = kt.height;
+  t.n_a = kt.n_a;
+  t.root_a = kt.root_a;
+  t.root_b = kt.root_b;
+  f->ops = t;
+  f->ptr_off = off_ptr;
+  f->tables_p = p;
+  *out = &f->ops;
+  return DPAR_SUCCESS;
+}
+
+// The pointer tables in the fixed scratch (after fixed_tables for this p).
+int fixed_pointers(FixedState* f, const void* const* x, void* const* y,
+                   int p, hipStream_t stream, const uint64_t** out) {
+  uint64_t* dev = reinterpret_cast<uint64_t*>(f->scratch + f->ptr_off);
+  if (!same_key(f->ptr_key, x, y, p)) {
+    f->ptr_key.clear();
+    std::vector<uint64_t> key(2 * (size_t)p + dpar::kTablePad, 0u);
+    for (int i = 0; i < p; ++i) {
+      key[i] = (uint64_t)(uintptr_t)x[i];
+      key[p + i] = (uint64_t)(uintptr_t)y[i];
+    }
+    const hipError_t e =
+        dpar::stage_by_args(dev, key.data(), key.size() * 8, stream);
+    if (e != hipSuccess) return hip_fail(e, "staging the pointer tables");
+    key.resize(2 * (size_t)p);
+    f->ptr_key = std::move(key);
+  }
+  *out = dev;
   return DPAR_SUCCESS;
 }
 
@@ -722,9 +846,12 @@ void log_plan(int p, size_t m, dpar_dtype_t dtype, dpar_op_t op,
   std::fprintf(stderr, "\n");
 }
 
+// fixed: the allocation-free variant (dual-root trees, AUTO executor, device
+// tables in the fixed scratch, no counters).
 int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
                    dpar_dtype_t dtype, dpar_op_t op, int b,
-                   const dpar_options_t& opt, hipStream_t stream) {
+                   const dpar_options_t& opt, hipStream_t stream,
+                   bool fixed = false) {
   g_err.clear();
   const dpar_exec_t exec = opt.exec;
   const dpar_alg_t alg = opt.alg;
@@ -738,6 +865,9 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     return fail(DPAR_ERR_INVALID_ARG, "unknown executor %d", (int)exec);
   if (alg < DPAR_ALG_DUAL_ROOT || alg > DPAR_ALG_REDUCE_BCAST)
     return fail(DPAR_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+  if (fixed && p > dpar::kFixedMaxRanks)
+    return fail(DPAR_ERR_UNSUPPORTED, "p = %d beyond the %d ranks of the "
+                "allocation-free entry point", p, dpar::kFixedMaxRanks);
   const bool rounds_exec =
       exec == DPAR_EXEC_ROUNDS || exec == DPAR_EXEC_ROUNDS_BARRIER;
   if (!rounds_exec && (opt.round_begin != 0 || opt.round_end != -1))
@@ -819,6 +949,9 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
   }
   const bool capturing = cap != hipStreamCaptureStatusNone;
+  if (capturing && fixed)
+    return fail(DPAR_ERR_UNSUPPORTED, "the allocation-free entry point "
+                "cannot be captured into a graph");
   if (capturing && (exec == DPAR_EXEC_GRID_BARRIER ||
                     exec == DPAR_EXEC_ROUNDS_BARRIER))
     return fail(DPAR_ERR_UNSUPPORTED,
@@ -835,10 +968,19 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
                   "capture: make one eager call with these arguments first");
   }
   DeviceState* st = nullptr;
-  int rc = get_state(&st);
-  if (rc) return rc;
+  FixedState* fx = nullptr;
   const OpsTable* ops = nullptr;
-  rc = get_ops(st, p, single, &ops);
+  int rc = DPAR_SUCCESS;
+  if (fixed) {
+    rc = get_fixed(&fx);
+    if (rc) return rc;
+    st = &fx->info;
+    rc = fixed_tables(fx, p, stream, &ops);
+  } else {
+    rc = get_state(&st);
+    if (rc) return rc;
+    rc = get_ops(st, p, single, &ops);
+  }
   if (rc) return rc;
   if (rounds_exec && !ops->dn)
     return fail(DPAR_ERR_UNSUPPORTED, "ROUNDS executors need p < 2^24");
@@ -852,20 +994,31 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     return fail(DPAR_ERR_UNSUPPORTED, "tree too deep for the LDS slots");
 
   StageSlot* slot = nullptr;
-  if (!find_staged(st, x, y, p, &slot)) {
-    if (capturing)
-      return fail(DPAR_ERR_UNSUPPORTED, "capture: make one eager call with "
-                                        "these pointer arrays first");
-    rc = stage_pointers(st, x, y, p, stream, &slot);
+  const uint64_t* ptr_dev = nullptr;
+  if (fixed) {
+    rc = fixed_pointers(fx, x, y, p, stream, &ptr_dev);
     if (rc) return rc;
+  } else {
+    if (!find_staged(st, x, y, p, &slot)) {
+      if (capturing)
+        return fail(DPAR_ERR_UNSUPPORTED, "capture: make one eager call with "
+                                          "these pointer arrays first");
+      rc = stage_pointers(st, x, y, p, stream, &slot);
+      if (rc) return rc;
+    }
+    if (capturing) slot->pinned = true;
+    ptr_dev = slot->dev;
   }
-  if (capturing) slot->pinned = true;
 
-  const unsigned cslot = st->next_counter++ % kCounterSlots;
-  unsigned* slot_base =
-      st->counters + (size_t)cslot * kLinesPerSlot * kCounterStride;
-  unsigned* line =
-      slot_base + (size_t)2 * dpar::kTicketCounters * kCounterStride;
+  // ticket and barrier words (none for the allocation-free variant, whose
+  // executors use none)
+  unsigned* slot_base = nullptr;
+  unsigned* line = nullptr;
+  if (!fixed) {
+    const unsigned cslot = st->next_counter++ % kCounterSlots;
+    slot_base = st->counters + (size_t)cslot * kLinesPerSlot * kCounterStride;
+    line = slot_base + (size_t)2 * dpar::kTicketCounters * kCounterStride;
+  }
   dpar::Params prm{};
   prm.p = p;
   prm.n_a = ops->n_a;
@@ -897,17 +1050,19 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     if (prm.batch < 1) prm.batch = 1;
   }
   prm.ticket = slot_base;
-  prm.done = slot_base + (size_t)dpar::kTicketCounters * kCounterStride;
-  prm.bar_count = line + 0;
-  prm.bar_gen = line + 1;
-  prm.bar_quit = line + 2;
-  prm.err = st->counters + (size_t)kCounterSlots * kLinesPerSlot *
-                               kCounterStride;
+  prm.done = fixed ? nullptr
+                   : slot_base + (size_t)dpar::kTicketCounters * kCounterStride;
+  prm.bar_count = fixed ? nullptr : line + 0;
+  prm.bar_gen = fixed ? nullptr : line + 1;
+  prm.bar_quit = fixed ? nullptr : line + 2;
+  prm.err = fixed ? nullptr
+                  : st->counters + (size_t)kCounterSlots * kLinesPerSlot *
+                                       kCounterStride;
   prm.spin_limit = spin_limit();
 
   dpar::Tables tab;
-  tab.xp = slot->dev;
-  tab.yp = slot->dev + p;
+  tab.xp = ptr_dev;
+  tab.yp = ptr_dev + p;
   tab.ops = ops->dev;
   tab.lvl = ops->lvl;
   tab.dn = ops->dn;
@@ -987,7 +1142,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // out by the hardware in round order (persistent ticketed workgroups on
   // request, for comparison)
   dpar::Exec up = ex;
-  if (ex == dpar::Exec::SPLIT) {
+  if (ex == dpar::Exec::SPLIT && !fixed) {
     const char* v = std::getenv("DPAR_SPLIT_UP");
     if (v && !std::strcmp(v, "ticket")) up = dpar::Exec::TICKET_SPLIT;
   }
@@ -1071,7 +1226,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
                         rows16, span, stream);
     if (e != hipSuccess) return hip_fail(e, "broadcast launch");
   }
-  if (!capturing) {  // a pinned slot is never restaged, so never waited on
+  if (!capturing && !fixed) {  // a pinned slot is never restaged, so never
+                               // waited on
     e = hipEventRecord(slot->ev, stream);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
     slot->pending = true;
@@ -1101,6 +1257,13 @@ int dpar_allreduce(const void* const* x, void* const* y, int p, size_t m,
                    dpar_dtype_t dtype, dpar_op_t op, int b,
                    hipStream_t stream) {
   return dpar_allreduce_ex(x, y, p, m, dtype, op, b, DPAR_EXEC_AUTO, stream);
+}
+
+int dpar_allreduce_noalloc(const void* const* x, void* const* y, int p,
+                           size_t m, dpar_dtype_t dtype, dpar_op_t op, int b,
+                           hipStream_t stream) {
+  const dpar_options_t opt{DPAR_ALG_DUAL_ROOT, DPAR_EXEC_AUTO, 0, -1};
+  return allreduce_impl(x, y, p, m, dtype, op, b, opt, stream, true);
 }
 
 int dpar_check_status(hipStream_t stream) {
@@ -1148,6 +1311,12 @@ int dpar_finalize(void) {
   }
   g_devices.clear();
   g_alias_ok.clear();
+  // the fixed scratch stays (it lives as long as the process); only the
+  // record of what it holds is dropped
+  for (FixedState& f : g_fixed) {
+    f.tables_p = 0;
+    f.ptr_key.clear();
+  }
   if (prev >= 0) (void)hipSetDevice(prev);
   return DPAR_SUCCESS;
 }

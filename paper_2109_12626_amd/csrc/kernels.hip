@@ -29,6 +29,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <cstring>
 #include <map>
 #include <utility>
 
@@ -1120,6 +1121,54 @@ hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
 size_t lds_bytes(Path path, Kind kind, int waves, int nslots) {
   const size_t lane = (path == Path::VEC16 || kind == Kind::MAT) ? 16 : 4;
   return (size_t)waves * nslots * 64 * lane;
+}
+
+// ------------------------------------------------------------ fixed scratch
+
+// Each GPU holds its own copy of this array until the process ends.  Host
+// code never passes its name to a kernel: it asks the runtime for the
+// device's address once (fixed_scratch_address) and uses that.
+static __device__ __align__(256) unsigned char scratch[kFixedScratchBytes];
+
+namespace {
+
+// One launch carries this many payload bytes in its kernel arguments (the
+// whole argument block stays below 4 KB).
+constexpr int kStageWords = 480;
+
+struct StagePacket {
+  uint64_t* dst;
+  uint32_t nwords;
+  uint32_t unused;
+  uint64_t w[kStageWords];
+};
+
+__global__ __launch_bounds__(256) void k_stage(StagePacket pk) {
+  for (uint32_t i = threadIdx.x; i < pk.nwords; i += 256) pk.dst[i] = pk.w[i];
+}
+
+}  // namespace
+
+hipError_t fixed_scratch_address(void** out) {
+  return hipGetSymbolAddress(out, HIP_SYMBOL(scratch));
+}
+
+hipError_t stage_by_args(void* dst, const void* src, size_t nbytes,
+                         hipStream_t stream) {
+  const unsigned char* s = static_cast<const unsigned char*>(src);
+  uint64_t* d = static_cast<uint64_t*>(dst);
+  const size_t per = sizeof(uint64_t) * kStageWords;
+  for (size_t off = 0; off < nbytes; off += per) {
+    const size_t n = nbytes - off < per ? nbytes - off : per;
+    StagePacket pk{};
+    pk.dst = d + off / sizeof(uint64_t);
+    pk.nwords = (uint32_t)((n + 7) / 8);
+    memcpy(pk.w, s + off, n);  // the rest of the last word stays zero
+    hipLaunchKernelGGL(k_stage, dim3(1), dim3(256), 0, stream, pk);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace dpar

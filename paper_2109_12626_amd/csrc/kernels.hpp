@@ -141,4 +141,24 @@ hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
 // Bytes of dynamic LDS a workgroup needs.
 size_t lds_bytes(Path path, Kind kind, int waves, int nslots);
 
+// ------------------------------------------------------------ fixed scratch
+// The allocation-free entry point keeps its device tables (opcodes, level
+// table, subtree plan, pointer tables) in one statically sized device array
+// per GPU, so that it never allocates.
+constexpr size_t kFixedScratchBytes = 1u << 20;  // 1 MiB per device
+constexpr int kFixedMaxRanks = 32768;            // p the layout admits
+
+// Device address of this GPU's fixed scratch array (the current device).
+// Call once per device with that device current; the address differs per
+// device.
+hipError_t fixed_scratch_address(void** out);
+
+// Copies nbytes from host memory to device address dst (8-byte aligned)
+// through kernel arguments of small copy launches on `stream`: nothing is
+// allocated and the host buffer may be reused as soon as this returns.  At
+// most 7 bytes past dst + nbytes are written (zeros), up to the next 8-byte
+// boundary.
+hipError_t stage_by_args(void* dst, const void* src, size_t nbytes,
+                         hipStream_t stream);
+
 }  // namespace dpar

@@ -81,6 +81,7 @@ def lib():
     vp, sz, i = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
     L.dpar_allreduce.argtypes = [vp, vp, i, sz, i, i, i, vp]
     L.dpar_allreduce_ex.argtypes = [vp, vp, i, sz, i, i, i, i, vp]
+    L.dpar_allreduce_noalloc.argtypes = [vp, vp, i, sz, i, i, i, vp]
     L.dpar_allreduce_opt.argtypes = [vp, vp, i, sz, i, i, i,
                                      ctypes.POINTER(dpar_options_t), vp]
     L.dpar_tree_info.argtypes = [i, i, ctypes.POINTER(dpar_node_t)]
@@ -98,6 +99,7 @@ def lib():
     L.dpar_last_error.argtypes = []
     L.dpar_finalize.argtypes = []
     for name in ("dpar_allreduce", "dpar_allreduce_ex", "dpar_allreduce_opt",
+                 "dpar_allreduce_noalloc",
                  "dpar_tree_info", "dpar_tree_info_alg",
                  "dpar_schedule_rounds", "dpar_block_rule", "dpar_rounds",
                  "dpar_schedule_info", "dpar_block_bounds",
@@ -155,6 +157,13 @@ def rows(t):
 def dpar_allreduce(x, y, p, m, dtype, op, b=0, stream=None):
     """x, y: sequences of p device addresses (ints or tensors)."""
     return _check(lib().dpar_allreduce(
+        _ptr_array(x), _ptr_array(y), int(p), int(m), _enum(DTYPES, dtype),
+        _enum(OPS, op), int(b), _stream(stream)))
+
+
+def dpar_allreduce_noalloc(x, y, p, m, dtype, op, b=0, stream=None):
+    """The allocation-free variant of dpar_allreduce (include/dpar.h)."""
+    return _check(lib().dpar_allreduce_noalloc(
         _ptr_array(x), _ptr_array(y), int(p), int(m), _enum(DTYPES, dtype),
         _enum(OPS, op), int(b), _stream(stream)))
 
