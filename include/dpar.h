@@ -95,9 +95,12 @@ typedef enum {
  *                     streams y_0 into the other p - 1 outputs.  HBM reads
  *                     and writes share one bus, so separating the two
  *                     directions avoids read/write turnarounds.
- *   AUTO              SPLIT; for calls moving at most 40 MB (2 p m times
- *                     the element size) one launch of every work item in
- *                     round order with the fused write-out instead.
+ *   AUTO              SPLIT; one launch of every work item in round order
+ *                     with the fused write-out instead for calls moving at
+ *                     most 40 MB (2 p m times the element size), and for
+ *                     calls that run in subtree work items (p >= 256 and at
+ *                     most two such items per CU, at least one per two
+ *                     CUs).
  * The last two run the algorithm's whole round structure, down-phase
  * included (dpar_schedule_rounds gives the number of rounds R):
  *   ROUNDS            one launch per round r = 0 .. R-1.  Round r runs the
@@ -305,10 +308,11 @@ int dpar_block_bounds(const dpar_schedule_t* s, size_t m, int j, size_t* start,
 int dpar_check_status(hipStream_t stream);
 
 /* Profiling aid: records `ev` on the call's stream between the up-phase and
- * the broadcast pass of the calling thread's next call that runs the SPLIT
- * executor, so that each pass can be timed with HIP events.
- * The setting is consumed by that call; NULL clears it.  It never changes
- * what a call computes.  No device work. */
+ * the broadcast pass of the calling thread's next reduction call, if that
+ * call runs the SPLIT executor, so that each pass can be timed with HIP
+ * events.  The next reduction call consumes the setting whatever it runs (a
+ * call that does not run SPLIT, or fails, drops it without touching `ev`);
+ * NULL clears it.  It never changes what a call computes.  No device work. */
 int dpar_set_phase_event(hipEvent_t ev);
 
 /* Text of the calling thread's last error ("" if none). */
@@ -342,6 +346,9 @@ const char* dpar_last_error(void);
  *   DPAR_SEQ_WG_PER_CU=n    SPLIT's post-order up-phase at p >= 256 with
  *                           at least 64 work items per CU: workgroups
  *                           resident per CU (default 4; 0 = as many as fit)
+ *   DPAR_BCAST_FASTDIV=0|1  SPLIT's broadcast pass: workgroups find their
+ *                           row and tile by multiplication (1, default) or
+ *                           by division (0)
  *   DPAR_SPIN_LIMIT=n       grid-barrier watchdog, in polls (default 2^26)
  *   DPAR_LOG=1              print each call's plan on stderr: p, m, dtype,
  *                           operator, algorithm, tree height H, b, lane

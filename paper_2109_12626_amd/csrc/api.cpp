@@ -853,6 +853,10 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
                    const dpar_options_t& opt, hipStream_t stream,
                    bool fixed = false) {
   g_err.clear();
+  // the phase event (dpar_set_phase_event) belongs to this call alone,
+  // recorded only if it runs the split executor's two passes
+  const hipEvent_t phase_event = g_phase_event;
+  g_phase_event = nullptr;
   const dpar_exec_t exec = opt.exec;
   const dpar_alg_t alg = opt.alg;
   if (!x || !y) return fail(DPAR_ERR_INVALID_ARG, "null pointer array");
@@ -1030,7 +1034,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   prm.qbase = 0;
   prm.b = s.b;
   prm.C = s.C;
-  const dpar::Exec ex = device_exec(exec, p, 2ull * p * m * esz);
+  dpar::Exec ex = device_exec(exec, p, 2ull * p * m * esz);
   prm.grp = block_group(ex, s);
   {
     // Work items per ticket: a claim is an atomic at device scope, whose
@@ -1083,6 +1087,22 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   prm.r1 = r1;
 
   const UnitChoice uc = choose_unit(ex, s, prm.grp, path, kind, p, *ops, *st);
+  // AUTO: a call that runs in subtree work items (at most two per CU) runs
+  // them as one fused launch rather than split: each item's y goes from
+  // registers to all p outputs while the few other items still read, and
+  // the broadcast pass's many short workgroups (and their launch) are gone.
+  // Measured, int32 SUM, cold caches, the sqrt(m log2 p) rule's b: p = 1152,
+  // m = 2^16 (256 items) split 0.126 ms, fused 0.107 ms; p = 2304,
+  // m = 57344 (224 items) 0.199 vs 0.180 ms; p = 576, m = 57344 0.063 vs
+  // 0.057 ms; p = 288, m = 115712 (452 items) 0.060 vs 0.055 ms; with fewer
+  // items than half the CUs the chains dominate and fused is no better
+  // (p = 2304, m = 14336, 56 items: 0.107 vs 0.117 ms).  Calls that take
+  // post-order items stay split, which is faster there from 256 MB up
+  // (p = 36 .. 2304: 8-35% at 1-38 GB).
+  if (exec == DPAR_EXEC_AUTO && ex == dpar::Exec::SPLIT &&
+      uc.unit == dpar::Unit::SUB &&
+      2 * ((s.Q + 63) / 64) >= (uint64_t)st->num_cus)
+    ex = dpar::Exec::DISPATCH;
   const dpar::Unit unit = uc.unit;
   prm.nlev = ops->height + 1;
   if (unit == dpar::Unit::LEVEL) {
@@ -1212,9 +1232,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     if (e != hipSuccess) return hip_fail(e, "tail launch");
   }
   if (ex == dpar::Exec::SPLIT) {
-    if (g_phase_event) {
-      e = hipEventRecord(g_phase_event, stream);
-      g_phase_event = nullptr;
+    if (phase_event) {
+      e = hipEventRecord(phase_event, stream);
       if (e != hipSuccess) return hip_fail(e, "hipEventRecord phase event");
     }
     // y_0 now holds y for the whole chunked part; stream it to y_1..y_{p-1}
@@ -1222,8 +1241,15 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     int span_kb = env_int("DPAR_BCAST_SPAN_KB", kBcastSpanKB);
     if (span_kb <= 0) span_kb = kBcastSpanKB;
     const uint64_t span = (uint64_t)span_kb << 10;
+    // each workgroup finds its row and tile by multiplication rather than
+    // 64-bit division (measured in one process, alternating, split
+    // executor's broadcast pass, int32: p = 1152, m = 2^16 cold 69 -> 66 us;
+    // p = 36, m = 2^20 cold 31.7 -> 29.4 us; p = 1152, m = 2^22 warm 2.77
+    // -> 2.72 ms; p = 1152, m = 2^20 cold 0.727 -> 0.659 ms but warm 0.683
+    // -> 0.715 ms, the one case found slower)
+    const bool fastdiv = env_int("DPAR_BCAST_FASTDIV", 1) != 0;
     e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16,
-                        rows16, span, stream);
+                        rows16, span, fastdiv, stream);
     if (e != hipSuccess) return hip_fail(e, "broadcast launch");
   }
   if (!capturing && !fixed) {  // a pinned slot is never restaged, so never

@@ -1098,8 +1098,10 @@ size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev) {
 }
 
 hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
-                     bool rows16, uint64_t span_bytes, hipStream_t stream) {
-  const BcastGrid g = bcast_grid(nbytes, vec16 ? 16 : 4, p, span_bytes);
+                     bool rows16, uint64_t span_bytes, bool fastdiv_tiles,
+                     hipStream_t stream) {
+  BcastGrid g = bcast_grid(nbytes, vec16 ? 16 : 4, p, span_bytes);
+  g.fast = fastdiv_tiles && g.total <= 0xFFFFFFFFull;
   // a launch's thread count stays below 2^32: pieces of at most 2^23
   // workgroups (a multiple of 8, so workgroup w stays on XCD w mod 8)
   const uint64_t kMaxGrid = (1ull << 31) / 256;

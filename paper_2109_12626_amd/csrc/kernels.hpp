@@ -134,9 +134,12 @@ size_t sub_lds_bytes(size_t lane_bytes, int ns);
 // workgroup per (row, 256-lane tile), y_0 taken in spans of at most
 // span_bytes (every row of a span, then the next span).  rows16: every
 // output row starts on a 16-byte boundary (else the 16-byte lanes of each
-// row are shifted to its own 16-byte boundaries).
+// row are shifted to its own 16-byte boundaries).  fastdiv_tiles: each
+// workgroup finds its row and tile by multiplication instead of division
+// (plan.hpp bcast_tile).
 hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
-                     bool rows16, uint64_t span_bytes, hipStream_t stream);
+                     bool rows16, uint64_t span_bytes, bool fastdiv_tiles,
+                     hipStream_t stream);
 
 // Bytes of dynamic LDS a workgroup needs.
 size_t lds_bytes(Path path, Kind kind, int waves, int nslots);

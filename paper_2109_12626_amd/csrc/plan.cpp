@@ -313,6 +313,8 @@ BcastGrid bcast_grid(uint64_t nbytes, uint64_t lane_bytes, int p,
   if (g.nspan > 1 || nbytes > kBcastNoPadBytes)
     g.ts = (g.ts + 7) & ~(uint64_t)7;  // still <= tmax
   g.total = g.nspan * g.rows * g.ts;
+  g.m_ts = fastdiv_magic(g.ts);
+  g.m_span = fastdiv_magic(g.rows * g.ts);
   return g;
 }
 

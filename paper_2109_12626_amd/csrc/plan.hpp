@@ -191,7 +191,27 @@ struct BcastGrid {
   uint64_t nspan = 0;   // spans
   uint64_t rows = 0;    // output rows p - 1
   uint64_t total = 0;   // workgroups nspan * rows * ts
+  uint64_t m_ts = 0;    // fastdiv_magic(ts)
+  uint64_t m_span = 0;  // fastdiv_magic(rows * ts)
+  uint64_t fast = 0;    // 1: bcast_tile divides by multiplication (needs
+                        // total < 2^32; the host decides, see broadcast())
 };
+
+// Division of a 32-bit n by a fixed divisor d without a divide (Lemire,
+// Kaser and Kurz, "Faster remainder by direct computation", 2019): with
+// M = floor((2^64 - 1) / d) + 1, floor(n / d) is the high 64 bits of the
+// 96-bit product M n, exactly, for every n < 2^32 and 1 < d < 2^32.  d = 1
+// is kept apart (M would wrap to 0).
+DPAR_HOST_DEVICE inline uint64_t fastdiv_magic(uint64_t d) {
+  return d > 1 ? ~0ull / d + 1 : 0;
+}
+DPAR_HOST_DEVICE inline uint32_t fastdiv(uint32_t n, uint64_t M, uint64_t d) {
+  if (d == 1) return n;
+  // high 64 bits of M n from 32-bit halves, without overflow
+  const uint64_t lo = (M & 0xFFFFFFFFull) * n;
+  const uint64_t hi = (M >> 32) * n + (lo >> 32);
+  return (uint32_t)(hi >> 32);
+}
 
 // Spans of at most max(span_bytes, 8 tiles) bytes, as few as that allows;
 // ts is a multiple of 8 unless y_0 has at most kBcastNoPadBytes (then it
@@ -201,10 +221,20 @@ BcastGrid bcast_grid(uint64_t nbytes, uint64_t lane_bytes, int p,
                      uint64_t span_bytes);
 
 // Output row (1 .. p-1) and tile of workgroup w < g.total: span
-// w / (rows ts), in it row 1 + (w / ts) mod rows and tile w mod ts.
+// w / (rows ts), in it row 1 + (w / ts) mod rows and tile w mod ts.  With
+// g.fast the divisions are multiplications (fastdiv), else divisions.
 DPAR_HOST_DEVICE inline void bcast_tile(const BcastGrid& g, uint64_t w,
                                         uint64_t* row, uint64_t* tile) {
   const uint64_t per_span = g.rows * g.ts;
+  if (g.fast && g.total <= 0xFFFFFFFFull) {
+    const uint32_t w32 = (uint32_t)w;
+    const uint32_t span = fastdiv(w32, g.m_span, per_span);
+    const uint32_t r = w32 - span * (uint32_t)per_span;
+    const uint32_t q = fastdiv(r, g.m_ts, g.ts);
+    *row = 1 + (uint64_t)q;
+    *tile = (uint64_t)span * g.ts + (r - q * (uint32_t)g.ts);
+    return;
+  }
   const uint64_t span = w / per_span;
   const uint64_t r = w - span * per_span;
   *row = 1 + r / g.ts;

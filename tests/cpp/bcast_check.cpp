@@ -39,9 +39,40 @@ static void split(unsigned long long dst, unsigned long long ndw) {
               (unsigned long long)misaligned);
 }
 
+// "div d": floor(n / d) by fastdiv against the divide instruction for n
+// near 0, near 2^32, around multiples of d and at pseudo-random points;
+// prints the number of mismatches.
+static void divcheck(unsigned long long d) {
+  const uint64_t M = dpar::fastdiv_magic(d);
+  uint64_t bad = 0;
+  auto one = [&](uint64_t n) {
+    if (n > 0xFFFFFFFFull) return;
+    if (dpar::fastdiv((uint32_t)n, M, d) != n / d) ++bad;
+  };
+  for (uint64_t n = 0; n < 4096; ++n) one(n);
+  for (uint64_t n = 0xFFFFFFFFull - 4096; n <= 0xFFFFFFFFull; ++n) one(n);
+  for (uint64_t k = 1; k < 4096; ++k) {
+    const uint64_t top = 0xFFFFFFFFull / d;
+    for (uint64_t q : {k, top >= k ? top - k : 0, top / 2 + k})
+      for (int e = -1; e <= 1; ++e) one(q * d + e);
+  }
+  uint64_t s = 0x9E3779B97F4A7C15ull ^ d;
+  for (int k = 0; k < 200000; ++k) {
+    s ^= s << 13; s ^= s >> 7; s ^= s << 17;
+    one(s & 0xFFFFFFFFull);
+  }
+  std::printf("%llu\n", (unsigned long long)bad);
+}
+
 int main() {
   char tag[32];
   while (std::scanf("%31s", tag) == 1) {
+    if (std::string(tag) == "div") {
+      unsigned long long d;
+      if (std::scanf("%llu", &d) != 1) return 1;
+      divcheck(d);
+      continue;
+    }
     if (std::string(tag) == "split") {
       unsigned long long dst, ndw;
       if (std::scanf("%llu %llu", &dst, &ndw) != 2) return 1;
@@ -52,13 +83,19 @@ int main() {
     unsigned long long lane, span;
     int p;
     if (std::scanf("%llu %d %llu", &lane, &p, &span) != 3) return 1;
-    const dpar::BcastGrid g = dpar::bcast_grid(nbytes, lane, p, span);
+    dpar::BcastGrid g = dpar::bcast_grid(nbytes, lane, p, span);
+    g.fast = 1;   // the division-free mapping, checked against division
     const uint64_t tiles = (g.n + 255) / 256;
     std::vector<unsigned char> seen(g.rows * tiles, 0);
     uint64_t covered = 0, padded = 0, bad = 0;
     for (uint64_t w = 0; w < g.total; ++w) {
       uint64_t row, tile;
       dpar::bcast_tile(g, w, &row, &tile);
+      // the same pair by plain division
+      const uint64_t per_span = g.rows * g.ts, sp = w / per_span;
+      if (row != 1 + (w - sp * per_span) / g.ts ||
+          tile != sp * g.ts + (w - sp * per_span) % g.ts)
+        ++bad;
       if (row < 1 || row > g.rows) {
         ++bad;
         continue;

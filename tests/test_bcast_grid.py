@@ -125,3 +125,18 @@ def test_row_split_writes_every_dword_once_with_aligned_stores(splits, case):
     assert misaligned == 0
     assert 0 <= ndw - h - 4 * nbody <= 3
     assert nbody <= ndw // 4          # body lanes inside the row's grid
+
+
+DIVISORS = [1, 2, 3, 5, 7, 8, 63, 64, 1151, 4096, 4096 * 1151, 65537,
+            (1 << 31) - 1, 1 << 31, (1 << 31) + 1, (1 << 32) - 1,
+            1000003, 123456789]
+
+
+def test_fastdiv_is_exact(checker):
+    """The broadcast grid's division by multiplication (Lemire, Kaser and
+    Kurz 2019) equals integer division for 32-bit dividends: edges, around
+    multiples of the divisor, and 200000 pseudo-random points per divisor."""
+    text = "\n".join(f"div {d}" for d in DIVISORS)
+    res = subprocess.run([checker], input=text, capture_output=True,
+                         text=True, check=True)
+    assert [int(v) for v in res.stdout.split()] == [0] * len(DIVISORS)

@@ -405,3 +405,39 @@ def test_plan_log_names_the_plan(capfd):
                  "H=2", f"b={b} (rule)", "exec=split", "items="):
         assert part in line, (part, line)
     assert_all_ranks_equal(out, _want(x, "int32", "sum"), "logged call")
+
+
+def test_phase_event_belongs_to_the_next_call_only():
+    """dpar_set_phase_event: recorded between the split executor's two
+    passes of the next call; a next call that runs another executor drops
+    the setting, so a later split call leaves the event alone."""
+    from paper_2109_12626_amd import dpar
+    p, m = 64, 1 << 18
+    x = synth.generate("uniform_int", 2310, p, m, lo=0, hi=1000)
+    xd = to_dev(x)
+    yd = poisoned_like(xd)
+    xs, ys = dpar.pointers(dpar.rows(xd)), dpar.pointers(dpar.rows(yd))
+    s = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    # recorded: start <= mid <= end
+    t0, mid, t1 = ev(), ev(), ev()
+    mid.record(s)
+    t0.record(s)
+    dpar.dpar_set_phase_event(mid)
+    dpar.dpar_allreduce_ex(xs, ys, p, m, "int32", "sum", 1, "split", s)
+    t1.record(s)
+    t1.synchronize()
+    assert 0 <= t0.elapsed_time(mid) <= t0.elapsed_time(t1)
+    # dropped by a ticket call: the split call after it does not record it
+    mark, t2 = ev(), ev()
+    mark.record(s)
+    t0.record(s)
+    dpar.dpar_set_phase_event(mark)
+    dpar.dpar_allreduce_ex(xs, ys, p, m, "int32", "sum", 1, "ticket", s)
+    dpar.dpar_allreduce_ex(xs, ys, p, m, "int32", "sum", 1, "split", s)
+    t2.record(s)
+    t2.synchronize()
+    assert mark.elapsed_time(t0) >= 0          # still the first record
+    dpar.dpar_check_status(s)
+    assert_all_ranks_equal(from_dev(yd, x), _want(x, "int32", "sum"),
+                           "phase event calls")
