@@ -19,6 +19,7 @@ Prints ONE JSON line.  Extra lines go to stderr.
   python bench.py --sweep OUT.jsonl # every workload, executor, block count
   python bench.py --table2          # the paper's Table 2 counts at p = 288
   python bench.py --copy-compare    # calls beside a device copy of their bytes
+  python bench.py --copy-ceiling    # interleaved read+write rates, headline size
 """
 
 import argparse
@@ -293,6 +294,79 @@ def copy_compare():
     print(json.dumps({"copy_compare": out}))
 
 
+def copy_ceiling():
+    """Interleaved read+write HBM traffic at the headline size, 19.33 GB read
+    and 19.33 GB written per call, each entry the minimum and median of 8
+    timed calls after 2 untimed ones (HIP events on the call's stream, warm):
+      - the library at p = 1 (its copy kernel: one 16-byte load and one
+        streaming store per thread, 256 threads per workgroup, the broadcast
+        pass's shape) copying one row of p*m floats;
+      - torch's copy_ of the same bytes (the runtime's copy kernel);
+      - the headline call with the executors that interleave the two
+        directions in one launch (ticket; one fused launch of every work
+        item) and with the split executor, whose phases run one direction
+        each (their times with the phase event)."""
+    import numpy as np
+    import torch
+
+    from paper_2109_12626_amd import dpar
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    n = P * M
+    nbytes = 2 * n * ELEM
+    out = {}
+
+    def timed(fn, phase=False):
+        for _ in range(2):
+            fn()
+        ts, ups = [], []
+        for _ in range(8):
+            e0, e1, e2 = [torch.cuda.Event(enable_timing=True)
+                          for _ in range(3)]
+            e1.record(stream)
+            e0.record(stream)
+            if phase:
+                dpar.dpar_set_phase_event(e1)
+            fn()
+            e2.record(stream)
+            e2.synchronize()
+            ts.append(e0.elapsed_time(e2))
+            if phase:
+                ups.append(e0.elapsed_time(e1))
+        rec = {"ms_min": round(min(ts), 4),
+               "ms_median": round(float(np.median(ts)), 4),
+               "GB/s": round(nbytes / min(ts) / 1e6, 1)}
+        if phase:
+            up = min(ups)
+            rec["up_ms"] = round(up, 4)
+            rec["up_read_GB/s"] = round((n + M) * ELEM / up / 1e6, 1)
+            bc = float(np.median([t - u for t, u in zip(ts, ups)]))
+            rec["broadcast_ms_median"] = round(bc, 4)
+        return rec
+
+    x = torch.randn(P, M, device=dev)
+    y = torch.empty_like(x)
+    xs, ys = dpar.pointers(dpar.rows(x)), dpar.pointers(dpar.rows(y))
+    flat_x, flat_y = x.view(-1), y.view(-1)
+    out["library_copy_p1"] = timed(lambda: dpar.dpar_allreduce(
+        [flat_x.data_ptr()], [flat_y.data_ptr()], 1, n, "float32", "sum", 1,
+        stream))
+    assert torch.equal(flat_y[:: 1 << 20], flat_x[:: 1 << 20])
+    out["torch_copy_"] = timed(lambda: flat_y.copy_(flat_x))
+    b = dpar.dpar_block_rule(P, M)
+    call = lambda ex: (lambda: dpar.dpar_allreduce_ex(  # noqa: E731
+        xs, ys, P, M, "float32", "sum", b, ex, stream))
+    out["call_ticket"] = timed(call("ticket"))
+    os.environ["DPAR_FUSE_BELOW_KB"] = str(1 << 30)
+    out["call_one_fused_launch"] = timed(call("auto"))
+    os.environ.pop("DPAR_FUSE_BELOW_KB")
+    out["call_split"] = timed(call("split"), phase=True)
+    dpar.dpar_check_status(stream)
+    for k, v in out.items():
+        log(k, json.dumps(v))
+    print(json.dumps({"copy_ceiling_bytes_per_call": nbytes, "rates": out}))
+
+
 def sweep(out_path, only=(), execs=("split", "ticket", "launch", "barrier"),
           algs=("dual",)):
     """Every workload x executor x block count, cold caches (a 512 MiB
@@ -395,6 +469,8 @@ def main():
                     help="the paper's Table 2 counts at p = 288")
     ap.add_argument("--copy-compare", action="store_true",
                     help="calls beside a plain device copy of their bytes")
+    ap.add_argument("--copy-ceiling", action="store_true",
+                    help="interleaved read+write rates at the headline size")
     ap.add_argument("--sweep", metavar="OUT_JSONL",
                     help="measure every workload, executor and block count")
     ap.add_argument("--only", default="",
@@ -430,6 +506,9 @@ def main():
         return
     if args.copy_compare:
         copy_compare()
+        return
+    if args.copy_ceiling:
+        copy_ceiling()
         return
     if args.sweep:
         sweep(args.sweep, [v for v in args.only.split(",") if v],

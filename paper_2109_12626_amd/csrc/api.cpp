@@ -943,6 +943,17 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     alias_remember(x, y, p, m * esz);
   }
   if (rounds_exec && r0 == r1) return DPAR_SUCCESS;
+  // One rank: the reduction is x_0 itself and the delivery a copy into y_0
+  // (nothing in place).  The round-structured executors keep their rounds.
+  if (p == 1 && !rounds_exec) {
+    if (env_int("DPAR_LOG", 0) != 0)
+      std::fprintf(stderr, "dpar: p=1 m=%zu exec=copy\n", m);
+    if (x[0] == y[0]) return DPAR_SUCCESS;
+    const hipError_t e = dpar::copy_row((uint64_t)(uintptr_t)x[0],
+                                        (uint64_t)(uintptr_t)y[0], m * esz,
+                                        stream);
+    return e == hipSuccess ? DPAR_SUCCESS : hip_fail(e, "copy launch");
+  }
   // Under stream capture (a HIP graph being recorded) a call may only
   // enqueue kernels: the device tables and the staged pointer set must exist
   // already (an eager call with the same arguments made them), the staging

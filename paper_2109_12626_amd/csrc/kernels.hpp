@@ -144,6 +144,12 @@ hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
 // Bytes of dynamic LDS a workgroup needs.
 size_t lds_bytes(Path path, Kind kind, int waves, int nslots);
 
+// The reduction of a single rank: bytes (a multiple of 4) from src to dst,
+// both 4-byte aligned and not overlapping, one 16-byte lane per thread (the
+// last up to 3 dwords one per thread), 256 threads per workgroup.
+hipError_t copy_row(uint64_t src, uint64_t dst, uint64_t bytes,
+                    hipStream_t stream);
+
 // ------------------------------------------------------------ fixed scratch
 // The allocation-free entry point keeps its device tables (opcodes, level
 // table, subtree plan, pointer tables) in one statically sized device array

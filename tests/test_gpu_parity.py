@@ -441,3 +441,29 @@ def test_phase_event_belongs_to_the_next_call_only():
     dpar.dpar_check_status(s)
     assert_all_ranks_equal(from_dev(yd, x), _want(x, "int32", "sum"),
                            "phase event calls")
+
+
+@pytest.mark.parametrize("shift", [0, 1, 2, 3])
+@pytest.mark.parametrize("m", [1, 3, 4, 7, 1023, 1 << 20, (1 << 20) + 5])
+def test_one_rank_copies_at_every_alignment(m, shift):
+    """p = 1: y_0 = x_0, through the copy kernel (16-byte lanes, the last
+    up to 3 elements one per thread) on rows shifted by 0..3 elements off
+    16-byte boundaries, with neighbours of the output left untouched; in
+    place the call writes nothing."""
+    from paper_2109_12626_amd import dpar
+    x = synth.generate("uniform_int", 2320 + m % 997, 1, m + 8, lo=-1000, hi=1000)
+    xd = to_dev(x)
+    yd = torch.full((1, m + 8), POISON, dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream()
+    xs = [xd.data_ptr() + 4 * ((shift + 1) % 4)]
+    ys = [yd.data_ptr() + 4 * shift]
+    dpar.dpar_allreduce(xs, ys, 1, m, "int32", "sum", 0, s)
+    dpar.dpar_check_status(s)
+    got = yd.cpu().numpy()[0]
+    src = x[0][(shift + 1) % 4:(shift + 1) % 4 + m]
+    assert np.array_equal(got[shift:shift + m], src)
+    assert (got[:shift] == POISON).all() and (got[shift + m:] == POISON).all()
+    before = xd.clone()
+    dpar.dpar_allreduce(xs, xs, 1, m, "int32", "sum", 0, s)
+    dpar.dpar_check_status(s)
+    assert torch.equal(xd, before)
