@@ -20,6 +20,7 @@ Prints ONE JSON line.  Extra lines go to stderr.
   python bench.py --table2          # the paper's Table 2 counts at p = 288
   python bench.py --copy-compare    # calls beside a device copy of their bytes
   python bench.py --copy-ceiling    # interleaved read+write rates, headline size
+  python bench.py --fixed-cost      # fixed vs per-byte cost per phase, mid sizes
 """
 
 import argparse
@@ -367,6 +368,96 @@ def copy_ceiling():
     print(json.dumps({"copy_ceiling_bytes_per_call": nbytes, "rates": out}))
 
 
+FIXED_COST = [  # name, p, m, dtype, op
+    ("p36_int32_sum", 36, 1 << 20, "int32", "sum"),
+    ("p64_u32mat2x2_matmul", 64, 1 << 18, "u32mat2x2", "matmul"),
+    ("p1152_int32_sum", 1152, 1 << 16, "int32", "sum"),
+]
+
+
+def fixed_cost():
+    """Where the mid-size workloads' time goes: each is run with the split
+    executor at 1/4 .. 8 times its m (same p, dtype, operator, b from the
+    sqrt(m log2 p) rule), cold caches (a 512 MiB write between calls), and
+    each phase's minimum time t over 10 calls is fitted as t = a + B / r
+    (least squares over the six sizes; B the phase's algorithmic bytes):
+    a is what the phase costs whatever it moves (launch, filling the GPU
+    with workgroups, draining the last ones), r the rate at which it moves
+    bytes once running.  Also the AUTO executor's whole call."""
+    import numpy as np
+    import torch
+
+    from paper_2109_12626_amd import dpar
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    flush = torch.empty(1 << 27, dtype=torch.float32, device=dev)
+    out = []
+    for name, p, m0, dt, op in FIXED_COST:
+        esz = 16 if dt == "u32mat2x2" else 4
+        pts = []
+        for f in (0.25, 0.5, 1, 2, 4, 8):
+            m = int(m0 * f)
+            x = torch.randint(0, 1 << 16, (p, m * esz // 4), dtype=torch.int32,
+                              device=dev)
+            y = torch.empty_like(x)
+            xs, ys = dpar.pointers(dpar.rows(x)), dpar.pointers(dpar.rows(y))
+            b = dpar.dpar_block_rule(p, m)
+            rec = {"m": m, "b": b}
+            for ex in ("split", "auto"):
+                fn = lambda: dpar.dpar_allreduce_ex(  # noqa: E731
+                    xs, ys, p, m, dt, op, b, ex, stream)
+                fn()
+                ups, tots = [], []
+                for it in range(12):
+                    flush.fill_(float(it))
+                    e0, e1, e2 = [torch.cuda.Event(enable_timing=True)
+                                  for _ in range(3)]
+                    e1.record(stream)
+                    e0.record(stream)
+                    if ex == "split":
+                        dpar.dpar_set_phase_event(e1)
+                    fn()
+                    e2.record(stream)
+                    e2.synchronize()
+                    if it >= 2:
+                        tots.append(e0.elapsed_time(e2))
+                        ups.append(e0.elapsed_time(e1))
+                if ex == "split":
+                    rec["up_ms"] = min(ups)
+                    rec["bcast_ms"] = min(t - u for t, u in zip(tots, ups))
+                    rec["split_ms"] = min(tots)
+                else:
+                    rec["auto_ms"] = min(tots)
+            dpar.dpar_check_status(stream)
+            rec["up_bytes"] = (p + 1) * m * esz
+            rec["bcast_bytes"] = (p - 1) * m * esz
+            rec["call_bytes"] = 2 * p * m * esz
+            pts.append(rec)
+            del x, y
+            torch.cuda.empty_cache()
+
+        def fit(tkey, bkey):
+            B = np.array([r[bkey] for r in pts], dtype=float)
+            t = np.array([r[tkey] for r in pts], dtype=float) * 1e-3
+            A = np.stack([np.ones_like(B), B], axis=1)
+            (a, inv_r), *_ = np.linalg.lstsq(A, t, rcond=None)
+            return {"fixed_us": round(a * 1e6, 2),
+                    "rate_TB/s": round(1.0 / inv_r / 1e12, 3)}
+        own = next(r for r in pts if r["m"] == m0)
+        res = {"workload": name, "p": p, "m": m0, "dtype": dt, "op": op,
+               "up": fit("up_ms", "up_bytes"),
+               "broadcast": fit("bcast_ms", "bcast_bytes"),
+               "split_call": fit("split_ms", "call_bytes"),
+               "auto_call": fit("auto_ms", "call_bytes"),
+               "at_own_m": {k: round(own[k], 4) for k in
+                            ("up_ms", "bcast_ms", "split_ms", "auto_ms")},
+               "points": [{k: (round(v, 4) if isinstance(v, float) else v)
+                           for k, v in r.items()} for r in pts]}
+        out.append(res)
+        log(json.dumps({k: v for k, v in res.items() if k != "points"}))
+    print(json.dumps({"fixed_cost": out}))
+
+
 def sweep(out_path, only=(), execs=("split", "ticket", "launch", "barrier"),
           algs=("dual",)):
     """Every workload x executor x block count, cold caches (a 512 MiB
@@ -471,6 +562,8 @@ def main():
                     help="calls beside a plain device copy of their bytes")
     ap.add_argument("--copy-ceiling", action="store_true",
                     help="interleaved read+write rates at the headline size")
+    ap.add_argument("--fixed-cost", action="store_true",
+                    help="fixed and per-byte cost of each phase, mid sizes")
     ap.add_argument("--sweep", metavar="OUT_JSONL",
                     help="measure every workload, executor and block count")
     ap.add_argument("--only", default="",
@@ -509,6 +602,9 @@ def main():
         return
     if args.copy_ceiling:
         copy_ceiling()
+        return
+    if args.fixed_cost:
+        fixed_cost()
         return
     if args.sweep:
         sweep(args.sweep, [v for v in args.only.split(",") if v],

@@ -345,7 +345,12 @@ const char* dpar_last_error(void);
  *                           next (default 16384)
  *   DPAR_SEQ_WG_PER_CU=n    SPLIT's post-order up-phase at p >= 256 with
  *                           at least 64 work items per CU: workgroups
- *                           resident per CU (default 4; 0 = as many as fit)
+ *                           resident per CU (default 4; 0 = as many as
+ *                           fit); set, it applies to every SPLIT call with
+ *                           post-order work items
+ *   DPAR_XCD_RUNS=0|1       SPLIT's up-phase: each XCD takes a contiguous
+ *                           run of work items (default 1 only when some
+ *                           input row is off a 16-byte boundary)
  *   DPAR_BCAST_FASTDIV=0|1  SPLIT's broadcast pass: workgroups find their
  *                           row and tile by multiplication (1, default) or
  *                           by division (0)

@@ -1182,10 +1182,13 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // with fewer workgroups resident per CU (fewer rows streamed at once) than
   // with a full CU; the cap is set through the LDS each workgroup requests.
   size_t lds_floor = 0;
+  const char* cap_env = std::getenv("DPAR_SEQ_WG_PER_CU");
+  const bool cap_forced = cap_env && *cap_env;
   if (up == dpar::Exec::SPLIT && unit == dpar::Unit::SEQ &&
-      p >= kCapMinRanks &&
-      grouped_units(s, prm.grp) >=
-          (uint64_t)kCapMinItemsPerCu * (uint64_t)st->num_cus) {
+      (cap_forced ||
+       (p >= kCapMinRanks &&
+        grouped_units(s, prm.grp) >=
+            (uint64_t)kCapMinItemsPerCu * (uint64_t)st->num_cus))) {
     const int per_cu = env_int("DPAR_SEQ_WG_PER_CU", kSeqWgPerCu);
     if (per_cu > 0)
       lds_floor = (size_t)st->lds_per_cu / (size_t)(per_cu + 1) + 1024;
@@ -1195,6 +1198,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // a contiguous run of work items (plan.hpp xcd_run_index)
   if (up == dpar::Exec::SPLIT && path == dpar::Path::VEC16 && !xrows16)
     prm.xcd_runs = 1;
+  if (up == dpar::Exec::SPLIT)
+    prm.xcd_runs = env_int("DPAR_XCD_RUNS", prm.xcd_runs) != 0;
   if (env_int("DPAR_LOG", 0) != 0)
     log_plan(p, m, dtype, op, alg, rule_b, s, path, up, unit, waves, prm,
              ops->real_height);
