@@ -714,8 +714,9 @@ struct UnitChoice {
 //         with p >= 256 (p = 1152, m = 2^16, b = 1: 0.113 vs 0.165 ms;
 //         two per CU, p = 1152, m = 2^17: 0.240 vs 0.260 ms), and in
 //         place of LEVEL at p >= 256 when the level plan needs more than
-//         two items per CU; not for per-round executors or short chunks,
-//         where it loses.
+//         two items per CU; for launch per round and grid barrier only when
+//         a round has half a chunk to two chunks per CU, none of them short
+//         (elsewhere it loses).
 UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
                        dpar::Path path, dpar::Kind kind, int p,
                        const OpsTable& ops, const DeviceState& st) {
@@ -737,9 +738,23 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
   // a one-launch subtree run cuts the columns into whole chunks of 64
   // quanta, whatever the blocks (see allreduce_impl): count those
   const uint64_t sub_items = (s.Q + 63) / 64;
-  bool want_sub = whole_call && p >= 256 && sub_items <= 2 * cus && ops.sub &&
-                  dpar::sub_lds_bytes(lane_bytes, ops.sub_ns) <=
-                      (size_t)st.lds_limit - dpar::kStaticLdsReserve;
+  const bool sub_fits = ops.sub &&
+                        dpar::sub_lds_bytes(lane_bytes, ops.sub_ns) <=
+                            (size_t)st.lds_limit - dpar::kStaticLdsReserve;
+  // Launch per round and grid barrier with rounds of between half a chunk
+  // and two chunks per CU: every round is one generation of work items whose
+  // chains of p/2 loads set the round's time; subtree items cut the chains.
+  // Measured at p = 1152, m = 2^22 fp32, b = 66 (249 chunks per round):
+  // launch per round 10.0 -> 7.3 ms, grid barrier 11.5 -> 9.0 ms (the
+  // round-structured executor, whose rounds also carry the down-step,
+  // 10.0 -> 10.7 ms: not taken there).  With shorter rounds level items
+  // win (b = 6532, 3 chunks per round: 143 ms level, 355 ms subtree).
+  const bool round_sub = (ex == dpar::Exec::LAUNCH_PER_ROUND ||
+                          ex == dpar::Exec::GRID_BARRIER) &&
+                         p >= 256 && (uint64_t)s.C >= cus / 2 &&
+                         (uint64_t)s.C <= 2 * cus && s.Q >= 32 * all_items;
+  bool want_sub = p >= 256 && sub_fits &&
+                  ((whole_call && sub_items <= 2 * cus) || round_sub);
   if (ops.lvl) {
     int tmax = -1;
     for (int lg = 6; lg >= 0; --lg) {
@@ -792,9 +807,7 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
       }
     }
   }
-  if (forced) want_sub = !std::strcmp(u, "sub") && ops.sub &&
-                         dpar::sub_lds_bytes(lane_bytes, ops.sub_ns) <=
-                             (size_t)st.lds_limit - dpar::kStaticLdsReserve;
+  if (forced) want_sub = !std::strcmp(u, "sub") && sub_fits;
   if (want_sub) uc.unit = dpar::Unit::SUB;
   return uc;
 }

@@ -354,3 +354,20 @@ def test_grouped_short_blocks_matrix_product(exec):
     want = oracle.allreduce_ltr(x, "u32mat2x2", "matmul")
     out = from_dev(_run(x, "u32mat2x2", "matmul", 300, "dual", exec), x)
     assert_all_ranks_equal(out, want, f"matmul grouped {exec}")
+
+
+@pytest.mark.parametrize("exec", ["launch", "barrier"])
+def test_per_round_executors_take_subtree_items_for_mid_rounds(exec, capfd):
+    """p = 256, m = 2^18, b = 2: each round holds 512 full chunks (two per
+    CU), so launch per round and the grid barrier run subtree work items
+    (the library's choice, shown by DPAR_LOG), bit-exact in fp32."""
+    from tests._gpu import _Env
+    need_gpu()
+    p, m, b = 256, 1 << 18, 2
+    x = _input("normal_f32", 2190, p, m)
+    want = _want(x, "float32", "sum", "dual")
+    with env_unit(None), _Env("DPAR_LOG", 1):
+        out = from_dev(_run(x, "float32", "sum", b, "dual", exec), x)
+    err = capfd.readouterr().err
+    assert "unit=subtree" in err, err[-400:]
+    assert_all_ranks_equal(out, want, f"{exec} subtree rounds")
