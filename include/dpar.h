@@ -352,8 +352,8 @@ const char* dpar_last_error(void);
  *                           run of work items (default 1 only when some
  *                           input row is off a 16-byte boundary)
  *   DPAR_BCAST_FASTDIV=0|1  SPLIT's broadcast pass: workgroups find their
- *                           row and tile by multiplication (1, default) or
- *                           by division (0)
+ *                           row and tile by multiplication (1; default for
+ *                           passes writing at most 2 GB) or by division (0)
  *   DPAR_SPIN_LIMIT=n       grid-barrier watchdog, in polls (default 2^26)
  *   DPAR_LOG=1              print each call's plan on stderr: p, m, dtype,
  *                           operator, algorithm, tree height H, b, lane

@@ -69,6 +69,14 @@ constexpr uint64_t kScalarBelowBytes = 24ull << 20;
 // this many KB (2 MB per XCD's 4 MB L2; a 32 MB y_0 taken as one span ran at
 // half the speed).
 constexpr int kBcastSpanKB = 16384;
+// The broadcast pass finds each workgroup's row and tile by multiplication
+// (plan.hpp fastdiv) when it writes at most this many bytes, else by
+// division (two instantiations of the pass).  Measured against division,
+// split executor, cold caches: p = 1152, m = 2^16 int32 (0.3 GB written)
+// 72 -> 69 us; p = 36, m = 2^20 31.3 -> 29.8 us; the 64-rank matrix product
+// 48.3 -> 46.4 us; at p = 1152, m = 2^22 fp32 (19 GB, warm) division is the
+// faster one (2.65 against 2.73 ms).
+constexpr uint64_t kBcastFastDivMaxBytes = 2ull << 30;
 
 struct OpsTable {
   uint32_t* dev = nullptr;   // opcodes, padded
@@ -1270,13 +1278,11 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     int span_kb = env_int("DPAR_BCAST_SPAN_KB", kBcastSpanKB);
     if (span_kb <= 0) span_kb = kBcastSpanKB;
     const uint64_t span = (uint64_t)span_kb << 10;
-    // each workgroup finds its row and tile by multiplication rather than
-    // 64-bit division (measured in one process, alternating, split
-    // executor's broadcast pass, int32: p = 1152, m = 2^16 cold 69 -> 66 us;
-    // p = 36, m = 2^20 cold 31.7 -> 29.4 us; p = 1152, m = 2^22 warm 2.77
-    // -> 2.72 ms; p = 1152, m = 2^20 cold 0.727 -> 0.659 ms but warm 0.683
-    // -> 0.715 ms, the one case found slower)
-    const bool fastdiv = env_int("DPAR_BCAST_FASTDIV", 1) != 0;
+    // passes that write at most kBcastFastDivMaxBytes: each workgroup finds
+    // its row and tile by multiplication rather than 64-bit division
+    const bool fastdiv =
+        env_int("DPAR_BCAST_FASTDIV",
+                main_bytes * (uint64_t)(p - 1) <= kBcastFastDivMaxBytes) != 0;
     e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16,
                         rows16, span, fastdiv, stream);
     if (e != hipSuccess) return hip_fail(e, "broadcast launch");

@@ -866,11 +866,11 @@ __global__ __launch_bounds__(U::kThreads) void k_ticket(DPAR_KARGS) {
 // on this part than long-running workgroups with many stores each (measured
 // at p = 1152, m = 2^22 fp32: 7.1 vs 5.7 TB/s).  Works on bytes, whatever
 // the element type.
-template <class T>
+template <class T, bool FAST>
 __global__ __launch_bounds__(256) void k_bcast(const uint64_t* __restrict__ yp,
                                                BcastGrid g, uint64_t first) {
   uint64_t row, tile;
-  bcast_tile(g, first + blockIdx.x, &row, &tile);     // workgroup-uniform
+  bcast_tile<FAST>(g, first + blockIdx.x, &row, &tile);  // workgroup-uniform
   const uint64_t lane = tile * 256 + threadIdx.x;
   if (lane >= g.n) return;
   const uint64_t off = lane * sizeof(T);
@@ -895,10 +895,11 @@ __global__ __launch_bounds__(256) void k_bcast(const uint64_t* __restrict__ yp,
 // cache lines leave partial lines to two workgroups); on 16-byte aligned
 // rows the plain pass is faster (2.6 against 3.1 ms), so the library picks
 // this one only when some output row needs it.
+template <bool FAST>
 __global__ __launch_bounds__(256) void k_bcast16_rows(
     const uint64_t* __restrict__ yp, BcastGrid g, uint64_t first) {
   uint64_t row, tile;
-  bcast_tile(g, first + blockIdx.x, &row, &tile);     // workgroup-uniform
+  bcast_tile<FAST>(g, first + blockIdx.x, &row, &tile);  // workgroup-uniform
   const uint64_t src = yp[0], dst = yp[row];
   const uint64_t ndw = g.n * 4;                       // dwords per row
   uint64_t h, nbody;
@@ -1113,27 +1114,34 @@ size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev) {
   return align16(off + (size_t)(nlev + 1) * 4);
 }
 
-hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
-                     bool rows16, uint64_t span_bytes, bool fastdiv_tiles,
-                     hipStream_t stream) {
-  BcastGrid g = bcast_grid(nbytes, vec16 ? 16 : 4, p, span_bytes);
-  g.fast = fastdiv_tiles && g.total <= 0xFFFFFFFFull;
+template <bool FAST>
+hipError_t broadcast_t(const Tables& tab, const BcastGrid& g, bool vec16,
+                       bool rows16, hipStream_t stream) {
   // a launch's thread count stays below 2^32: pieces of at most 2^23
   // workgroups (a multiple of 8, so workgroup w stays on XCD w mod 8)
   const uint64_t kMaxGrid = (1ull << 31) / 256;
   for (uint64_t first = 0; first < g.total; first += kMaxGrid) {
     const unsigned n = (unsigned)min(kMaxGrid, g.total - first);
     if (vec16 && rows16)
-      hipLaunchKernelGGL((k_bcast<u32x4g>), dim3(n), dim3(256), 0, stream,
-                         tab.yp, g, first);
+      hipLaunchKernelGGL((k_bcast<u32x4g, FAST>), dim3(n), dim3(256), 0,
+                         stream, tab.yp, g, first);
     else if (vec16)
-      hipLaunchKernelGGL(k_bcast16_rows, dim3(n), dim3(256), 0, stream,
-                         tab.yp, g, first);
+      hipLaunchKernelGGL((k_bcast16_rows<FAST>), dim3(n), dim3(256), 0,
+                         stream, tab.yp, g, first);
     else
-      hipLaunchKernelGGL((k_bcast<uint32_t>), dim3(n), dim3(256), 0, stream,
-                         tab.yp, g, first);
+      hipLaunchKernelGGL((k_bcast<uint32_t, FAST>), dim3(n), dim3(256), 0,
+                         stream, tab.yp, g, first);
   }
   return hipGetLastError();
+}
+
+hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
+                     bool rows16, uint64_t span_bytes, bool fastdiv_tiles,
+                     hipStream_t stream) {
+  BcastGrid g = bcast_grid(nbytes, vec16 ? 16 : 4, p, span_bytes);
+  g.fast = fastdiv_tiles && g.total <= 0xFFFFFFFFull;
+  return g.fast ? broadcast_t<true>(tab, g, vec16, rows16, stream)
+                : broadcast_t<false>(tab, g, vec16, rows16, stream);
 }
 
 size_t lds_bytes(Path path, Kind kind, int waves, int nslots) {

@@ -193,7 +193,7 @@ struct BcastGrid {
   uint64_t total = 0;   // workgroups nspan * rows * ts
   uint64_t m_ts = 0;    // fastdiv_magic(ts)
   uint64_t m_span = 0;  // fastdiv_magic(rows * ts)
-  uint64_t fast = 0;    // 1: bcast_tile divides by multiplication (needs
+  uint64_t fast = 0;    // 1: the pass runs bcast_tile<true> (needs
                         // total < 2^32; the host decides, see broadcast())
 };
 
@@ -221,12 +221,14 @@ BcastGrid bcast_grid(uint64_t nbytes, uint64_t lane_bytes, int p,
                      uint64_t span_bytes);
 
 // Output row (1 .. p-1) and tile of workgroup w < g.total: span
-// w / (rows ts), in it row 1 + (w / ts) mod rows and tile w mod ts.  With
-// g.fast the divisions are multiplications (fastdiv), else divisions.
+// w / (rows ts), in it row 1 + (w / ts) mod rows and tile w mod ts.
+// FAST (grids of fewer than 2^32 workgroups, g.fast set): the divisions are
+// multiplications (fastdiv).
+template <bool FAST>
 DPAR_HOST_DEVICE inline void bcast_tile(const BcastGrid& g, uint64_t w,
                                         uint64_t* row, uint64_t* tile) {
   const uint64_t per_span = g.rows * g.ts;
-  if (g.fast && g.total <= 0xFFFFFFFFull) {
+  if (FAST) {
     const uint32_t w32 = (uint32_t)w;
     const uint32_t span = fastdiv(w32, g.m_span, per_span);
     const uint32_t r = w32 - span * (uint32_t)per_span;

@@ -89,8 +89,10 @@ int main() {
     std::vector<unsigned char> seen(g.rows * tiles, 0);
     uint64_t covered = 0, padded = 0, bad = 0;
     for (uint64_t w = 0; w < g.total; ++w) {
-      uint64_t row, tile;
-      dpar::bcast_tile(g, w, &row, &tile);
+      uint64_t row, tile, row_d, tile_d;
+      dpar::bcast_tile<true>(g, w, &row, &tile);
+      dpar::bcast_tile<false>(g, w, &row_d, &tile_d);
+      if (row != row_d || tile != tile_d) ++bad;
       // the same pair by plain division
       const uint64_t per_span = g.rows * g.ts, sp = w / per_span;
       if (row != 1 + (w - sp * per_span) / g.ts ||
