@@ -371,3 +371,22 @@ def test_per_round_executors_take_subtree_items_for_mid_rounds(exec, capfd):
     err = capfd.readouterr().err
     assert "unit=subtree" in err, err[-400:]
     assert_all_ranks_equal(out, want, f"{exec} subtree rounds")
+
+
+@pytest.mark.parametrize("m,unit", [(1 << 17, "subtree"),
+                                    ((1 << 17) + 256, "postorder")])
+def test_subtree_item_boundary_two_per_cu(m, unit, capfd):
+    """The library's own choice at the boundary of two subtree items per CU
+    (256 CUs): p = 1152, m = 2^17 is 512 whole chunks of 64 quanta
+    (subtree items, one fused launch); 256 more columns make 513 chunks
+    (post-order items, split).  Both at the rule's b, bit-exact in fp32,
+    every rank's output."""
+    from tests._gpu import _Env
+    need_gpu()
+    x = _input("normal_f32", 2191, 1152, m)
+    want = _want(x, "float32", "sum", "dual")
+    with env_unit(None), _Env("DPAR_LOG", 1):
+        out = from_dev(_run(x, "float32", "sum", 0, "dual", "auto"), x)
+    err = capfd.readouterr().err
+    assert f"unit={unit}" in err, err[-400:]
+    assert_all_ranks_equal(out, want, f"boundary m={m}")
