@@ -312,3 +312,28 @@ def test_work_item_limit_is_checked_before_narrowing():
     ys = [A + (2 << 41), A + (3 << 41)]
     assert _err(dpar.dpar_allreduce_ex, xs, ys, 2, 1 << 39, "int32", "sum", 1,
                 "split") == dpar.DPAR_ERR_UNSUPPORTED
+
+
+def test_noalloc_argument_errors_before_device_work():
+    """dpar_allreduce_noalloc checks its arguments like dpar_allreduce, and
+    refuses p beyond the ranks its fixed device memory holds, all before
+    any device work (so on the CPU too)."""
+    f = dpar.dpar_allreduce_noalloc
+    xs = [A + i * 4096 for i in range(4)]
+    ys = [A + (1 << 20) + i * 4096 for i in range(4)]
+    assert _err(f, xs, ys, 0, 1000, "int32", "sum", 4) == \
+        dpar.DPAR_ERR_INVALID_ARG
+    assert _err(f, xs, ys, 4, 1000, "int32", "sum", 1001) == \
+        dpar.DPAR_ERR_INVALID_ARG
+    assert _err(f, xs, ys, 4, 1000, "float32", "max", 4) == \
+        dpar.DPAR_ERR_UNSUPPORTED
+    assert _err(f, xs, [A + 8] + ys[1:], 4, 1000, "int32", "sum", 4) == \
+        dpar.DPAR_ERR_ALIAS
+    big = 32769
+    bx = [A + i * 8192 for i in range(big)]
+    by = [A + (1 << 32) + i * 8192 for i in range(big)]
+    assert _err(f, bx, by, big, 16, "int32", "sum", 0) == \
+        dpar.DPAR_ERR_UNSUPPORTED
+    assert "32768" in dpar.dpar_last_error()
+    # m = 0 is a successful no-op, as for dpar_allreduce
+    assert f(xs, ys, 4, 0, "int32", "sum", 0) == 0
