@@ -320,8 +320,13 @@ const char* dpar_last_error(void);
 
 /* Tuning and test knobs, read from the environment at every call; none of
  * them changes what a call computes:
- *   DPAR_UNIT=seq|level|sub force the post-order, level or subtree work
- *                           item
+ *   DPAR_UNIT=seq|level|sub|wide
+ *                           force the post-order, level, subtree or wide
+ *                           post-order work item (wide: 16-byte lanes and
+ *                           the one-launch executors only, else post-order;
+ *                           by default it runs one-launch calls with at
+ *                           most 128 ranks and at least one 16 KB column
+ *                           chunk per CU)
  *   DPAR_LEVEL_LOG2T=k      level work items of 2^k quanta (at most what
  *                           fits in LDS)
  *   DPAR_SUB_DEEP=0|1       subtree work items with 8 or 16 loads in flight

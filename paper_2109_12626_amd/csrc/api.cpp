@@ -52,6 +52,9 @@ constexpr int kCapMinRanks = 256;
 constexpr int kCapMinItemsPerCu = 64;
 // Subtree work items: the deep load pipeline from this many ranks on.
 constexpr int kSubDeepMinRanks = 1024;
+// Wide post-order work items (kernels.hpp Unit::WIDE) for one-launch calls
+// with at most kWideMaxRanks ranks and at least one wide item per CU.
+constexpr int kWideMaxRanks = 128;
 // Level work item: loads in flight at once (1024 threads, 8 loads each).
 constexpr uint64_t kLvLoadsInFlight = 1024 * 8;
 // Ticket executor: rank loads per claimed batch of work items.
@@ -717,6 +720,10 @@ struct UnitChoice {
 //         17.9 vs 15.8 ms), or for few short chunks with long chains (a
 //         post-order item costs its p/2-load chain however little it
 //         carries: p = 1152, m = 4096, b = 205: 117 us post-order, 31 level);
+//   WIDE  the post-order walk with kWideQ quanta per lane: a whole call
+//         (split, ticket, one fused launch) on 16-byte lanes with at most
+//         kWideMaxRanks ranks and at least one wide item (kWideChunk
+//         quanta) per CU, i.e. short walks over long rows;
 //   SUB   eight subtree walks, then the spines: a whole call (split,
 //         ticket, one fused launch) in at most two full chunks per CU
 //         with p >= 256 (p = 1152, m = 2^16, b = 1: 0.113 vs 0.165 ms;
@@ -816,7 +823,18 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
     }
   }
   if (forced) want_sub = !std::strcmp(u, "sub") && sub_fits;
-  if (want_sub) uc.unit = dpar::Unit::SUB;
+  if (want_sub) {
+    uc.unit = dpar::Unit::SUB;
+    return uc;
+  }
+  const bool wide_fits =
+      whole_call && lane_bytes == 16 &&
+      dpar::wide_lds_bytes(lane_bytes, ops.height + 1) <=
+          (size_t)st.lds_limit - dpar::kStaticLdsReserve;
+  bool want_wide = wide_fits && p <= kWideMaxRanks &&
+                   (s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk >= cus;
+  if (forced) want_wide = !std::strcmp(u, "wide") && wide_fits;
+  if (want_wide) uc.unit = dpar::Unit::WIDE;
   return uc;
 }
 
@@ -835,8 +853,10 @@ const char* exec_name(dpar::Exec e) {
 }
 
 const char* unit_name(dpar::Unit u) {
-  return u == dpar::Unit::LEVEL ? "level" : u == dpar::Unit::SUB ? "subtree"
-                                                                  : "postorder";
+  return u == dpar::Unit::LEVEL  ? "level"
+         : u == dpar::Unit::SUB  ? "subtree"
+         : u == dpar::Unit::WIDE ? "wide"
+                                 : "postorder";
 }
 
 // DPAR_LOG=1: one line per call on stderr with the plan it runs (tree
@@ -1175,6 +1195,19 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     prm.sub_deep = env_int("DPAR_SUB_DEEP",
                            p >= kSubDeepMinRanks &&
                                sub_items <= (uint64_t)st->num_cus);
+  }
+  if (unit == dpar::Unit::WIDE) {
+    // One launch of wide items (one-launch executors only): item t takes the
+    // quanta [t kWideChunk, (t + 1) kWideChunk), whatever the blocks, as the
+    // subtree items above (element-wise, so the result does not depend on
+    // the cut); each item is claimed on its own.
+    const dpar::Schedule s1 = dpar::make_schedule(m, 1, s.g, 8);
+    prm.b = 1;
+    prm.NL = s1.NL;
+    prm.lq = (uint32_t)s1.lq;
+    prm.C = (int)((s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk);
+    prm.grp = 1;
+    prm.batch = 1;
   }
   // round-structured down-step: two ranks per wavefront per work item, the
   // largest block in pieces of kDownPiece quanta

@@ -193,6 +193,7 @@ static_assert(2 * kU <= kTablePad, "tables are padded for 2 * kU reads");
 // per wavefront, for calls whose items all run at once, one per CU.
 constexpr int kUDeep = 16;
 static_assert(2 * kUDeep <= kTablePad, "tables are padded for 2 * kU reads");
+static_assert(16 <= kTablePad, "the wide walk reads two groups of 8 ahead");
 
 // Up-step of one chunk over the ranks [r0, r1) in post-order (Algorithm 1's
 // "Y <- t (.) Y" with the first child's block, then with the second
@@ -570,6 +571,183 @@ __device__ __forceinline__ void run_unit_sub(const uint64_t* __restrict__ xp,
   __syncthreads();  // LDS is reused by the next work item
 }
 
+// ------------------------------------------------------------ wide units
+// Post-order work item for short walks over long rows.  A wavefront carries
+// kWideQ quanta per lane (lane l: quanta l, l + 64, ...), so each rank
+// visit reads kWideQ contiguous pieces of 64 quanta (kWideQ KB of the row
+// on 16-byte lanes), with kWideKF visits in flight; the workgroup's
+// kWideWaves wavefronts take neighbouring column ranges of its chunk, and
+// each walks both trees (all p ranks, tree A then tree B) for its own
+// columns, so the wavefronts never wait for each other.  Same association,
+// same operations as the post-order work item, per column.  Only the
+// one-launch executors run it, over chunks of kWideChunk quanta.
+//
+// Why: with few ranks every work item's walk is short, all the items of a
+// call run at once and proceed in step, and one-KB pieces with many ranks
+// in flight per wavefront then read HBM slowly (p = 36, rows of 4 MB:
+// 5.5 TB/s with 1 KB per visit and 8 visits in flight; 6.5 TB/s with
+// 4 KB per visit and 2 in flight, as fast as contiguous 16 KB tiles).
+//
+// LDS: per wavefront nslots depth slots of kWideQ x 64 lanes, slot d's
+// piece u at [(d kWideQ + u) 64 + lane] (one 16-byte access per lane,
+// conflict-free).
+
+// The scalars a wide work item reads: 64 bytes, loaded together at the
+// start of its kernel.
+struct WideArgs {
+  const uint64_t* xp;
+  const uint64_t* yp;
+  const uint32_t* ops;
+  uint64_t Q;
+  uint64_t qbase;
+  int p;
+  int nslots;
+  int out0;
+  int out1;
+  int dual;
+  int unused;
+};
+
+__host__ __device__ inline WideArgs wide_args(const uint64_t* xp,
+                                              const uint64_t* yp,
+                                              const uint32_t* ops,
+                                              const Params& prm) {
+  return WideArgs{xp,       yp,          ops,       prm.Q,    prm.qbase,
+                  prm.p,    prm.nslots,  prm.out0,  prm.out1, prm.dual,
+                  0};
+}
+
+template <class L, bool FUSED>
+__device__ __forceinline__ void run_unit_wide(const WideArgs& a, uint64_t t,
+                                              typename L::T* slots) {
+  using T = typename L::T;
+  const uint64_t* __restrict__ xp = a.xp;
+  const uint64_t* __restrict__ yp = a.yp;
+  const uint32_t* __restrict__ ops = a.ops;
+  constexpr int QW = kWideQ, KF = kWideKF;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+
+  // Work item t: quanta [t kWideChunk, (t + 1) kWideChunk) of the call's
+  // Q (the host cuts the columns into whole wide chunks, whatever the
+  // blocks); this wavefront's share [ws, we).
+  const uint64_t ws = min(t * kWideChunk + (uint64_t)wave * 64 * QW, a.Q);
+  const uint64_t we = min(ws + 64 * QW, a.Q);
+  const uint32_t count = (uint32_t)(we - ws);
+  // wave-uniform; the unit has no workgroup barrier, so a wavefront without
+  // columns may leave at once
+  if (count == 0) return;
+  const uint64_t unit_off = (a.qbase + ws) * (uint64_t)L::bytes;
+  // piece u of this lane: quantum lane + 64 u; lanes past the wavefront's
+  // columns re-read its last quantum (no branch on the loads)
+  uint32_t off[QW];
+  bool act[QW];
+#pragma unroll
+  for (int u = 0; u < QW; ++u) {
+    const uint32_t q = (uint32_t)lane + 64u * u;
+    act[u] = q < count;
+    off[u] = (act[u] ? q : count - 1) * L::bytes;
+  }
+  T* my = slots + (size_t)wave * a.nslots * QW * 64 + lane;
+
+  const int p = a.p;
+  T cur[QW];
+#pragma unroll
+  for (int u = 0; u < QW; ++u) cur[u] = T{};
+  // rank visit: rank i's pieces combined with its first child's value
+  // (cur) and its second child's (slot d + 1), then parked in slot d (a
+  // second child) or kept as cur
+  auto step = [&](T (&v)[QW], uint32_t op) {
+    const int d = (int)(op & OP_DEPTH_MASK);
+#pragma unroll
+    for (int u = 0; u < QW; ++u) {
+      T w = v[u];
+      if (op & OP_C0) w = L::ap(cur[u], w);
+      if (op & OP_C1) w = L::ap(my[((d + 1) * QW + u) * 64], w);
+      if (op & OP_SAVE)
+        my[(d * QW + u) * 64] = w;
+      else
+        cur[u] = w;
+    }
+  };
+  // Rotating pipeline of KF visits: buffer slot k % KF holds visit k and
+  // is refilled with visit k + KF once its step is done.  The row
+  // addresses and opcodes come from the tables a group of G visits ahead
+  // (scalar loads issued a group before they are needed); ranks past p
+  // re-read row p - 1 and are not processed (the opcode table is padded).
+  constexpr int G = 8;
+  static_assert(G % KF == 0 && KF <= G, "groups hold whole pipelines");
+  // (ranks past p read row p - 1 through a clamped index: a table load
+  // under a condition would become a branch around a scalar load that waits
+  // for it)
+  uint64_t row_cur[G];
+  uint32_t op_cur[G];
+#pragma unroll
+  for (int k = 0; k < G; ++k) {
+    row_cur[k] = xp[min(k, p - 1)] + unit_off;
+    op_cur[k] = ops[k];
+  }
+  T buf[KF][QW];
+#pragma unroll
+  for (int k = 0; k < KF; ++k) {
+#pragma unroll
+    for (int u = 0; u < QW; ++u) buf[k][u] = L::load(row_cur[k], off[u]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (int gb = 0; gb < p; gb += G) {
+    uint64_t row_nxt[G];
+    uint32_t op_nxt[G];
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+      row_nxt[k] = xp[min(gb + G + k, p - 1)] + unit_off;
+      op_nxt[k] = ops[gb + G + k];
+    }
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+      const uint64_t nrow = k + KF < G ? row_cur[k + KF] : row_nxt[k + KF - G];
+      // consumed before refilled: at most KF visits in flight (measured
+      // 0-2% faster than refilling first, with one visit more in flight)
+      if (gb + k < p) step(buf[k % KF], op_cur[k]);
+#pragma unroll
+      for (int u = 0; u < QW; ++u) buf[k % KF][u] = L::load(nrow, off[u]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+      row_cur[k] = row_nxt[k];
+      op_cur[k] = op_nxt[k];
+    }
+  }
+
+  // dual-root combine: tree A's root waits in slot 0, tree B's is cur
+  T y[QW];
+#pragma unroll
+  for (int u = 0; u < QW; ++u)
+    y[u] = a.dual ? L::ap(my[u * 64], cur[u]) : my[u * 64];
+
+  if (!FUSED) {
+#pragma unroll
+    for (int u = 0; u < QW; ++u) {
+      if (!act[u]) continue;
+      L::store(yp[a.out0] + unit_off, off[u], y[u]);
+      if (a.out1 >= 0) L::store(yp[a.out1] + unit_off, off[u], y[u]);
+    }
+  } else {
+    for (int base = 0; base < p; base += kU) {
+      uint64_t row[kU];
+#pragma unroll
+      for (int k = 0; k < kU; ++k) row[k] = yp[base + k] + unit_off;
+#pragma unroll
+      for (int k = 0; k < kU; ++k) {
+        if (base + k >= p) continue;
+#pragma unroll
+        for (int u = 0; u < QW; ++u)
+          if (act[u]) L::store(row[k], off[u], y[u]);
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------ unit policies
 
 template <class L, int W, bool FUSED>
@@ -624,6 +802,24 @@ struct LvUnit {
   }
 };
 
+template <class L, bool FUSED>
+struct WideUnit {
+  using Lane = L;
+  static constexpr int kThreads = 64 * kWideWaves;
+  __device__ static void run(const uint64_t* __restrict__ xp,
+                             const uint64_t* __restrict__ yp,
+                             const uint32_t* __restrict__ ops,
+                             const uint32_t* __restrict__ lvl,
+                             const Params& prm, uint64_t t, char* lds) {
+    (void)lvl;
+    run_unit_wide<L, FUSED>(wide_args(xp, yp, ops, prm), t,
+                            reinterpret_cast<typename L::T*>(lds));
+  }
+  static size_t lds(const Params& prm) {
+    return wide_lds_bytes(sizeof(typename L::T), prm.nslots);
+  }
+};
+
 // ------------------------------------------------------------ executors
 
 #define DPAR_KARGS                                                     \
@@ -639,6 +835,16 @@ __global__ __launch_bounds__(U::kThreads) void k_round(DPAR_KARGS, int round,
   const uint64_t w =
       prm.xcd_runs ? xcd_run_index(blockIdx.x, gridDim.x) : blockIdx.x;
   U::run(xp, yp, ops, lvl, prm, (uint64_t)round * prm.C + first + w, lds_raw);
+}
+
+// One launch of wide work items (split up-phase, one fused launch): item
+// first + blockIdx.x, its scalars in one 64-byte argument.
+template <class L, bool FUSED>
+__global__ __launch_bounds__(64 * kWideWaves) void k_wide(WideArgs a,
+                                                         uint64_t first) {
+  extern __shared__ char lds_raw[];
+  run_unit_wide<L, FUSED>(a, first + blockIdx.x,
+                          reinterpret_cast<typename L::T*>(lds_raw));
 }
 
 __device__ inline void grid_barrier(const Params& prm) {
@@ -958,6 +1164,23 @@ hipError_t occupancy(const void* kfn, int threads, size_t lds, int* out) {
   return e;
 }
 
+// The persistent ticketed executor: per_cu workgroups per CU, no more than
+// there are batches of work items.
+template <class U>
+hipError_t launch_ticket(const Tables& tab, const Params& prm,
+                         hipStream_t stream, int num_cus, size_t lds,
+                         int per_cu) {
+  // no workgroup fits (dynamic plus static LDS beyond a CU's): never launch
+  if (per_cu < 1) return hipErrorInvalidConfiguration;
+  const uint64_t nunits = item_groups(prm) * prm.C;
+  uint64_t grid = (uint64_t)per_cu * num_cus;
+  const uint64_t batches = (nunits + prm.batch - 1) / prm.batch;
+  if (grid > batches) grid = batches;
+  hipLaunchKernelGGL((k_ticket<U>), dim3((unsigned)grid), dim3(U::kThreads),
+                     lds, stream, tab.xp, tab.yp, tab.ops, tab.lvl, prm);
+  return hipGetLastError();
+}
+
 template <class U>
 hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
                     hipStream_t stream, int num_cus, size_t lds_floor) {
@@ -1042,14 +1265,33 @@ hipError_t launch_u(Exec exec, const Tables& tab, const Params& prm,
     return hipLaunchCooperativeKernel(kfn, dim3((unsigned)grid), block, args,
                                       (unsigned)lds, stream);
   }
-  // no workgroup fits (dynamic plus static LDS beyond a CU's): never launch
-  if (per_cu < 1) return hipErrorInvalidConfiguration;
-  uint64_t grid = (uint64_t)per_cu * num_cus;
-  const uint64_t batches = (nunits + prm.batch - 1) / prm.batch;
-  if (grid > batches) grid = batches;
-  hipLaunchKernelGGL((k_ticket<U>), dim3((unsigned)grid), block, lds, stream,
-                     tab.xp, tab.yp, tab.ops, tab.lvl, prm);
-  return hipGetLastError();
+  return launch_ticket<U>(tab, prm, stream, num_cus, lds, per_cu);
+}
+
+// Wide work items: one launch of k_wide, one workgroup per item (split
+// up-phase, one fused launch), or the persistent ticketed executor.
+template <class L, bool FUSED>
+hipError_t launch_wide(Exec exec, const Tables& tab, const Params& prm,
+                       hipStream_t stream, int num_cus) {
+  using U = WideUnit<L, FUSED>;
+  const size_t lds = U::lds(prm);
+  const uint64_t nunits = item_groups(prm) * prm.C;
+  if (exec == Exec::DISPATCH) {
+    const WideArgs a = wide_args(tab.xp, tab.yp, tab.ops, prm);
+    const uint64_t kMaxGrid = (1ull << 31) / U::kThreads;
+    for (uint64_t first = 0; first < nunits; first += kMaxGrid) {
+      const uint64_t n = min(kMaxGrid, nunits - first);
+      hipLaunchKernelGGL((k_wide<L, FUSED>), dim3((unsigned)n),
+                         dim3(U::kThreads), lds, stream, a, first);
+    }
+    return hipGetLastError();
+  }
+  if (exec != Exec::TICKET) return hipErrorInvalidValue;
+  int per_cu = 0;
+  const hipError_t e = occupancy(reinterpret_cast<const void*>(&k_ticket<U>),
+                                 U::kThreads, lds, &per_cu);
+  if (e != hipSuccess) return e;
+  return launch_ticket<U>(tab, prm, stream, num_cus, lds, per_cu);
 }
 
 template <class L>
@@ -1072,6 +1314,15 @@ hipError_t launch_l(Unit unit, int waves, Exec exec, const Tables& tab,
                    : DPAR_LAUNCH_U(SubUnit<L, false, kUDeep>);
     return fused ? DPAR_LAUNCH_U(SubUnit<L, true>)
                  : DPAR_LAUNCH_U(SubUnit<L, false>);
+  }
+  if (unit == Unit::WIDE) {
+    // 16-byte lanes and one-launch executors only (the host asks for
+    // nothing else)
+    if constexpr (L::bytes == 16)
+      return fused ? launch_wide<L, true>(ex, tab, prm, stream, num_cus)
+                   : launch_wide<L, false>(ex, tab, prm, stream, num_cus);
+    else
+      return hipErrorInvalidValue;
   }
   if (waves == 2)
     return fused ? DPAR_LAUNCH_U(SeqUnit<L, 2, true>)
@@ -1142,6 +1393,10 @@ hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
   g.fast = fastdiv_tiles && g.total <= 0xFFFFFFFFull;
   return g.fast ? broadcast_t<true>(tab, g, vec16, rows16, stream)
                 : broadcast_t<false>(tab, g, vec16, rows16, stream);
+}
+
+size_t wide_lds_bytes(size_t lane_bytes, int nslots) {
+  return (size_t)kWideWaves * nslots * kWideQ * 64 * lane_bytes;
 }
 
 size_t lds_bytes(Path path, Kind kind, int waves, int nslots) {

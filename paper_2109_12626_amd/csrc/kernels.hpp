@@ -16,8 +16,10 @@ enum class Path : int { VEC16 = 0, SCALAR = 1 };
 // wavefront over 16-byte lanes (SEQ) or level by level with the whole chunk
 // staged in LDS (LEVEL; short chunks, latency-bound cases).
 // SUB: the trees cut into subtrees, one wavefront each, then the spines
-// (few chunks, large p).
-enum class Unit : int { SEQ = 0, LEVEL = 1, SUB = 2 };
+// (few chunks, large p).  WIDE: the post-order walk with kWideQ quanta per
+// lane and kWideWaves wavefronts on neighbouring columns (few ranks, long
+// rows; 16-byte lanes).
+enum class Unit : int { SEQ = 0, LEVEL = 1, SUB = 2, WIDE = 3 };
 enum class Exec : int {
   LAUNCH_PER_ROUND = 1,
   GRID_BARRIER = 2,
@@ -124,6 +126,27 @@ constexpr size_t kStaticLdsReserve = 256;
 
 // Bytes of dynamic LDS a LEVEL work item needs.
 size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev);
+
+// WIDE work items: quanta per lane, wavefronts per workgroup (each on its
+// own 64 kWideQ quanta of the chunk), rank visits in flight per wavefront.
+#ifndef DPAR_WIDE_Q
+#define DPAR_WIDE_Q 4
+#endif
+#ifndef DPAR_WIDE_WAVES
+#define DPAR_WIDE_WAVES 4
+#endif
+#ifndef DPAR_WIDE_KF
+#define DPAR_WIDE_KF 2
+#endif
+constexpr int kWideQ = DPAR_WIDE_Q;
+constexpr int kWideWaves = DPAR_WIDE_WAVES;
+constexpr int kWideKF = DPAR_WIDE_KF;
+// Quanta of one WIDE work item.
+constexpr uint64_t kWideChunk = 64ull * kWideQ * kWideWaves;
+
+// Bytes of dynamic LDS a WIDE work item needs with `nslots` slots per
+// wavefront (lane_bytes 16).
+size_t wide_lds_bytes(size_t lane_bytes, int nslots);
 
 // Bytes of dynamic LDS a SUB work item needs with `ns` slots per wavefront
 // (lane_bytes: 16 on the vector path and for matrices, else 4).

@@ -40,8 +40,38 @@ def _case(k):
 @pytest.mark.parametrize("k", range(300))
 def test_random_combination(k):
     need_gpu()
+    _check_case(_case(k))
+
+
+def _wide_case(k):
+    r = np.random.default_rng(9700 + k)
+    p = int(r.integers(2, 129))
+    dtype, op, dist = PAIRS[int(r.integers(len(PAIRS)))]
+    words = 4 if dtype == "u32mat2x2" else 1
+    # up to 2^20 words of input: a few wide items (1024 quanta each) with a
+    # ragged last one, or less than one
+    m = int(r.integers(1, max(2, (1 << 20) // (p * words))))
+    b = int(r.choice([0, 1, int(r.integers(1, m + 1))]))
+    return dict(p=p, m=m, b=min(b, m), dtype=dtype, op=op, dist=dist,
+                alg=ALGS[int(r.integers(3))],
+                exec=["auto", "split", "ticket"][int(r.integers(3))],
+                unit="wide", misalign=bool(r.integers(2)),
+                inplace=bool(r.integers(4) == 0), separate=bool(r.integers(2)),
+                seed=2700 + k)
+
+
+@pytest.mark.parametrize("k", range(60))
+def test_random_wide_items(k):
+    """Seeded random calls with the wide post-order work item forced (the
+    one-launch executors; on 4-byte lanes the library keeps the plain
+    post-order item): p = 2 .. 128, every operator and tree layout,
+    misaligned rows, in place, separate allocations."""
+    need_gpu()
+    _check_case(_wide_case(k))
+
+
+def _check_case(c):
     dpar = lib()
-    c = _case(k)
     p, m = c["p"], c["m"]
     kw = {"lo": -50, "hi": 50} if c["dist"] == "uniform_int" else {}
     x = synth.generate(c["dist"], c["seed"], p, m, **kw)

@@ -390,3 +390,71 @@ def test_subtree_item_boundary_two_per_cu(m, unit, capfd):
     err = capfd.readouterr().err
     assert f"unit={unit}" in err, err[-400:]
     assert_all_ranks_equal(out, want, f"boundary m={m}")
+
+
+@pytest.mark.parametrize("alg", ALGS)
+@pytest.mark.parametrize("exec", ["auto", "split", "ticket"])
+@pytest.mark.parametrize("p", [2, 3, 7, 36, 64, 100, 128])
+def test_wide_unit(alg, exec, p, capfd):
+    """The wide post-order work item (4 quanta per lane, 4 wavefronts on
+    neighbouring columns, each walking both trees): bit-exact fp32 for every
+    algorithm and one-launch executor.  m = 4 (3 * 1024 + 300): three whole
+    wide items and a ragged fourth (one full wavefront, one partial, two
+    without columns).  (Trailing elements: test_wide_unit_choice.)"""
+    from tests._gpu import _Env
+    need_gpu()
+    m = 4 * (3 * 1024 + 300)
+    x = _input("normal_f32", 2200 + p, p, m)
+    want = _want(x, "float32", "sum", alg)
+    for b in (1, 0):
+        with env_unit("wide"), _Env("DPAR_LOG", 1):
+            out = from_dev(_run(x, "float32", "sum", b, alg, exec), x)
+        err = capfd.readouterr().err
+        assert "unit=wide " in err, err[-400:]
+        assert_all_ranks_equal(out, want, f"wide {alg}/{exec}/p={p}/b={b}")
+
+
+@pytest.mark.parametrize("dtype,op,dist", [("int32", "max", "uniform_int"),
+                                           ("int32", "sum", "uniform_int"),
+                                           ("u32mat2x2", "matmul",
+                                            "uniform_u32_mat")])
+def test_wide_unit_other_operators(dtype, op, dist):
+    """Matrices keep the rank order (left-to-right product) through the
+    wide item's slots and dual-root combine."""
+    need_gpu()
+    kw = {"lo": -99, "hi": 99} if dist == "uniform_int" else {}
+    x = _input(dist, 2201, 45, 5000, **kw)
+    want = oracle.allreduce_ltr(x, dtype, op)
+    for exec in ("auto", "split", "ticket"):
+        with env_unit("wide"):
+            out = from_dev(_run(x, dtype, op, 3, "dual", exec), x)
+        assert_all_ranks_equal(out, want, f"wide {dtype}/{exec}")
+
+
+@pytest.mark.parametrize("p,m,dtype,unit", [
+    (36, 1 << 20, "int32", "wide"),            # 256 wide items
+    (36, (1 << 20) + 3, "int32", "wide"),      # and 3 trailing elements
+    (36, 4 * (255 * 1024), "int32", "postorder"),  # 255: fewer than CUs
+    (128, 1 << 20, "int32", "wide"),
+    (129, 1 << 20, "int32", "postorder"),      # beyond the rank limit
+    (64, 1 << 18, "u32mat2x2", "wide"),        # the 64-rank matrix product
+])
+def test_wide_unit_choice(p, m, dtype, unit, capfd):
+    """The library's own choice (split executor, the rule's b): wide items
+    for few ranks and at least one wide item per CU (256 CUs), post-order
+    items otherwise (shown by DPAR_LOG), bit-exact against the oracle."""
+    from tests._gpu import _Env
+    need_gpu()
+    if dtype == "u32mat2x2":
+        x = _input("uniform_u32_mat", 2202, p, m)
+        op = "matmul"
+        want = oracle.allreduce_ltr(x, dtype, op)
+    else:
+        x = _input("uniform_int", 2203, p, m, lo=-1000, hi=1000)
+        op = "sum"
+        want = oracle.allreduce_ltr(x, dtype, op)
+    with env_unit(None), _Env("DPAR_LOG", 1):
+        out = from_dev(_run(x, dtype, op, 0, "dual", "auto"), x)
+    err = capfd.readouterr().err
+    assert f"unit={unit} " in err, err[-400:]
+    assert_all_ranks_equal(out, want, f"choice p={p} m={m}")
