@@ -323,10 +323,11 @@ const char* dpar_last_error(void);
  *   DPAR_UNIT=seq|level|sub|wide
  *                           force the post-order, level, subtree or wide
  *                           post-order work item (wide: 16-byte lanes and
- *                           the one-launch executors only, else post-order;
- *                           by default it runs one-launch calls with at
- *                           most 128 ranks and at least one 16 KB column
- *                           chunk per CU)
+ *                           the one-launch executors and p < 1024 only,
+ *                           else post-order; by default it runs one-launch
+ *                           calls with at least one 16 KB column chunk per
+ *                           CU unless the split up-phase caps its
+ *                           post-order items' residency)
  *   DPAR_LEVEL_LOG2T=k      level work items of 2^k quanta (at most what
  *                           fits in LDS)
  *   DPAR_SUB_DEEP=0|1       subtree work items with 8 or 16 loads in flight

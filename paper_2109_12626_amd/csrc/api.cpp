@@ -52,9 +52,6 @@ constexpr int kCapMinRanks = 256;
 constexpr int kCapMinItemsPerCu = 64;
 // Subtree work items: the deep load pipeline from this many ranks on.
 constexpr int kSubDeepMinRanks = 1024;
-// Wide post-order work items (kernels.hpp Unit::WIDE) for one-launch calls
-// with at most kWideMaxRanks ranks and at least one wide item per CU.
-constexpr int kWideMaxRanks = 128;
 // Level work item: loads in flight at once (1024 threads, 8 loads each).
 constexpr uint64_t kLvLoadsInFlight = 1024 * 8;
 // Ticket executor: rank loads per claimed batch of work items.
@@ -705,6 +702,14 @@ int block_group(dpar::Exec ex, const dpar::Schedule& s) {
   return dpar::block_group(s);
 }
 
+// The split up-phase's residency cap for post-order work items (at most
+// kSeqWgPerCu workgroups per CU, set through the LDS request): long walks
+// (p >= kCapMinRanks) and at least kCapMinItemsPerCu items per CU.
+bool seq_wg_capped(int p, uint64_t items, const DeviceState& st) {
+  return p >= kCapMinRanks &&
+         items >= (uint64_t)kCapMinItemsPerCu * (uint64_t)st.num_cus;
+}
+
 struct UnitChoice {
   dpar::Unit unit = dpar::Unit::SEQ;
   int lv_log2t = 0;  // LEVEL: log2 of the chunk capacity in quanta
@@ -721,9 +726,16 @@ struct UnitChoice {
 //         post-order item costs its p/2-load chain however little it
 //         carries: p = 1152, m = 4096, b = 205: 117 us post-order, 31 level);
 //   WIDE  the post-order walk with kWideQ quanta per lane: a whole call
-//         (split, ticket, one fused launch) on 16-byte lanes with at most
-//         kWideMaxRanks ranks and at least one wide item (kWideChunk
-//         quanta) per CU, i.e. short walks over long rows;
+//         (split, ticket, one fused launch) on 16-byte lanes whose slots
+//         fit in LDS (p < 1024) with at least one wide item (16 KB of
+//         columns) per CU, unless the split up-phase would run post-order
+//         items under its residency cap
+//         (measured, int32 SUM, split, rows of 4 / 8 / 16 MB: p = 36
+//         61.4 -> 57.5, 110 -> 103, 211 -> 195 us; p = 128 180 -> 164,
+//         340 -> 315, 675 -> 627 us; p = 511 667 -> 611, 1311 -> 1235 us;
+//         under the cap, p = 256 .. 768 with 16 MB rows, post-order items
+//         are 0-4% faster; 2 wavefronts per item for deeper trees won only
+//         at p = 1152 with 4 MB rows and lost up to 30% elsewhere);
 //   SUB   eight subtree walks, then the spines: a whole call (split,
 //         ticket, one fused launch) in at most two full chunks per CU
 //         with p >= 256 (p = 1152, m = 2^16, b = 1: 0.113 vs 0.165 ms;
@@ -831,7 +843,9 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
       whole_call && lane_bytes == 16 &&
       dpar::wide_lds_bytes(lane_bytes, ops.height + 1) <=
           (size_t)st.lds_limit - dpar::kStaticLdsReserve;
-  bool want_wide = wide_fits && p <= kWideMaxRanks &&
+  const bool seq_capped =
+      ex == dpar::Exec::SPLIT && seq_wg_capped(p, all_items, st);
+  bool want_wide = wide_fits && !seq_capped &&
                    (s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk >= cus;
   if (forced) want_wide = !std::strcmp(u, "wide") && wide_fits;
   if (want_wide) uc.unit = dpar::Unit::WIDE;
@@ -1239,10 +1253,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   const char* cap_env = std::getenv("DPAR_SEQ_WG_PER_CU");
   const bool cap_forced = cap_env && *cap_env;
   if (up == dpar::Exec::SPLIT && unit == dpar::Unit::SEQ &&
-      (cap_forced ||
-       (p >= kCapMinRanks &&
-        grouped_units(s, prm.grp) >=
-            (uint64_t)kCapMinItemsPerCu * (uint64_t)st->num_cus))) {
+      (cap_forced || seq_wg_capped(p, grouped_units(s, prm.grp), *st))) {
     const int per_cu = env_int("DPAR_SEQ_WG_PER_CU", kSeqWgPerCu);
     if (per_cu > 0)
       lds_floor = (size_t)st->lds_per_cu / (size_t)(per_cu + 1) + 1024;

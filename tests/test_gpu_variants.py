@@ -431,30 +431,73 @@ def test_wide_unit_other_operators(dtype, op, dist):
         assert_all_ranks_equal(out, want, f"wide {dtype}/{exec}")
 
 
-@pytest.mark.parametrize("p,m,dtype,unit", [
-    (36, 1 << 20, "int32", "wide"),            # 256 wide items
-    (36, (1 << 20) + 3, "int32", "wide"),      # and 3 trailing elements
-    (36, 4 * (255 * 1024), "int32", "postorder"),  # 255: fewer than CUs
-    (128, 1 << 20, "int32", "wide"),
-    (129, 1 << 20, "int32", "postorder"),      # beyond the rank limit
-    (64, 1 << 18, "u32mat2x2", "wide"),        # the 64-rank matrix product
+@pytest.mark.parametrize("p,m,b,dtype,unit", [
+    (36, 1 << 20, 0, "int32", "wide"),            # 256 wide items
+    (36, (1 << 20) + 3, 0, "int32", "wide"),      # and 3 trailing elements
+    (36, 4 * (255 * 1024), 0, "int32", "postorder"),  # 255: fewer than CUs
+    (128, 1 << 20, 0, "int32", "wide"),
+    (300, 1 << 20, 0, "int32", "wide"),
+    (64, 1 << 18, 0, "u32mat2x2", "wide"),        # the 64-rank matrix product
 ])
-def test_wide_unit_choice(p, m, dtype, unit, capfd):
-    """The library's own choice (split executor, the rule's b): wide items
-    for few ranks and at least one wide item per CU (256 CUs), post-order
-    items otherwise (shown by DPAR_LOG), bit-exact against the oracle."""
+def test_wide_unit_choice(p, m, b, dtype, unit, capfd):
+    """The library's own choice (split executor): wide items where their
+    slots fit in LDS, at least one wide item per CU (256 CUs) and no
+    residency cap for post-order items; post-order items otherwise (shown
+    by DPAR_LOG); bit-exact against the oracle."""
     from tests._gpu import _Env
     need_gpu()
     if dtype == "u32mat2x2":
         x = _input("uniform_u32_mat", 2202, p, m)
         op = "matmul"
-        want = oracle.allreduce_ltr(x, dtype, op)
     else:
         x = _input("uniform_int", 2203, p, m, lo=-1000, hi=1000)
         op = "sum"
-        want = oracle.allreduce_ltr(x, dtype, op)
+    want = oracle.allreduce_ltr(x, dtype, op)
     with env_unit(None), _Env("DPAR_LOG", 1):
-        out = from_dev(_run(x, dtype, op, 0, "dual", "auto"), x)
+        out = from_dev(_run(x, dtype, op, b, "dual", "auto"), x)
     err = capfd.readouterr().err
     assert f"unit={unit} " in err, err[-400:]
-    assert_all_ranks_equal(out, want, f"choice p={p} m={m}")
+    assert_all_ranks_equal(out, want, f"choice p={p} m={m} b={b}")
+
+
+def test_wide_unit_needs_its_slots_in_lds(capfd):
+    """p = 1024: the four wavefronts' depth slots (10 per wavefront, 16 KB
+    each) exceed the LDS a workgroup may use, so a forced wide item falls
+    back to the post-order item, bit-exact."""
+    from tests._gpu import _Env
+    need_gpu()
+    x = _input("normal_f32", 2205, 1024, 8192)
+    want = _want(x, "float32", "sum", "dual")
+    for exec in ("split", "auto"):
+        with env_unit("wide"), _Env("DPAR_LOG", 1):
+            out = from_dev(_run(x, "float32", "sum", 1, "dual", exec), x)
+        err = capfd.readouterr().err
+        assert "unit=wide " not in err, err[-400:]
+        assert_all_ranks_equal(out, want, f"p=1024 wide fallback {exec}")
+
+
+def test_wide_unit_not_under_the_residency_cap(capfd):
+    """p = 256, m = 2^22 int32 (rows of 16 MB), the rule's b = 5793: the
+    split up-phase has 17379 post-order items, more than 64 per CU, and
+    runs them under its residency cap rather than taking wide items (shown
+    by DPAR_LOG).  Every output row equals row 0 (checked on the device),
+    row 0 equals the oracle."""
+    from tests._gpu import _Env
+    need_gpu()
+    p, m = 256, 1 << 22
+    x = _input("uniform_int", 2206, p, m, lo=-1000, hi=1000)
+    want = oracle.allreduce_ltr(x, "int32", "sum")
+    xd = to_dev(x)
+    del x
+    y = torch.empty_like(xd)
+    y.view(torch.int32).fill_(POISON)
+    dpar = lib()
+    st = torch.cuda.current_stream()
+    with env_unit(None), _Env("DPAR_LOG", 1):
+        dpar.dpar_allreduce_opt(dpar.rows(xd), dpar.rows(y), p, m, "int32",
+                                "sum", 0, "dual", "auto", 0, -1, st)
+        dpar.dpar_check_status(st)
+    err = capfd.readouterr().err
+    assert "unit=postorder " in err, err[-400:]
+    assert bool((y == y[0:1]).all().item()), "rows differ"
+    np.testing.assert_array_equal(y[0].cpu().numpy(), want)
