@@ -431,19 +431,26 @@ def test_wide_unit_other_operators(dtype, op, dist):
         assert_all_ranks_equal(out, want, f"wide {dtype}/{exec}")
 
 
-@pytest.mark.parametrize("p,m,b,dtype,unit", [
-    (36, 1 << 20, 0, "int32", "wide"),            # 256 wide items
-    (36, (1 << 20) + 3, 0, "int32", "wide"),      # and 3 trailing elements
-    (36, 4 * (255 * 1024), 0, "int32", "postorder"),  # 255: fewer than CUs
-    (128, 1 << 20, 0, "int32", "wide"),
-    (300, 1 << 20, 0, "int32", "wide"),
-    (64, 1 << 18, 0, "u32mat2x2", "wide"),        # the 64-rank matrix product
+F, S = "one_launch_fused", "split"
+
+
+@pytest.mark.parametrize("p,m,b,dtype,unit,ex", [
+    (36, 1 << 20, 0, "int32", "wide", F),         # 256 wide items
+    (36, (1 << 20) + 3, 0, "int32", "wide", F),   # and 3 trailing elements
+    (36, 1 << 21, 0, "int32", "wide", S),         # two items per CU
+    (36, 4 * (255 * 1024), 0, "int32", "postorder", S),  # fewer than CUs
+    (56, 1 << 20, 0, "int32", "wide", F),
+    (57, 1 << 20, 0, "int32", "wide", S),
+    (128, 1 << 20, 0, "int32", "wide", S),
+    (300, 1 << 20, 0, "int32", "wide", S),
+    (64, 1 << 18, 0, "u32mat2x2", "wide", S),     # the 64-rank matrix product
 ])
-def test_wide_unit_choice(p, m, b, dtype, unit, capfd):
-    """The library's own choice (split executor): wide items where their
-    slots fit in LDS, at least one wide item per CU (256 CUs) and no
-    residency cap for post-order items; post-order items otherwise (shown
-    by DPAR_LOG); bit-exact against the oracle."""
+def test_wide_unit_choice(p, m, b, dtype, unit, ex, capfd):
+    """The library's own choice under AUTO (256 CUs): wide items where their
+    slots fit in LDS, at least one wide item per CU and no residency cap
+    for post-order items, post-order items otherwise; wide items of at most
+    56 ranks and one item per CU in one fused launch, else split (shown by
+    DPAR_LOG); bit-exact against the oracle."""
     from tests._gpu import _Env
     need_gpu()
     if dtype == "u32mat2x2":
@@ -457,6 +464,7 @@ def test_wide_unit_choice(p, m, b, dtype, unit, capfd):
         out = from_dev(_run(x, dtype, op, b, "dual", "auto"), x)
     err = capfd.readouterr().err
     assert f"unit={unit} " in err, err[-400:]
+    assert f"exec={ex} " in err, err[-400:]
     assert_all_ranks_equal(out, want, f"choice p={p} m={m} b={b}")
 
 
