@@ -54,7 +54,7 @@ constexpr int kCapMinItemsPerCu = 64;
 constexpr int kSubDeepMinRanks = 1024;
 // AUTO: a call of wide work items with at most this many ranks and at most
 // one item per CU runs as one fused launch.
-constexpr int kWideFuseMaxRanks = 56;
+constexpr int kWideFuseMaxRanks = 48;
 // Level work item: loads in flight at once (1024 threads, 8 loads each).
 constexpr uint64_t kLvLoadsInFlight = 1024 * 8;
 // Ticket executor: rank loads per claimed batch of work items.
@@ -1176,10 +1176,11 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // their rows together and then write y together, so one fused launch
   // keeps reads and writes apart in time and saves the broadcast pass; the
   // p writes per item then cost less than that pass as long as p is small.
-  // Measured, int32 SUM, m = 2^20 (256 items), cold caches, split -> fused:
-  // p = 8 24.5 -> 18.2 us, p = 36 58.4 -> 56.2 us, p = 56 80.6 -> 80.4 us,
-  // p = 64 89.3 -> 91.7 us; with two items per CU (p = 36, m = 2^21)
-  // 103 -> 109 us.
+  // Measured, int32 SUM, m = 2^20 (256 items), cold caches, split -> fused
+  // (best of 3 runs): p = 8 24.5 -> 18.2 us, p = 24 43.1 -> 37.8 us,
+  // p = 36 57.8 -> 56.5 us, p = 48 70.9 -> 69.5 us, p = 56 80.2 -> 80.3 us,
+  // p = 64 89.3 -> 91.7 us (on another box p = 36 went the other way by
+  // 2-3%); with two items per CU (p = 36, m = 2^21) 103 -> 109 us.
   if (exec == DPAR_EXEC_AUTO && ex == dpar::Exec::SPLIT &&
       uc.unit == dpar::Unit::WIDE && p <= kWideFuseMaxRanks &&
       (s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk <=
