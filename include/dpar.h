@@ -97,10 +97,11 @@ typedef enum {
  *                     directions avoids read/write turnarounds.
  *   AUTO              SPLIT; one launch of every work item in round order
  *                     with the fused write-out instead for calls moving at
- *                     most 40 MB (2 p m times the element size), and for
- *                     calls that run in subtree work items (p >= 256 and at
- *                     most two such items per CU, at least one per two
- *                     CUs).
+ *                     most 40 MB (2 p m times the element size), for calls
+ *                     that run in subtree work items (p >= 256 and at most
+ *                     two such items per CU, at least one per two CUs), and
+ *                     for calls that run in wide work items with p <= 48
+ *                     and at most one such item (16 KB of columns) per CU.
  * The last two run the algorithm's whole round structure, down-phase
  * included (dpar_schedule_rounds gives the number of rounds R):
  *   ROUNDS            one launch per round r = 0 .. R-1.  Round r runs the
