@@ -509,3 +509,37 @@ def test_wide_unit_not_under_the_residency_cap(capfd):
     assert "unit=postorder " in err, err[-400:]
     assert bool((y == y[0:1]).all().item()), "rows differ"
     np.testing.assert_array_equal(y[0].cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("exec", ["auto", "split", "ticket"])
+def test_wide_unit_on_misaligned_rows(exec, capfd):
+    """The library's own choice on rows 4 bytes past a 16-byte boundary, one
+    row per separate allocation (16-byte lanes at 4-byte aligned addresses;
+    the broadcast then shifts each output row to its own 4 KB boundary):
+    p = 40, m = 2^20 + 5 (5 trailing elements), wide items, bit-exact."""
+    from tests._gpu import _Env
+    need_gpu()
+    dpar = lib()
+    p, m = 40, (1 << 20) + 5
+    x = _input("normal_f32", 2207, p, m)
+    want = _want(x, "float32", "sum", "dual")
+    xb = [torch.empty(m + 8, dtype=torch.float32, device="cuda")
+          for _ in range(p)]
+    yb = [torch.full((m + 8,), float("nan"), dtype=torch.float32,
+                     device="cuda") for _ in range(p)]
+    for i in range(p):
+        xb[i][1:1 + m] = torch.from_numpy(np.ascontiguousarray(x[i])).cuda()
+    xs = [t.data_ptr() + 4 for t in xb]
+    ys = [t.data_ptr() + 4 for t in yb]
+    s = torch.cuda.current_stream()
+    with env_unit(None), _Env("DPAR_LOG", 1):
+        dpar.dpar_allreduce_opt(xs, ys, p, m, "float32", "sum", 0, "dual",
+                                exec, 0, -1, s)
+        dpar.dpar_check_status(s)
+    err = capfd.readouterr().err
+    assert "unit=wide " in err, err[-400:]
+    got = np.stack([t[1:1 + m].cpu().numpy() for t in yb])
+    assert_all_ranks_equal(got, want, f"wide misaligned {exec}")
+    for t in yb:  # nothing written outside the m elements
+        assert bool(torch.isnan(t[0]).item())
+        assert bool(torch.isnan(t[1 + m:]).all().item())

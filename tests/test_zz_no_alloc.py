@@ -84,6 +84,8 @@ def test_same_pointers_new_contents():
     (64, 4096, "u32mat2x2", "matmul"),
     (300, 20000, "float32", "sum"),
     (2304, 1 << 12, "int32", "max"),
+    (36, 1 << 20, "int32", "sum"),          # wide items, one fused launch
+    (64, 1 << 18, "u32mat2x2", "matmul"),   # wide items, split
 ])
 def test_sizes_and_types(p, m, dtype, op):
     need_gpu()
