@@ -20,6 +20,18 @@ pytestmark = pytest.mark.gpu
                                    (300, 4096, 3)])
 def test_captured_call_replays(alg, exec, p, m, b):
     need_gpu()
+    _replays(alg, exec, p, m, b)
+
+
+@pytest.mark.parametrize("exec", ["auto", "split", "ticket"])
+def test_captured_wide_items_replay(exec):
+    """p = 36, m = 2^20, the rule's b: wide work items (one fused launch
+    under AUTO, split, ticket) recorded into a graph and replayed."""
+    need_gpu()
+    _replays("dual", exec, 36, 1 << 20, 0)
+
+
+def _replays(alg, exec, p, m, b):
     dpar = lib()
     trees = oracle.build_trees(p) if alg == "dual" else \
         oracle.build_trees(p, layout="single")
