@@ -101,7 +101,8 @@ typedef enum {
  *                     that run in subtree work items (p >= 256 and at most
  *                     two such items per CU, at least one per two CUs), and
  *                     for calls that run in wide work items with p <= 48
- *                     and at most one such item (16 KB of columns) per CU.
+ *                     and at most one such item (16 KB of columns) per CU,
+ *                     or with p <= 8.
  * The last two run the algorithm's whole round structure, down-phase
  * included (dpar_schedule_rounds gives the number of rounds R):
  *   ROUNDS            one launch per round r = 0 .. R-1.  Round r runs the

@@ -52,9 +52,11 @@ constexpr int kCapMinRanks = 256;
 constexpr int kCapMinItemsPerCu = 64;
 // Subtree work items: the deep load pipeline from this many ranks on.
 constexpr int kSubDeepMinRanks = 1024;
-// AUTO: a call of wide work items with at most this many ranks and at most
-// one item per CU runs as one fused launch.
+// AUTO: a call of wide work items with at most kWideFuseMaxRanks ranks and
+// at most one item per CU, or with at most kWideFuseAnyRanks ranks, runs as
+// one fused launch.
 constexpr int kWideFuseMaxRanks = 48;
+constexpr int kWideFuseAnyRanks = 8;
 // Level work item: loads in flight at once (1024 threads, 8 loads each).
 constexpr uint64_t kLvLoadsInFlight = 1024 * 8;
 // Ticket executor: rank loads per claimed batch of work items.
@@ -1180,11 +1182,18 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // (best of 3 runs): p = 8 24.5 -> 18.2 us, p = 24 43.1 -> 37.8 us,
   // p = 36 57.8 -> 56.5 us, p = 48 70.9 -> 69.5 us, p = 56 80.2 -> 80.3 us,
   // p = 64 89.3 -> 91.7 us (on another box p = 36 went the other way by
-  // 2-3%); with two items per CU (p = 36, m = 2^21) 103 -> 109 us.
+  // 2-3%); with two items per CU (p = 36, m = 2^21) 103 -> 109 us.  With
+  // very few ranks the split executor's extra traffic (y_0 written, then
+  // read back: 1/p of the call's bytes) outweighs the interleaving at any
+  // size: p = 2, m = 2^22 (1024 items) 35.6 -> 17.6 us; p = 8, 1024 / 2048
+  // / 4096 items 59.4 -> 51.6, 106.8 -> 102.0, 204.5 -> 202.3 us; p = 12
+  // within 3% either way, p = 16 7-18% slower fused.
   if (exec == DPAR_EXEC_AUTO && ex == dpar::Exec::SPLIT &&
-      uc.unit == dpar::Unit::WIDE && p <= kWideFuseMaxRanks &&
-      (s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk <=
-          (uint64_t)st->num_cus)
+      uc.unit == dpar::Unit::WIDE &&
+      (p <= kWideFuseAnyRanks ||
+       (p <= kWideFuseMaxRanks &&
+        (s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk <=
+            (uint64_t)st->num_cus)))
     ex = dpar::Exec::DISPATCH;
   const dpar::Unit unit = uc.unit;
   prm.nlev = ops->height + 1;

@@ -31,6 +31,7 @@
 #include <cstdint>
 #include <cstring>
 #include <map>
+#include <type_traits>
 #include <utility>
 
 #include "kernels.hpp"
@@ -673,8 +674,8 @@ __device__ __forceinline__ void run_unit_wide(const WideArgs& a, uint64_t t,
   // Rotating pipeline of KF visits: buffer slot k % KF holds visit k and
   // is refilled with visit k + KF once its step is done.  The row
   // addresses and opcodes come from the tables a group of G visits ahead
-  // (scalar loads issued a group before they are needed); ranks past p
-  // re-read row p - 1 and are not processed (the opcode table is padded).
+  // (scalar loads issued a group before they are needed; entries past p
+  // name row p - 1, the opcode table is padded).
   constexpr int G = 8;
   static_assert(G % KF == 0 && KF <= G, "groups hold whole pipelines");
   // (ranks past p read row p - 1 through a clamped index: a table load
@@ -694,7 +695,12 @@ __device__ __forceinline__ void run_unit_wide(const WideArgs& a, uint64_t t,
     for (int u = 0; u < QW; ++u) buf[k][u] = L::load(row_cur[k], off[u]);
     __builtin_amdgcn_sched_barrier(0);
   }
-  for (int gb = 0; gb < p; gb += G) {
+  // One group of G visits from gb.  STEP: a visit may lie past the last
+  // rank (then it is not processed); LOAD: a refill may (then it is not
+  // issued).  Groups that need neither run without a per-visit branch.
+  auto group = [&](int gb, auto step_c, auto load_c) {
+    constexpr bool STEP = decltype(step_c)::value;
+    constexpr bool LOAD = decltype(load_c)::value;
     uint64_t row_nxt[G];
     uint32_t op_nxt[G];
 #pragma unroll
@@ -707,9 +713,11 @@ __device__ __forceinline__ void run_unit_wide(const WideArgs& a, uint64_t t,
       const uint64_t nrow = k + KF < G ? row_cur[k + KF] : row_nxt[k + KF - G];
       // consumed before refilled: at most KF visits in flight (measured
       // 0-2% faster than refilling first, with one visit more in flight)
-      if (gb + k < p) step(buf[k % KF], op_cur[k]);
+      if (!STEP || gb + k < p) step(buf[k % KF], op_cur[k]);
+      if (!LOAD || gb + k + KF < p) {
 #pragma unroll
-      for (int u = 0; u < QW; ++u) buf[k % KF][u] = L::load(nrow, off[u]);
+        for (int u = 0; u < QW; ++u) buf[k % KF][u] = L::load(nrow, off[u]);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
@@ -717,6 +725,24 @@ __device__ __forceinline__ void run_unit_wide(const WideArgs& a, uint64_t t,
       row_cur[k] = row_nxt[k];
       op_cur[k] = op_nxt[k];
     }
+  };
+  using yes = std::true_type;
+  using no = std::false_type;
+  int gb = 0;
+  if constexpr (FUSED) {
+    // The write-out follows the walk at once: loads issued past the last
+    // rank would hold it up (they still count in the wavefront's memory
+    // counter), and with few ranks outnumber the real ones (p = 2,
+    // m = 2^22, one fused launch: 25.8 -> 17.3 us; p = 36, m = 2^20:
+    // 56.6 -> 54.4 us).  So the full groups run branch-free and only the
+    // last visits test for the end.
+    for (; gb + G + KF <= p; gb += G) group(gb, no{}, no{});
+    for (; gb < p; gb += G) group(gb, yes{}, yes{});
+  } else {
+    // Split up-phase: the last group re-reads row p - 1 for the visits past
+    // the end (cache hits) rather than branch around those loads, whose
+    // waits at the branches cost more there (p = 64 and 128: 1.5-2.3%).
+    for (; gb < p; gb += G) group(gb, yes{}, no{});
   }
 
   // dual-root combine: tree A's root waits in slot 0, tree B's is cur

@@ -438,6 +438,8 @@ F, S = "one_launch_fused", "split"
     (36, 1 << 20, 0, "int32", "wide", F),         # 256 wide items
     (36, (1 << 20) + 3, 0, "int32", "wide", F),   # and 3 trailing elements
     (36, 1 << 21, 0, "int32", "wide", S),         # two items per CU
+    (8, 1 << 22, 0, "int32", "wide", F),          # four per CU, 8 ranks
+    (9, 1 << 22, 0, "int32", "wide", S),
     (36, 4 * (255 * 1024), 0, "int32", "postorder", S),  # fewer than CUs
     (48, 1 << 20, 0, "int32", "wide", F),
     (49, 1 << 20, 0, "int32", "wide", S),
@@ -449,8 +451,9 @@ def test_wide_unit_choice(p, m, b, dtype, unit, ex, capfd):
     """The library's own choice under AUTO (256 CUs): wide items where their
     slots fit in LDS, at least one wide item per CU and no residency cap
     for post-order items, post-order items otherwise; wide items of at most
-    48 ranks and one item per CU in one fused launch, else split (shown by
-    DPAR_LOG); bit-exact against the oracle."""
+    48 ranks and one item per CU, or of at most 8 ranks, in one fused
+    launch, else split (shown by DPAR_LOG); bit-exact against the
+    oracle."""
     from tests._gpu import _Env
     need_gpu()
     if dtype == "u32mat2x2":
