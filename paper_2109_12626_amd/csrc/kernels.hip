@@ -205,9 +205,11 @@ static_assert(16 <= kTablePad, "the wide walk reads two groups of 8 ahead");
 // pipeline of kU: slot k of `buf` holds rank base + k; it is consumed and at
 // once refilled with rank base + kU + k.  The tables are padded by kU
 // entries, so reading kU entries ahead stays inside them; ranks past r1
-// re-read row r1 - 1 (cache hits) and are not processed.  Returns the value
-// of the last rank walked.
-template <class L, int KU = kU>
+// re-read row r1 - 1 (cache hits) and are not processed.  TAIL (fused work
+// items, whose write-out follows at once): no load is issued for a rank
+// past r1; the full rounds of KU ranks run branch-free and only the last
+// ones test for the end.  Returns the value of the last rank walked.
+template <class L, int KU = kU, bool TAIL = false>
 __device__ __forceinline__ typename L::T walk(const uint64_t* __restrict__ xp,
                                               const uint32_t* __restrict__ ops,
                                               int r0, int r1,
@@ -229,6 +231,49 @@ __device__ __forceinline__ typename L::T walk(const uint64_t* __restrict__ xp,
   };
   const uint64_t last_row = xp[r1 - 1] + unit_off;
   T buf[KU];
+  if constexpr (TAIL) {
+#pragma unroll
+    for (int k = 0; k < KU; ++k) {
+      buf[k] = T{};
+      if (r0 + k < r1) buf[k] = L::load(xp[r0 + k] + unit_off, lane_off);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    int rb = r0;
+    // full rounds: every rank consumed and every refill a rank below r1
+    for (; rb + 2 * KU <= r1; rb += KU) {
+      uint64_t next_row[KU];
+      uint32_t op[KU];
+#pragma unroll
+      for (int k = 0; k < KU; ++k) {
+        next_row[k] = xp[rb + KU + k] + unit_off;
+        op[k] = ops[rb + k];
+      }
+#pragma unroll
+      for (int k = 0; k < KU; ++k) {
+        const T v = buf[k];
+        buf[k] = L::load(next_row[k], lane_off);
+        __builtin_amdgcn_sched_barrier(0);
+        step(v, op[k]);
+      }
+    }
+    for (; rb < r1; rb += KU) {
+      uint64_t next_row[KU];
+      uint32_t op[KU];
+#pragma unroll
+      for (int k = 0; k < KU; ++k) {
+        next_row[k] = xp[rb + KU + k] + unit_off;
+        op[k] = ops[rb + k];
+      }
+#pragma unroll
+      for (int k = 0; k < KU; ++k) {
+        const T v = buf[k];
+        if (rb + KU + k < r1) buf[k] = L::load(next_row[k], lane_off);
+        __builtin_amdgcn_sched_barrier(0);
+        if (rb + k < r1) step(v, op[k]);
+      }
+    }
+    return last;
+  }
 #pragma unroll
   for (int k = 0; k < KU; ++k) {
     const uint64_t row = xp[r0 + k] + unit_off;
@@ -293,7 +338,7 @@ __device__ __forceinline__ void run_unit(const uint64_t* __restrict__ xp,
   T* my = slots + (size_t)wave * prm.nslots * 64 + lane;
 
   T cur = T{};
-  walk<L>(xp, ops, r0, r1, unit_off, lane_off, my, 0, cur);
+  walk<L, kU, FUSED>(xp, ops, r0, r1, unit_off, lane_off, my, 0, cur);
 
   // Dual-root exchange.
   T y;
@@ -517,7 +562,8 @@ __device__ __forceinline__ void run_unit_sub(const uint64_t* __restrict__ xp,
     const int base = (int)parts[3 * wave + 2];
     T cur = T{};
     pval[(size_t)wave * 64 + lane] =
-        walk<L, KU>(xp, ops, lo, hi + 1, unit_off, lane_off, my, base, cur);
+        walk<L, KU, FUSED>(xp, ops, lo, hi + 1, unit_off, lane_off, my, base,
+                           cur);
   }
   if (wave < 2) {
 #pragma unroll
