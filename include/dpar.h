@@ -330,6 +330,13 @@ const char* dpar_last_error(void);
  *                           calls with at least one 16 KB column chunk per
  *                           CU unless the split up-phase caps its
  *                           post-order items' residency)
+ *   DPAR_WIDE_TAIL=0|1      wide work items: the columns past the last
+ *                           whole round of one item per CU in tail items
+ *                           (one quantum per lane, shorter chains) unless
+ *                           they fill more than 7/8 of a round (default 1;
+ *                           0: full items only)
+ *   DPAR_WIDE_ROUND=n       wide work items per round for that cut
+ *                           (default: the CU count; tests)
  *   DPAR_LEVEL_LOG2T=k      level work items of 2^k quanta (at most what
  *                           fits in LDS)
  *   DPAR_SUB_DEEP=0|1       subtree work items with 8 or 16 loads in flight

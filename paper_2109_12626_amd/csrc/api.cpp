@@ -715,6 +715,31 @@ bool seq_wg_capped(int p, uint64_t items, const DeviceState& st) {
          items >= (uint64_t)kCapMinItemsPerCu * (uint64_t)st.num_cus;
 }
 
+// Full wide items of a call of n wide chunks.  A wide item holds its CU for
+// a chain of p / kWideKF dependent visits, so a last round of one item per
+// CU with only a few items left leaves most CUs idle for about as long as
+// a full round (int32 SUM, split, p = 288, up-phase: 256 items 178 us,
+// 264 items 308 us, 519 items 483 us), and where two fit per CU by LDS
+// (p <= 48) the CUs that get two finish late (p = 36: 256 items 60.3 us
+// per call, 264 items 67.6 us).  The columns past the last whole round of
+// one item per CU go instead to tail items with one quantum per lane and
+// 8 visits in flight (p = 288: 211 and 387 us; p = 128, 264 items:
+// 140 -> 97 us; p = 36, 264 items: 62.0 us per call), unless they fill
+// more than 7/8 of a round, where the full items are as fast or faster
+// (p = 288, 504 items: 353 us full, 363 us with tail items; p = 36:
+// 102.0 vs 102.4 us per call; with 448 items tail items are faster: p = 128
+// 152 -> 142 us, p = 36 94.5 -> 92.4 us per call).  DPAR_WIDE_TAIL=0: no
+// tail items; DPAR_WIDE_ROUND: items per round (default: the CU count;
+// tests: tail items on small calls).
+uint64_t wide_full_items(uint64_t n, const DeviceState& st) {
+  const uint64_t round = (uint64_t)std::max(
+      1, env_int("DPAR_WIDE_ROUND", st.num_cus));
+  const uint64_t r = n % round;
+  if (env_int("DPAR_WIDE_TAIL", 1) == 0 || n <= round || 8 * r > 7 * round)
+    return n;
+  return n - r;
+}
+
 struct UnitChoice {
   dpar::Unit unit = dpar::Unit::SEQ;
   int lv_log2t = 0;  // LEVEL: log2 of the chunk capacity in quanta
@@ -902,6 +927,8 @@ void log_plan(int p, size_t m, dpar_dtype_t dtype, dpar_op_t op,
     std::fprintf(stderr, " level_chunk_quanta=%d", 1 << prm.lv_log2t);
   if (unit == dpar::Unit::SUB)
     std::fprintf(stderr, " sub_deep=%d", prm.sub_deep);
+  if (unit == dpar::Unit::WIDE)
+    std::fprintf(stderr, " full_items=%u", prm.wide_full);
   if (ex == dpar::Exec::TICKET) std::fprintf(stderr, " batch=%u", prm.batch);
   std::fprintf(stderr, "\n");
 }
@@ -1245,9 +1272,14 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     prm.b = 1;
     prm.NL = s1.NL;
     prm.lq = (uint32_t)s1.lq;
-    prm.C = (int)((s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk);
     prm.grp = 1;
     prm.batch = 1;
+    const uint64_t n = (s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk;
+    const uint64_t full = wide_full_items(n, *st);
+    prm.wide_full = (uint32_t)full;
+    prm.C = (int)(full + (s.Q - std::min(s.Q, full * dpar::kWideChunk) +
+                          dpar::kWideTailChunk - 1) /
+                             dpar::kWideTailChunk);
   }
   // round-structured down-step: two ranks per wavefront per work item, the
   // largest block in pieces of kDownPiece quanta

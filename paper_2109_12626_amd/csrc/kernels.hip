@@ -194,7 +194,6 @@ static_assert(2 * kU <= kTablePad, "tables are padded for 2 * kU reads");
 // per wavefront, for calls whose items all run at once, one per CU.
 constexpr int kUDeep = 16;
 static_assert(2 * kUDeep <= kTablePad, "tables are padded for 2 * kU reads");
-static_assert(16 <= kTablePad, "the wide walk reads two groups of 8 ahead");
 
 // Up-step of one chunk over the ranks [r0, r1) in post-order (Algorithm 1's
 // "Y <- t (.) Y" with the first child's block, then with the second
@@ -635,9 +634,15 @@ __device__ __forceinline__ void run_unit_sub(const uint64_t* __restrict__ xp,
 // 5.5 TB/s with 1 KB per visit and 8 visits in flight; 6.5 TB/s with
 // 4 KB per visit and 2 in flight, as fast as contiguous 16 KB tiles).
 //
-// LDS: per wavefront nslots depth slots of kWideQ x 64 lanes, slot d's
-// piece u at [(d kWideQ + u) 64 + lane] (one 16-byte access per lane,
-// conflict-free).
+// A wide item holds its CU for a chain of p / kWideKF dependent visits,
+// long next to its share of the bandwidth once fewer items than CUs are
+// left; so the columns past the call's last whole round of full items (one
+// item per resident workgroup) go to tail items of kWideTailQ quanta per
+// lane with kWideTailKF visits in flight, whose chains are shorter.
+//
+// LDS: per wavefront nslots depth slots of QW x 64 lanes, slot d's piece u
+// at [(d QW + u) 64 + lane] (one 16-byte access per lane, conflict-free);
+// a tail item uses the first part of the full item's allocation.
 
 // The scalars a wide work item reads: 64 bytes, loaded together at the
 // start of its kernel.
@@ -652,7 +657,7 @@ struct WideArgs {
   int out0;
   int out1;
   int dual;
-  int unused;
+  uint32_t nfull;  // items [0, nfull) are full, later ones tail items
 };
 
 __host__ __device__ inline WideArgs wide_args(const uint64_t* xp,
@@ -661,24 +666,23 @@ __host__ __device__ inline WideArgs wide_args(const uint64_t* xp,
                                               const Params& prm) {
   return WideArgs{xp,       yp,          ops,       prm.Q,    prm.qbase,
                   prm.p,    prm.nslots,  prm.out0,  prm.out1, prm.dual,
-                  0};
+                  prm.wide_full};
 }
 
-template <class L, bool FUSED>
-__device__ __forceinline__ void run_unit_wide(const WideArgs& a, uint64_t t,
+// One wide or tail work item whose columns start at quantum q0 of the
+// call, QW quanta per lane, KF visits in flight per wavefront.
+template <class L, bool FUSED, int QW, int KF>
+__device__ __forceinline__ void run_unit_wide(const WideArgs& a, uint64_t q0,
                                               typename L::T* slots) {
   using T = typename L::T;
   const uint64_t* __restrict__ xp = a.xp;
   const uint64_t* __restrict__ yp = a.yp;
   const uint32_t* __restrict__ ops = a.ops;
-  constexpr int QW = kWideQ, KF = kWideKF;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 
-  // Work item t: quanta [t kWideChunk, (t + 1) kWideChunk) of the call's
-  // Q (the host cuts the columns into whole wide chunks, whatever the
-  // blocks); this wavefront's share [ws, we).
-  const uint64_t ws = min(t * kWideChunk + (uint64_t)wave * 64 * QW, a.Q);
+  // this wavefront's share [ws, we) of the item's 64 QW kWideWaves quanta
+  const uint64_t ws = min(q0 + (uint64_t)wave * 64 * QW, a.Q);
   const uint64_t we = min(ws + 64 * QW, a.Q);
   const uint32_t count = (uint32_t)(we - ws);
   // wave-uniform; the unit has no workgroup barrier, so a wavefront without
@@ -722,8 +726,9 @@ __device__ __forceinline__ void run_unit_wide(const WideArgs& a, uint64_t t,
   // addresses and opcodes come from the tables a group of G visits ahead
   // (scalar loads issued a group before they are needed; entries past p
   // name row p - 1, the opcode table is padded).
-  constexpr int G = 8;
+  constexpr int G = KF > 8 ? KF : 8;
   static_assert(G % KF == 0 && KF <= G, "groups hold whole pipelines");
+  static_assert(2 * G <= kTablePad, "the walk reads two groups ahead");
   // (ranks past p read row p - 1 through a clamped index: a table load
   // under a condition would become a branch around a scalar load that waits
   // for it)
@@ -820,6 +825,20 @@ __device__ __forceinline__ void run_unit_wide(const WideArgs& a, uint64_t t,
   }
 }
 
+// Work item t of a wide call: full items first (kWideChunk quanta each,
+// from the call's first column), then tail items (kWideTailChunk each); the
+// host cuts the columns this way whatever the blocks.
+template <class L, bool FUSED>
+__device__ __forceinline__ void run_wide_item(const WideArgs& a, uint64_t t,
+                                              typename L::T* slots) {
+  if (t < (uint64_t)a.nfull)
+    run_unit_wide<L, FUSED, kWideQ, kWideKF>(a, t * kWideChunk, slots);
+  else
+    run_unit_wide<L, FUSED, kWideTailQ, kWideTailKF>(
+        a, (uint64_t)a.nfull * kWideChunk + (t - a.nfull) * kWideTailChunk,
+        slots);
+}
+
 // ------------------------------------------------------------ unit policies
 
 template <class L, int W, bool FUSED>
@@ -884,7 +903,7 @@ struct WideUnit {
                              const uint32_t* __restrict__ lvl,
                              const Params& prm, uint64_t t, char* lds) {
     (void)lvl;
-    run_unit_wide<L, FUSED>(wide_args(xp, yp, ops, prm), t,
+    run_wide_item<L, FUSED>(wide_args(xp, yp, ops, prm), t,
                             reinterpret_cast<typename L::T*>(lds));
   }
   static size_t lds(const Params& prm) {
@@ -915,7 +934,7 @@ template <class L, bool FUSED>
 __global__ __launch_bounds__(64 * kWideWaves) void k_wide(WideArgs a,
                                                          uint64_t first) {
   extern __shared__ char lds_raw[];
-  run_unit_wide<L, FUSED>(a, first + blockIdx.x,
+  run_wide_item<L, FUSED>(a, first + blockIdx.x,
                           reinterpret_cast<typename L::T*>(lds_raw));
 }
 

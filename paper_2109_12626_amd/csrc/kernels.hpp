@@ -82,6 +82,9 @@ struct Params {
   int sub_deep;         // SUB: the parts are walked with 16 loads in flight
                         // per wavefront instead of 8 (host-side choice of
                         // the kernel)
+  uint32_t wide_full;   // WIDE: items [0, wide_full) take kWideChunk quanta
+                        // each, later ones kWideTailChunk (the columns past
+                        // the full items)
 };
 
 // Quanta per down-step piece: 64 lanes x 4 quanta per lane.
@@ -143,6 +146,18 @@ constexpr int kWideWaves = DPAR_WIDE_WAVES;
 constexpr int kWideKF = DPAR_WIDE_KF;
 // Quanta of one WIDE work item.
 constexpr uint64_t kWideChunk = 64ull * kWideQ * kWideWaves;
+// Tail items of a WIDE call (the columns past its last whole round of
+// full items): the same walk with kWideTailQ quanta per lane and
+// kWideTailKF visits in flight per wavefront, kWideTailChunk quanta each.
+#ifndef DPAR_WIDE_TAIL_Q
+#define DPAR_WIDE_TAIL_Q 1
+#endif
+#ifndef DPAR_WIDE_TAIL_KF
+#define DPAR_WIDE_TAIL_KF 8
+#endif
+constexpr int kWideTailQ = DPAR_WIDE_TAIL_Q;
+constexpr int kWideTailKF = DPAR_WIDE_TAIL_KF;
+constexpr uint64_t kWideTailChunk = 64ull * kWideTailQ * kWideWaves;
 
 // Bytes of dynamic LDS a WIDE work item needs with `nslots` slots per
 // wavefront (lane_bytes 16).

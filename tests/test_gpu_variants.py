@@ -431,6 +431,76 @@ def test_wide_unit_other_operators(dtype, op, dist):
         assert_all_ranks_equal(out, want, f"wide {dtype}/{exec}")
 
 
+@pytest.mark.parametrize("exec", ["auto", "split", "ticket"])
+@pytest.mark.parametrize("p", [2, 37, 300])
+def test_wide_tail_items(exec, p, capfd):
+    """Columns past the last whole round of full wide items go to tail items
+    (one quantum per lane, 8 visits in flight).  Rounds forced to 4 items
+    (DPAR_WIDE_ROUND): m = 4 (5 * 1024 + 300) is 4 full items, then 1324
+    quanta in five whole tail items and a ragged sixth (44 quanta, part of
+    one wavefront).  Bit-exact fp32 for both trees and for one tree, every
+    rank's output."""
+    from tests._gpu import _Env
+    need_gpu()
+    m = 4 * (5 * 1024 + 300)
+    x = _input("normal_f32", 2207 + p, p, m)
+    for alg in ("dual", "single"):
+        want = _want(x, "float32", "sum", alg)
+        with env_unit("wide"), _Env("DPAR_LOG", 1), _Env("DPAR_WIDE_ROUND", 4):
+            out = from_dev(_run(x, "float32", "sum", 0, alg, exec), x)
+        err = capfd.readouterr().err
+        assert "unit=wide " in err and " full_items=4" in err, err[-400:]
+        assert " items=10" in err, err[-400:]
+        assert_all_ranks_equal(out, want, f"wide tail {alg}/{exec}/p={p}")
+
+
+@pytest.mark.parametrize("dtype,op,dist", [("int32", "max", "uniform_int"),
+                                           ("u32mat2x2", "matmul",
+                                            "uniform_u32_mat")])
+def test_wide_tail_items_other_operators(dtype, op, dist, capfd):
+    """Tail items keep the rank order of the matrix product: p = 45,
+    m = 5000 (5000 quanta of 16 bytes for the matrices) in rounds of 2
+    items: 4 full items, then 904 quanta in 4 tail items (three whole, one
+    of 136 quanta)."""
+    from tests._gpu import _Env
+    need_gpu()
+    kw = {"lo": -99, "hi": 99} if dist == "uniform_int" else {}
+    x = _input(dist, 2208, 45, 5000 if dtype == "u32mat2x2" else 20000, **kw)
+    want = oracle.allreduce_ltr(x, dtype, op)
+    for exec in ("auto", "split", "ticket"):
+        with env_unit("wide"), _Env("DPAR_LOG", 1), _Env("DPAR_WIDE_ROUND", 2):
+            out = from_dev(_run(x, dtype, op, 3, "dual", exec), x)
+        err = capfd.readouterr().err
+        assert " full_items=4" in err and " items=8" in err, err[-400:]
+        assert_all_ranks_equal(out, want, f"wide tail {dtype}/{exec}")
+
+
+@pytest.mark.parametrize("p,n,unit,full", [
+    (36, 264, "wide", 256),        # two fit per CU by LDS; rounds of 256
+    (36, 519, "wide", 512),        # a short tail after two rounds
+    (36, 504, "wide", 504),        # over 7/8 of a round: no tail items
+    (128, 264, "wide", 256),
+    (128, 448, "wide", 256),       # 3/4 of a round in tail items
+])
+def test_wide_tail_choice(p, n, unit, full, capfd):
+    """The library's own choice (256 CUs): int32 SUM with rows of n wide
+    chunks (16 KB each), split.  Full items in whole rounds of one per CU
+    and tail items past them unless those fill more than 7/8 of a round
+    (shown by DPAR_LOG); bit-exact against the oracle."""
+    from tests._gpu import _Env
+    need_gpu()
+    m = 4096 * n
+    x = _input("uniform_int", 2209, p, m, lo=-1000, hi=1000)
+    want = oracle.allreduce_ltr(x, "int32", "sum")
+    with env_unit(None), _Env("DPAR_LOG", 1):
+        out = from_dev(_run(x, "int32", "sum", 0, "dual", "auto"), x)
+    err = capfd.readouterr().err
+    assert f"unit={unit} " in err and "exec=split " in err, err[-400:]
+    if full is not None:
+        assert f" full_items={full}" in err, err[-400:]
+    assert_all_ranks_equal(out, want, f"tail choice p={p} n={n}")
+
+
 F, S = "one_launch_fused", "split"
 
 
