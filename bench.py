@@ -178,18 +178,22 @@ def table2():
     p, blk = 288, 16000
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
-    cmax = max(TABLE2_COUNTS)
     g = torch.Generator(device=dev)
     g.manual_seed(2109)
-    x = torch.randint(-1000, 1001, (p, cmax), dtype=torch.int32, device=dev,
-                      generator=g)
-    y = torch.empty_like(x)
-    xs, ys = dpar.pointers(dpar.rows(x)), dpar.pointers(dpar.rows(y))
     variants = [("dual", "auto"), ("dual", "rounds"),
                 ("reduce_bcast", "auto"), ("reduce_bcast", "rounds")]
     out = []
     for count in TABLE2_COUNTS:
         b = max(1, -(-count // blk))
+        # each rank's input and output in an allocation of its own, as each
+        # of the paper's processes has its own buffers (a p x count array
+        # would leave most rows off the 128-byte lines for odd counts)
+        x = y = None
+        torch.cuda.empty_cache()
+        x = [torch.randint(-1000, 1001, (max(count, 1),), dtype=torch.int32,
+                           device=dev, generator=g) for _ in range(p)]
+        y = [torch.empty_like(t) for t in x]
+        xs, ys = dpar.pointers(x), dpar.pointers(y)
         ref = None
         rec = {"count": count, "b": b}
         for alg, ex in variants:
@@ -212,7 +216,8 @@ def table2():
             dpar.dpar_check_status(stream)
             if count:
                 # every algorithm and executor gives the same int32 result
-                got = y[:, :count:max(1, count // 4096)].clone()
+                got = torch.stack([t[:count:max(1, count // 4096)]
+                                   for t in y])
                 assert bool((got == got[0]).all()), (count, alg, ex)
                 if ref is None:
                     ref = got[0]
