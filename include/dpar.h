@@ -365,7 +365,7 @@ const char* dpar_last_error(void);
  *                           post-order work items
  *   DPAR_XCD_RUNS=0|1       SPLIT's up-phase: each XCD takes a contiguous
  *                           run of work items (default 1 only when some
- *                           input row is off a 16-byte boundary)
+ *                           input row is off a 128-byte line)
  *   DPAR_BCAST_FASTDIV=0|1  SPLIT's broadcast pass: workgroups find their
  *                           row and tile by multiplication (1; default for
  *                           passes writing at most 2 GB) or by division (0)

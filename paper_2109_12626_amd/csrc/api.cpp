@@ -967,8 +967,10 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
       (opt.round_end >= 0 && opt.round_end < opt.round_begin))
     return fail(DPAR_ERR_INVALID_ARG, "bad round range [%d, %d)",
                 opt.round_begin, opt.round_end);
-  bool rows16 = true;   // every output row starts on a 16-byte boundary
-  bool xrows16 = true;  // every input row does
+  // every output row starts on a 128-byte cache line (else the broadcast
+  // pass aligns each row's stores itself)
+  bool rows_lines = true;
+  bool xrows_lines = true;  // every input row starts on a 128-byte line
   for (int i = 0; i < p; ++i) {
     if (!x[i] || !y[i])
       return fail(DPAR_ERR_INVALID_ARG, "null buffer for rank %d", i);
@@ -976,8 +978,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     if ((a | c) & 3)
       return fail(DPAR_ERR_INVALID_ARG, "rank %d buffer not 4-byte aligned",
                   i);
-    if (c & 15) rows16 = false;
-    if (a & 15) xrows16 = false;
+    if (c & 127) rows_lines = false;
+    if (a & 127) xrows_lines = false;
     if (((a | c) >> 48) != 0)
       return fail(DPAR_ERR_UNSUPPORTED, "rank %d address above 2^48", i);
   }
@@ -1317,9 +1319,11 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
       lds_floor = (size_t)st->lds_per_cu / (size_t)(per_cu + 1) + 1024;
     if (lds_floor > (size_t)st->lds_limit) lds_floor = 0;
   }
-  // the split up-phase on input rows off 16-byte boundaries: each XCD takes
-  // a contiguous run of work items (plan.hpp xcd_run_index)
-  if (up == dpar::Exec::SPLIT && path == dpar::Path::VEC16 && !xrows16)
+  // the split up-phase on input rows off the 128-byte lines: each XCD takes
+  // a contiguous run of work items (plan.hpp xcd_run_index; rows 16 bytes
+  // past a line, p = 1152: m = 2^22 up-phase 3.25 -> 3.07 ms, m = 2^18
+  // 227 -> 186 us)
+  if (up == dpar::Exec::SPLIT && path == dpar::Path::VEC16 && !xrows_lines)
     prm.xcd_runs = 1;
   if (up == dpar::Exec::SPLIT)
     prm.xcd_runs = env_int("DPAR_XCD_RUNS", prm.xcd_runs) != 0;
@@ -1386,7 +1390,7 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
         env_int("DPAR_BCAST_FASTDIV",
                 main_bytes * (uint64_t)(p - 1) <= kBcastFastDivMaxBytes) != 0;
     e = dpar::broadcast(tab, p, main_bytes, path == dpar::Path::VEC16,
-                        rows16, span, fastdiv, stream);
+                        rows_lines, span, fastdiv, stream);
     if (e != hipSuccess) return hip_fail(e, "broadcast launch");
   }
   if (!capturing && !fixed) {  // a pinned slot is never restaged, so never

@@ -1177,11 +1177,12 @@ __global__ __launch_bounds__(256) void k_bcast(const uint64_t* __restrict__ yp,
   __builtin_nontemporal_store(v,
                               reinterpret_cast<DPAR_GLOBAL T*>(yp[row] + off));
 }
-// (T = u32x4g: 16-byte lanes on 16-byte aligned rows; uint32_t: 4-byte
-// lanes)
+// (T = u32x4g: 16-byte lanes on rows that all start on 128-byte lines;
+// uint32_t: 4-byte lanes)
 
-// The same pass with 16-byte lanes for output rows that are not all 16-byte
-// aligned.  The body of row i starts at the row's own first 4 KB boundary,
+// The same pass with 16-byte lanes for output rows that do not all start on
+// a 128-byte line.  The body of row i starts at the row's own first 4 KB
+// boundary,
 // h dwords in (plan.hpp bcast_row_split), so that every store fills 16
 // aligned bytes and every workgroup's tile is whole cache lines of one
 // page; lane l of the body copies dwords [h + 4 l, h + 4 l + 4), reading
@@ -1193,7 +1194,10 @@ __global__ __launch_bounds__(256) void k_bcast(const uint64_t* __restrict__ yp,
 // 16-byte boundary and 3.06 ms to the next 128-byte line (tiles straddling
 // cache lines leave partial lines to two workgroups); on 16-byte aligned
 // rows the plain pass is faster (2.6 against 3.1 ms), so the library picks
-// this one only when some output row needs it.
+// this one only when some output row needs it.  Rows on 16-byte boundaries
+// but off the 128-byte lines need it too: their plain tiles leave partial
+// lines to two workgroups (p = 1152, m = 2^22, rows 16 bytes past a line:
+// 3.50 ms plain).
 template <bool FAST>
 __global__ __launch_bounds__(256) void k_bcast16_rows(
     const uint64_t* __restrict__ yp, BcastGrid g, uint64_t first) {
@@ -1466,13 +1470,13 @@ size_t level_lds_bytes(Path path, Kind kind, int p, int log2t, int nlev) {
 
 template <bool FAST>
 hipError_t broadcast_t(const Tables& tab, const BcastGrid& g, bool vec16,
-                       bool rows16, hipStream_t stream) {
+                       bool rows_lines, hipStream_t stream) {
   // a launch's thread count stays below 2^32: pieces of at most 2^23
   // workgroups (a multiple of 8, so workgroup w stays on XCD w mod 8)
   const uint64_t kMaxGrid = (1ull << 31) / 256;
   for (uint64_t first = 0; first < g.total; first += kMaxGrid) {
     const unsigned n = (unsigned)min(kMaxGrid, g.total - first);
-    if (vec16 && rows16)
+    if (vec16 && rows_lines)
       hipLaunchKernelGGL((k_bcast<u32x4g, FAST>), dim3(n), dim3(256), 0,
                          stream, tab.yp, g, first);
     else if (vec16)
@@ -1486,12 +1490,12 @@ hipError_t broadcast_t(const Tables& tab, const BcastGrid& g, bool vec16,
 }
 
 hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
-                     bool rows16, uint64_t span_bytes, bool fastdiv_tiles,
+                     bool rows_lines, uint64_t span_bytes, bool fastdiv_tiles,
                      hipStream_t stream) {
   BcastGrid g = bcast_grid(nbytes, vec16 ? 16 : 4, p, span_bytes);
   g.fast = fastdiv_tiles && g.total <= 0xFFFFFFFFull;
-  return g.fast ? broadcast_t<true>(tab, g, vec16, rows16, stream)
-                : broadcast_t<false>(tab, g, vec16, rows16, stream);
+  return g.fast ? broadcast_t<true>(tab, g, vec16, rows_lines, stream)
+                : broadcast_t<false>(tab, g, vec16, rows_lines, stream);
 }
 
 size_t wide_lds_bytes(size_t lane_bytes, int nslots) {

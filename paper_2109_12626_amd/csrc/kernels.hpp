@@ -170,13 +170,13 @@ size_t sub_lds_bytes(size_t lane_bytes, int ns);
 // Broadcast pass of the split executor: copies bytes [0, nbytes) of y_0 into
 // y_1 .. y_{p-1} (16-byte lanes when vec16, else 4-byte lanes), one
 // workgroup per (row, 256-lane tile), y_0 taken in spans of at most
-// span_bytes (every row of a span, then the next span).  rows16: every
-// output row starts on a 16-byte boundary (else the 16-byte lanes of each
-// row are shifted to its own 16-byte boundaries).  fastdiv_tiles: each
+// span_bytes (every row of a span, then the next span).  rows_lines: every
+// output row starts on a 128-byte line (else the 16-byte lanes of each row
+// are shifted to its own 4 KB boundaries).  fastdiv_tiles: each
 // workgroup finds its row and tile by multiplication instead of division
 // (plan.hpp bcast_tile).
 hipError_t broadcast(const Tables& tab, int p, uint64_t nbytes, bool vec16,
-                     bool rows16, uint64_t span_bytes, bool fastdiv_tiles,
+                     bool rows_lines, uint64_t span_bytes, bool fastdiv_tiles,
                      hipStream_t stream);
 
 // Bytes of dynamic LDS a workgroup needs.

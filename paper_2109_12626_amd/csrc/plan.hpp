@@ -167,7 +167,7 @@ DPAR_HOST_DEVICE inline void item_quanta(uint64_t NL, uint64_t b, uint64_t C,
 // contiguous run of the items: workgroup w runs on XCD k = w mod 8, which
 // takes items [k q + min(k, r), (k + 1) q + min(k + 1, r)) in order
 // (n = 8 q + r).  A bijection of [0, n).  Used for the up-phase when some
-// input row is off a 16-byte boundary: neighbouring work items then share
+// input row is off a 128-byte line: neighbouring work items then share
 // the cache line at their common edge, and on one XCD that line is fetched
 // from HBM once (p = 1152, m = 2^22: 3.19 -> 3.05 ms; on aligned rows,
 // where no line is shared, it is 0.6% slower, so it is not used there).

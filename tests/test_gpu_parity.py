@@ -253,6 +253,50 @@ def test_split_with_output_rows_off_16_byte_boundaries(span_kb, offset, dtype,
     assert (got[:, :k] == POISON).all() and (got[:, k + m * words:] == POISON).all()
 
 
+@pytest.mark.parametrize("offset", [16, 48, 112])
+@pytest.mark.parametrize("dtype,op,dist", [
+    ("int32", "sum", "uniform_int"), ("u32mat2x2", "matmul", "odd_det_u32_mat")])
+def test_split_with_rows_off_the_cache_lines(offset, dtype, op, dist):
+    """Rows on 16-byte boundaries but 16, 48 or 112 bytes past a 128-byte
+    line: the broadcast pass shifts each output row's stores to the row's
+    own 4 KB boundary and the up-phase hands each XCD a contiguous run of
+    work items.  Nothing outside the rows is touched."""
+    p, m = 11, 9000
+    kw = {"lo": -999, "hi": 999} if dist == "uniform_int" else {}
+    x = synth.generate(dist, 800 + offset, p, m, **kw)
+    words = 4 if dtype == "u32mat2x2" else 1
+    k = offset // 4
+    xi = np.ascontiguousarray(x).view(np.int32).reshape(p, m * words)
+    # rows 128-byte aligned in `big` (stride a multiple of 32 words)
+    stride = -(-(m * words + k + 32) // 32) * 32
+    big = torch.zeros((p, stride), dtype=torch.int32, device="cuda")
+    big[:, k:k + m * words] = torch.from_numpy(xi).cuda()
+    yb = torch.full_like(big, POISON)
+    from paper_2109_12626_amd import dpar
+    xs = [a + offset for a in dpar.rows(big)]
+    ys = [a + offset for a in dpar.rows(yb)]
+    s = torch.cuda.current_stream()
+    for b in (1, 7):
+        yb.fill_(POISON)
+        dpar.dpar_allreduce_ex(xs, ys, p, m, dtype, op, b, "split", s)
+        dpar.dpar_check_status(s)
+        got = yb.cpu().numpy()
+        out = got[:, k:k + m * words].copy().view(x.dtype).reshape(x.shape)
+        assert_all_ranks_equal(out, _want(x, dtype, op), f"offset {offset}")
+        assert (got[:, :k] == POISON).all()
+        assert (got[:, k + m * words:] == POISON).all()
+
+
+@pytest.mark.parametrize("exec", ["auto", "split"])
+def test_rows_16_bytes_apart_from_the_lines(exec):
+    """One [36, 2^16 + 4] int32 tensor: row i starts 16 i bytes (mod 128)
+    past a 128-byte line, every row on a 16-byte boundary."""
+    p, m = 36, (1 << 16) + 4
+    x = synth.generate("uniform_int", 4343, p, m, lo=-1000, hi=1000)
+    out = run(x, "int32", "sum", 0, exec)
+    assert_all_ranks_equal(out, _want(x, "int32", "sum"), exec)
+
+
 @pytest.mark.parametrize("exec", ["auto", "split"])
 def test_large_call_with_rows_of_every_misalignment(exec):
     """One [4, 2^20 + 1] fp32 tensor: its rows start 0, 4, 8 and 12 bytes
