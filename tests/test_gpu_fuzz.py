@@ -9,7 +9,8 @@ import torch
 
 import oracle
 import synth
-from tests._gpu import POISON, assert_all_ranks_equal, env_unit, lib, need_gpu
+from tests._gpu import (POISON, _Env, assert_all_ranks_equal, env_unit, lib,
+                        need_gpu)
 
 pytestmark = pytest.mark.gpu
 
@@ -57,7 +58,8 @@ def _wide_case(k):
                 exec=["auto", "split", "ticket"][int(r.integers(3))],
                 unit="wide", misalign=bool(r.integers(2)),
                 inplace=bool(r.integers(4) == 0), separate=bool(r.integers(2)),
-                seed=2700 + k)
+                seed=2700 + k,
+                wide_round=[None, 1, 2, 3, 5][int(r.integers(5))])
 
 
 @pytest.mark.parametrize("k", range(60))
@@ -65,7 +67,9 @@ def test_random_wide_items(k):
     """Seeded random calls with the wide post-order work item forced (the
     one-launch executors; on 4-byte lanes the library keeps the plain
     post-order item): p = 2 .. 128, every operator and tree layout,
-    misaligned rows, in place, separate allocations."""
+    misaligned rows, in place, separate allocations; rounds of 1, 2, 3 or 5
+    wide items in most cases (DPAR_WIDE_ROUND), so that the columns past the
+    last whole round go to tail items."""
     need_gpu()
     _check_case(_wide_case(k))
 
@@ -105,7 +109,7 @@ def _check_case(c):
         yb, ys = alloc()
     torch.cuda.synchronize()
     s = torch.cuda.current_stream()
-    with env_unit(c["unit"]):
+    with env_unit(c["unit"]), _Env("DPAR_WIDE_ROUND", c.get("wide_round")):
         dpar.dpar_allreduce_opt(xs, ys, p, m, c["dtype"], c["op"], c["b"],
                                 c["alg"], c["exec"], 0, -1, s)
     dpar.dpar_check_status(s)

@@ -86,6 +86,7 @@ def test_same_pointers_new_contents():
     (2304, 1 << 12, "int32", "max"),
     (36, 1 << 20, "int32", "sum"),          # wide items, one fused launch
     (64, 1 << 18, "u32mat2x2", "matmul"),   # wide items, split
+    (40, 4096 * 264 + 100, "int32", "sum"),  # full and tail wide items, split
 ])
 def test_sizes_and_types(p, m, dtype, op):
     need_gpu()
