@@ -463,6 +463,90 @@ def fixed_cost():
     print(json.dumps({"fixed_cost": out}))
 
 
+# AUTO's choice audited against the forced alternatives: int32 SUM, p ranks,
+# rows of n chunks of 16 KB (m = 4096 n).
+AUDIT_PS = (8, 12, 16, 20, 24, 32, 36, 40, 48, 64, 96, 128, 200, 288, 511,
+            700, 1152)
+AUDIT_NS = (32, 64, 96, 128, 160, 192, 224, 256, 320, 401, 512, 640)
+AUDIT_MODES = {
+    "auto": ({}, "auto"),
+    "postorder_split": ({"DPAR_UNIT": "seq"}, "split"),
+    "postorder_fused": ({"DPAR_UNIT": "seq",
+                         "DPAR_FUSE_BELOW_KB": str(1 << 30)}, "auto"),
+    "wide_split": ({"DPAR_UNIT": "wide"}, "split"),
+    "wide_fused": ({"DPAR_UNIT": "wide",
+                    "DPAR_FUSE_BELOW_KB": str(1 << 30)}, "auto"),
+}
+
+
+def auto_audit():
+    """AUTO's executor and work-item choice beside the forced alternatives
+    (post-order or wide items, split or one fused launch; forced wide items
+    fall back to post-order ones where their slots do not fit in LDS), for
+    int32 SUM over AUDIT_PS x AUDIT_NS, cold caches, minimum of 6 calls.
+    Prints one JSON line per case and a summary: how far AUTO is from the
+    best of the five."""
+    import torch
+
+    from paper_2109_12626_amd import dpar
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    flush = torch.empty(1 << 27, dtype=torch.float32, device=dev)
+    keys = ("DPAR_UNIT", "DPAR_FUSE_BELOW_KB")
+    saved = {k: os.environ.get(k) for k in keys}
+    rows = []
+    for p in AUDIT_PS:
+        for n in AUDIT_NS:
+            m = 4096 * n
+            if 2 * p * m * 4 > 24e9:
+                continue
+            x = torch.randint(-1000, 1000, (p, m), dtype=torch.int32,
+                              device=dev)
+            y = torch.empty_like(x)
+            xs, ys = dpar.pointers(dpar.rows(x)), dpar.pointers(dpar.rows(y))
+            rec = {"p": p, "n": n, "m": m}
+            for name, (env, ex) in AUDIT_MODES.items():
+                for k in keys:
+                    os.environ.pop(k, None)
+                os.environ.update(env)
+                fn = lambda: dpar.dpar_allreduce_ex(  # noqa: E731
+                    xs, ys, p, m, "int32", "sum", 0, ex, stream)
+                fn()
+                dpar.dpar_check_status(stream)
+                ts = []
+                for it in range(6):
+                    flush.fill_(float(it))
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    fn()
+                    e1.record(stream)
+                    e1.synchronize()
+                    ts.append(e0.elapsed_time(e1) * 1e3)
+                rec[name + "_us"] = round(min(ts), 1)
+            best = min(AUDIT_MODES, key=lambda k: rec[k + "_us"])
+            rec["best"] = best
+            rec["auto_over_best_pct"] = round(
+                (rec["auto_us"] / rec[best + "_us"] - 1) * 100, 1)
+            rows.append(rec)
+            log(json.dumps(rec))
+            del x, y
+            torch.cuda.empty_cache()
+    for k, v in saved.items():
+        if v is None:
+            os.environ.pop(k, None)
+        else:
+            os.environ[k] = v
+    over = sorted(r["auto_over_best_pct"] for r in rows)
+    print(json.dumps({"auto_audit": rows, "cases": len(rows),
+                      "auto_over_best_pct": {
+                          "mean": round(sum(over) / len(over), 2),
+                          "median": over[len(over) // 2],
+                          "max": over[-1],
+                          "over_3": sum(v > 3 for v in over),
+                          "over_6": sum(v > 6 for v in over)}}))
+
+
 def sweep(out_path, only=(), execs=("split", "ticket", "launch", "barrier"),
           algs=("dual",)):
     """Every workload x executor x block count, cold caches (a 512 MiB
@@ -569,6 +653,9 @@ def main():
                     help="interleaved read+write rates at the headline size")
     ap.add_argument("--fixed-cost", action="store_true",
                     help="fixed and per-byte cost of each phase, mid sizes")
+    ap.add_argument("--auto-audit", action="store_true",
+                    help="AUTO's choice beside forced work items and "
+                         "executors, int32 SUM over a grid of p and m")
     ap.add_argument("--sweep", metavar="OUT_JSONL",
                     help="measure every workload, executor and block count")
     ap.add_argument("--only", default="",
@@ -610,6 +697,9 @@ def main():
         return
     if args.fixed_cost:
         fixed_cost()
+        return
+    if args.auto_audit:
+        auto_audit()
         return
     if args.sweep:
         sweep(args.sweep, [v for v in args.only.split(",") if v],

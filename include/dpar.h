@@ -98,11 +98,15 @@ typedef enum {
  *   AUTO              SPLIT; one launch of every work item in round order
  *                     with the fused write-out instead for calls moving at
  *                     most 40 MB (2 p m times the element size), for calls
- *                     that run in subtree work items (p >= 256 and at most
- *                     two such items per CU, at least one per two CUs), and
- *                     for calls that run in wide work items with p <= 48
- *                     and at most one such item (16 KB of columns) per CU,
- *                     or with p <= 8.
+ *                     that run in post-order work items on rows of at most
+ *                     3.5 MB (p <= 16), 2.5 MB (p <= 48), 1.5 MB (p <= 64)
+ *                     or 1 MB (p < 1024),
+ *                     for calls that run in subtree work items (p >= 256
+ *                     and at most two such items per CU, at least one per
+ *                     two CUs), and for calls that run in wide work items
+ *                     with p <= 36 and at most one such item (16 KB of
+ *                     columns) per CU, with p <= 20 and at most two, or
+ *                     with p <= 8.
  * The last two run the algorithm's whole round structure, down-phase
  * included (dpar_schedule_rounds gives the number of rounds R):
  *   ROUNDS            one launch per round r = 0 .. R-1.  Round r runs the
@@ -327,8 +331,9 @@ const char* dpar_last_error(void);
  *                           post-order work item (wide: 16-byte lanes and
  *                           the one-launch executors and p < 1024 only,
  *                           else post-order; by default it runs one-launch
- *                           calls with at least one 16 KB column chunk per
- *                           CU unless the split up-phase caps its
+ *                           calls with at least 3/4 of a 16 KB column chunk
+ *                           per CU, 7/8 with p <= 16, unless the split
+ *                           up-phase caps its
  *                           post-order items' residency)
  *   DPAR_WIDE_TAIL=0|1      wide work items: the columns past the last
  *                           whole round of one item per CU in tail items
@@ -336,7 +341,10 @@ const char* dpar_last_error(void);
  *                           they fill more than 7/8 of a round (default 1;
  *                           0: full items only)
  *   DPAR_WIDE_ROUND=n       wide work items per round for that cut
- *                           (default: the CU count; tests)
+ *                           (default: the CU count; set, it applies to
+ *                           every wide call, also the fused calls of at
+ *                           most 20 ranks that otherwise take full items
+ *                           only; tests)
  *   DPAR_LEVEL_LOG2T=k      level work items of 2^k quanta (at most what
  *                           fits in LDS)
  *   DPAR_SUB_DEEP=0|1       subtree work items with 8 or 16 loads in flight

@@ -52,11 +52,19 @@ constexpr int kCapMinRanks = 256;
 constexpr int kCapMinItemsPerCu = 64;
 // Subtree work items: the deep load pipeline from this many ranks on.
 constexpr int kSubDeepMinRanks = 1024;
-// AUTO: a call of wide work items with at most kWideFuseMaxRanks ranks and
-// at most one item per CU, or with at most kWideFuseAnyRanks ranks, runs as
-// one fused launch.
-constexpr int kWideFuseMaxRanks = 48;
+// AUTO: a call of wide work items runs as one fused launch with at most
+// kWideFuseAnyRanks ranks, with at most kWideFuseTwoRanks ranks and at most
+// two items per CU (then without tail items), or with at most
+// kWideFuseMaxRanks ranks and at most one item per CU.
+constexpr int kWideFuseMaxRanks = 36;
+constexpr int kWideFuseTwoRanks = 20;
 constexpr int kWideFuseAnyRanks = 8;
+// Wide work items from 3/4 of an item per CU on, from 7/8 with at most
+// kWideLateRanks ranks.
+constexpr int kWideLateRanks = 16;
+// AUTO: calls of post-order items with fewer ranks than this, on rows of at
+// most seq_fuse_row_bytes(p), run as one fused launch.
+constexpr int kSeqFuseMaxRanks = 1024;
 // Level work item: loads in flight at once (1024 threads, 8 loads each).
 constexpr uint64_t kLvLoadsInFlight = 1024 * 8;
 // Ticket executor: rank loads per claimed batch of work items.
@@ -715,6 +723,17 @@ bool seq_wg_capped(int p, uint64_t items, const DeviceState& st) {
          items >= (uint64_t)kCapMinItemsPerCu * (uint64_t)st.num_cus;
 }
 
+// Longest rows (bytes) on which AUTO runs post-order items as one fused
+// launch: 3.5 MB up to 16 ranks (where wide items take longer rows), 2.5 MB
+// up to 48, 1.5 MB up to 64, 1 MB beyond (rows of 16 KB chunks: 224, 160,
+// 96, 64).
+uint64_t seq_fuse_row_bytes(int p) {
+  return p <= kWideLateRanks ? (7ull << 19)
+         : p <= 48           ? (5ull << 19)
+         : p <= 64           ? (3ull << 19)
+                             : (1ull << 20);
+}
+
 // Full wide items of a call of n wide chunks.  A wide item holds its CU for
 // a chain of p / kWideKF dependent visits, so a last round of one item per
 // CU with only a few items left leaves most CUs idle for about as long as
@@ -757,10 +776,12 @@ struct UnitChoice {
 //         carries: p = 1152, m = 4096, b = 205: 117 us post-order, 31 level);
 //   WIDE  the post-order walk with kWideQ quanta per lane: a whole call
 //         (split, ticket, one fused launch) on 16-byte lanes whose slots
-//         fit in LDS (p < 1024) with at least one wide item (16 KB of
-//         columns) per CU, unless the split up-phase would run post-order
-//         items under its residency cap
-//         (measured, int32 SUM, split, rows of 4 / 8 / 16 MB: p = 36
+//         fit in LDS (p < 1024) with at least 3/4 of a wide item (16 KB
+//         of columns) per CU (7/8 with at most 16 ranks), unless the split up-phase would run
+//         post-order items under its residency cap (measured, int32 SUM,
+//         split, 192 items: p = 96 107 -> 100 us, p = 288 291 -> 277 us,
+//         p = 900 893 -> 881 us; 224 items 5-11% faster; with 160 items
+//         post-order items are 0-3% faster; rows of 4 / 8 / 16 MB: p = 36
 //         61.4 -> 57.5, 110 -> 103, 211 -> 195 us; p = 128 180 -> 164,
 //         340 -> 315, 675 -> 627 us; p = 511 667 -> 611, 1311 -> 1235 us;
 //         under the cap, p = 256 .. 768 with 16 MB rows, post-order items
@@ -875,8 +896,13 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
           (size_t)st.lds_limit - dpar::kStaticLdsReserve;
   const bool seq_capped =
       ex == dpar::Exec::SPLIT && seq_wg_capped(p, all_items, st);
+  // at most kWideLateRanks ranks post-order items in one fused launch
+  // stay faster up to 7/8 of an item per CU (192 items, p = 8 / 12 / 16:
+  // 16.4 / 20.4 / 24.2 us post-order, 18.2 / 21.0 / 25.8 us wide)
+  const uint64_t wide_num = p <= kWideLateRanks ? 7 : 6;
   bool want_wide = wide_fits && !seq_capped &&
-                   (s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk >= cus;
+                   8 * ((s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk) >=
+                       wide_num * cus;
   if (forced) want_wide = !std::strcmp(u, "wide") && wide_fits;
   if (want_wide) uc.unit = dpar::Unit::WIDE;
   return uc;
@@ -1209,20 +1235,44 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // p writes per item then cost less than that pass as long as p is small.
   // Measured, int32 SUM, m = 2^20 (256 items), cold caches, split -> fused
   // (best of 3 runs): p = 8 24.5 -> 18.2 us, p = 24 43.1 -> 37.8 us,
-  // p = 36 57.8 -> 56.5 us, p = 48 70.9 -> 69.5 us, p = 56 80.2 -> 80.3 us,
-  // p = 64 89.3 -> 91.7 us (on another box p = 36 went the other way by
-  // 2-3%); with two items per CU (p = 36, m = 2^21) 103 -> 109 us.  With
-  // very few ranks the split executor's extra traffic (y_0 written, then
-  // read back: 1/p of the call's bytes) outweighs the interleaving at any
-  // size: p = 2, m = 2^22 (1024 items) 35.6 -> 17.6 us; p = 8, 1024 / 2048
-  // / 4096 items 59.4 -> 51.6, 106.8 -> 102.0, 204.5 -> 202.3 us; p = 12
-  // within 3% either way, p = 16 7-18% slower fused.
+  // p = 36 57.8 -> 56.5 us (on another box 2-3% the other way, and on a
+  // third within 2%); p = 32, 40 and 48 were 1-5% slower fused on that
+  // third box, p = 64 89.3 -> 91.7 us; with two items per CU (p = 36,
+  // m = 2^21) 103 -> 109 us.  With up to 20 ranks (two or three items fit
+  // per CU by LDS) the fused launch also wins with up to two items per CU,
+  // when it runs full items only (split -> fused, full items only / with
+  // tail items: p = 12, 401 items 1.00 -> 0.84 / 0.96; p = 16, 448 items
+  // 1.00 -> 0.95 / 1.07; p = 20, 480 items 1.00 -> 0.93 / 1.05; p = 24,
+  // 0.95-1.08, taken split).  With very few ranks the split executor's
+  // extra traffic (y_0 written, then read back: 1/p of the call's bytes)
+  // outweighs the interleaving at any size: p = 2, m = 2^22 (1024 items)
+  // 35.6 -> 17.6 us; p = 8, 1024 / 2048 / 4096 items 59.4 -> 51.6,
+  // 106.8 -> 102.0, 204.5 -> 202.3 us; 256 to 640 items 8-19% faster.
+  const uint64_t wide_n = (s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk;
+  const uint64_t ncu = (uint64_t)st->num_cus;
+  const bool wide_fuse_two =
+      p <= kWideFuseTwoRanks && wide_n > ncu && wide_n <= 2 * ncu;
   if (exec == DPAR_EXEC_AUTO && ex == dpar::Exec::SPLIT &&
       uc.unit == dpar::Unit::WIDE &&
-      (p <= kWideFuseAnyRanks ||
-       (p <= kWideFuseMaxRanks &&
-        (s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk <=
-            (uint64_t)st->num_cus)))
+      (p <= kWideFuseAnyRanks || wide_fuse_two ||
+       (p <= kWideFuseMaxRanks && wide_n <= ncu)))
+    ex = dpar::Exec::DISPATCH;
+  // AUTO, post-order items on short rows: one fused launch saves the split
+  // executor's second launch, the y_0 round trip and the broadcast pass's
+  // fill and drain, which on rows of at most seq_fuse_row_bytes(p) cost
+  // more than reading and writing in the same launch.  Measured, int32 SUM,
+  // cold caches, split -> fused: p = 36, m = 2^19 (2 MB rows) 36.2 ->
+  // 31.9 us; 2.5 MB rows: p = 12 24.2 -> 18.9 us, p = 24 32.6 -> 26.7 us,
+  // p = 48 52.7 -> 51.0 us; 3 MB rows: p = 8 / 12 / 16 20.9 / 25.7 / 28.5
+  // -> 16.4 / 20.4 / 24.2 us; p = 64, m = 393216 (1.5 MB rows) 45.7 ->
+  // 42.7 us; p = 128,
+  // m = 2^18 (1 MB rows) 60.4 -> 53.4 us; p = 288 120.6 -> 110.7 us;
+  // p = 511 201.7 -> 189.2 us; from p = 700 on within 2% either way; one
+  // step longer the split executor wins (p = 64, 2 MB rows: 58.6 vs 62.0 us;
+  // p = 128, 1.5 MB rows: 80.2 vs 85.1 us).
+  if (exec == DPAR_EXEC_AUTO && ex == dpar::Exec::SPLIT &&
+      uc.unit == dpar::Unit::SEQ && p < kSeqFuseMaxRanks &&
+      (uint64_t)m * esz <= seq_fuse_row_bytes(p))
     ex = dpar::Exec::DISPATCH;
   const dpar::Unit unit = uc.unit;
   prm.nlev = ops->height + 1;
@@ -1277,7 +1327,13 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     prm.grp = 1;
     prm.batch = 1;
     const uint64_t n = (s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk;
-    const uint64_t full = wide_full_items(n, *st);
+    // a fused launch of at most two items per CU with few ranks: full items
+    // only (see the executor choice above)
+    const bool full_only = ex == dpar::Exec::DISPATCH &&
+                           p <= kWideFuseTwoRanks &&
+                           n <= 2 * (uint64_t)st->num_cus &&
+                           !std::getenv("DPAR_WIDE_ROUND");
+    const uint64_t full = full_only ? n : wide_full_items(n, *st);
     prm.wide_full = (uint32_t)full;
     prm.C = (int)(full + (s.Q - std::min(s.Q, full * dpar::kWideChunk) +
                           dpar::kWideTailChunk - 1) /

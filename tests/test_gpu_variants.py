@@ -504,26 +504,65 @@ def test_wide_tail_choice(p, n, unit, full, capfd):
 F, S = "one_launch_fused", "split"
 
 
+@pytest.mark.parametrize("p,n", [(12, 401), (20, 480), (8, 300)])
+def test_fused_wide_calls_of_few_ranks_take_full_items(p, n, capfd):
+    """A fused launch of at most two wide items per CU with at most 20
+    ranks runs full items only (no tail items; DPAR_LOG shows
+    full_items = items); bit-exact against the oracle."""
+    from tests._gpu import _Env
+    need_gpu()
+    m = 4096 * n + 4
+    x = _input("uniform_int", 2211, p, m, lo=-1000, hi=1000)
+    want = oracle.allreduce_ltr(x, "int32", "sum")
+    with env_unit(None), _Env("DPAR_LOG", 1):
+        out = from_dev(_run(x, "int32", "sum", 0, "dual", "auto"), x)
+    err = capfd.readouterr().err
+    assert "unit=wide " in err and f"exec={F} " in err, err[-400:]
+    assert f" items={n + 1} full_items={n + 1}" in err, err[-400:]
+    assert_all_ranks_equal(out, want, f"fused full items p={p} n={n}")
+
+
 @pytest.mark.parametrize("p,m,b,dtype,unit,ex", [
     (36, 1 << 20, 0, "int32", "wide", F),         # 256 wide items
     (36, (1 << 20) + 3, 0, "int32", "wide", F),   # and 3 trailing elements
     (36, 1 << 21, 0, "int32", "wide", S),         # two items per CU
     (8, 1 << 22, 0, "int32", "wide", F),          # four per CU, 8 ranks
     (9, 1 << 22, 0, "int32", "wide", S),
-    (36, 4 * (255 * 1024), 0, "int32", "postorder", S),  # fewer than CUs
-    (48, 1 << 20, 0, "int32", "wide", F),
-    (49, 1 << 20, 0, "int32", "wide", S),
+    (36, 4 * (255 * 1024), 0, "int32", "wide", F),  # 3/4 of an item per CU
+    (36, 4 * (191 * 1024), 0, "int32", "postorder", S),  # fewer: post-order
+    (128, 4 * (192 * 1024), 0, "int32", "wide", S),
+    (128, 4 * (191 * 1024), 0, "int32", "postorder", S),
+    # post-order items on short rows in one fused launch: rows of at most
+    # 3.5 MB up to 16 ranks, 2.5 MB up to 48, 1.5 MB up to 64, 1 MB from 65
+    # to 1023 ranks
+    (48, 5 << 17, 0, "int32", "postorder", F),
+    (48, (5 << 17) + 4, 0, "int32", "postorder", S),
+    (16, 4 * (192 * 1024), 0, "int32", "postorder", F),  # 7/8 with p <= 16
+    (16, 4 * (224 * 1024), 0, "int32", "wide", F),
+    (64, 3 << 17, 0, "int32", "postorder", F),
+    (64, (3 << 17) + 4, 0, "int32", "postorder", S),
+    (96, 1 << 18, 0, "int32", "postorder", F),
+    (96, (1 << 18) + 4, 0, "int32", "postorder", S),
+    (37, 1 << 20, 0, "int32", "wide", S),
+    (48, 1 << 20, 0, "int32", "wide", S),
+    (16, 4 * (384 * 1024), 0, "int32", "wide", F),  # two per CU, 20 ranks
+    (20, 4 * (448 * 1024), 0, "int32", "wide", F),
+    (21, 4 * (448 * 1024), 0, "int32", "wide", S),
+    (16, 4 * (520 * 1024), 0, "int32", "wide", S),  # more than two per CU
+    (8, 4 * (520 * 1024), 0, "int32", "wide", F),
     (128, 1 << 20, 0, "int32", "wide", S),
     (300, 1 << 20, 0, "int32", "wide", S),
     (64, 1 << 18, 0, "u32mat2x2", "wide", S),     # the 64-rank matrix product
 ])
 def test_wide_unit_choice(p, m, b, dtype, unit, ex, capfd):
     """The library's own choice under AUTO (256 CUs): wide items where their
-    slots fit in LDS, at least one wide item per CU and no residency cap
-    for post-order items, post-order items otherwise; wide items of at most
-    48 ranks and one item per CU, or of at most 8 ranks, in one fused
-    launch, else split (shown by DPAR_LOG); bit-exact against the
-    oracle."""
+    slots fit in LDS, at least 3/4 of a wide item per CU (7/8 up to 16
+    ranks) and no residency
+    cap for post-order items, post-order items otherwise; wide items of at
+    most 36 ranks and one item per CU, of at most 20 ranks and two per CU,
+    or of at most 8 ranks, in one fused launch, else split; post-order items
+    in one fused launch on short rows (shown by DPAR_LOG); bit-exact against
+    the oracle."""
     from tests._gpu import _Env
     need_gpu()
     if dtype == "u32mat2x2":
