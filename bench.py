@@ -463,29 +463,47 @@ def fixed_cost():
     print(json.dumps({"fixed_cost": out}))
 
 
-# AUTO's choice audited against the forced alternatives: int32 SUM, p ranks,
-# rows of n chunks of 16 KB (m = 4096 n).
-AUDIT_PS = (8, 12, 16, 20, 24, 32, 36, 40, 48, 64, 96, 128, 200, 288, 511,
-            700, 1152)
-AUDIT_NS = (32, 64, 96, 128, 160, 192, 224, 256, 320, 401, 512, 640)
-AUDIT_MODES = {
-    "auto": ({}, "auto"),
-    "postorder_split": ({"DPAR_UNIT": "seq"}, "split"),
-    "postorder_fused": ({"DPAR_UNIT": "seq",
-                         "DPAR_FUSE_BELOW_KB": str(1 << 30)}, "auto"),
-    "wide_split": ({"DPAR_UNIT": "wide"}, "split"),
-    "wide_fused": ({"DPAR_UNIT": "wide",
-                    "DPAR_FUSE_BELOW_KB": str(1 << 30)}, "auto"),
-}
+# AUTO's choice audited against the forced alternatives, int32 SUM: (1) p
+# ranks, rows of n chunks of 16 KB (m = 4096 n), post-order or wide items;
+# (2) many ranks, short rows, post-order, subtree or level items.
+def _forced(unit, fused):
+    env = {"DPAR_UNIT": unit}
+    if fused:
+        env["DPAR_FUSE_BELOW_KB"] = str(1 << 30)
+    return env, "auto" if fused else "split"
+
+
+AUDIT_GRIDS = [
+    ("rows of 16 KB chunks",
+     (8, 12, 16, 20, 24, 32, 36, 40, 48, 64, 96, 128, 200, 288, 511, 700,
+      1152),
+     [4096 * n for n in (32, 64, 96, 128, 160, 192, 224, 256, 320, 401, 512,
+                         640)],
+     {"auto": ({}, "auto"),
+      "postorder_split": _forced("seq", False),
+      "postorder_fused": _forced("seq", True),
+      "wide_split": _forced("wide", False),
+      "wide_fused": _forced("wide", True)}),
+    ("many ranks, short rows",
+     (256, 400, 511, 700, 1152, 2304, 4608),
+     [256, 1024, 4096, 8192, 16384, 32768, 65536, 131072, 262144],
+     {"auto": ({}, "auto"),
+      "postorder_split": _forced("seq", False),
+      "postorder_fused": _forced("seq", True),
+      "subtree_split": _forced("sub", False),
+      "subtree_fused": _forced("sub", True),
+      "level_split": _forced("level", False),
+      "level_fused": _forced("level", True)}),
+]
 
 
 def auto_audit():
     """AUTO's executor and work-item choice beside the forced alternatives
-    (post-order or wide items, split or one fused launch; forced wide items
-    fall back to post-order ones where their slots do not fit in LDS), for
-    int32 SUM over AUDIT_PS x AUDIT_NS, cold caches, minimum of 6 calls.
-    Prints one JSON line per case and a summary: how far AUTO is from the
-    best of the five."""
+    (the work items of each grid, split or one fused launch; a forced item
+    that does not fit falls back as the library does), int32 SUM over the
+    grids of AUDIT_GRIDS, cold caches, minimum of 6 calls.  Prints one JSON
+    line per case and a summary per grid: how far AUTO is from the best of
+    the forced modes and itself."""
     import torch
 
     from paper_2109_12626_amd import dpar
@@ -494,18 +512,18 @@ def auto_audit():
     flush = torch.empty(1 << 27, dtype=torch.float32, device=dev)
     keys = ("DPAR_UNIT", "DPAR_FUSE_BELOW_KB")
     saved = {k: os.environ.get(k) for k in keys}
-    rows = []
-    for p in AUDIT_PS:
-        for n in AUDIT_NS:
-            m = 4096 * n
+    grids = []
+    for title, ps, ms, modes in AUDIT_GRIDS:
+        rows = []
+        for p, m in ((p, m) for p in ps for m in ms):
             if 2 * p * m * 4 > 24e9:
                 continue
             x = torch.randint(-1000, 1000, (p, m), dtype=torch.int32,
                               device=dev)
             y = torch.empty_like(x)
             xs, ys = dpar.pointers(dpar.rows(x)), dpar.pointers(dpar.rows(y))
-            rec = {"p": p, "n": n, "m": m}
-            for name, (env, ex) in AUDIT_MODES.items():
+            rec = {"p": p, "m": m}
+            for name, (env, ex) in modes.items():
                 for k in keys:
                     os.environ.pop(k, None)
                 os.environ.update(env)
@@ -524,7 +542,7 @@ def auto_audit():
                     e1.synchronize()
                     ts.append(e0.elapsed_time(e1) * 1e3)
                 rec[name + "_us"] = round(min(ts), 1)
-            best = min(AUDIT_MODES, key=lambda k: rec[k + "_us"])
+            best = min(modes, key=lambda k: rec[k + "_us"])
             rec["best"] = best
             rec["auto_over_best_pct"] = round(
                 (rec["auto_us"] / rec[best + "_us"] - 1) * 100, 1)
@@ -532,19 +550,20 @@ def auto_audit():
             log(json.dumps(rec))
             del x, y
             torch.cuda.empty_cache()
-    for k, v in saved.items():
-        if v is None:
-            os.environ.pop(k, None)
-        else:
-            os.environ[k] = v
-    over = sorted(r["auto_over_best_pct"] for r in rows)
-    print(json.dumps({"auto_audit": rows, "cases": len(rows),
+        over = sorted(r["auto_over_best_pct"] for r in rows)
+        grids.append({"grid": title, "modes": list(modes), "cases": rows,
                       "auto_over_best_pct": {
                           "mean": round(sum(over) / len(over), 2),
                           "median": over[len(over) // 2],
                           "max": over[-1],
                           "over_3": sum(v > 3 for v in over),
-                          "over_6": sum(v > 6 for v in over)}}))
+                          "over_6": sum(v > 6 for v in over)}})
+    for k, v in saved.items():
+        if v is None:
+            os.environ.pop(k, None)
+        else:
+            os.environ[k] = v
+    print(json.dumps({"auto_audit": grids}))
 
 
 def sweep(out_path, only=(), execs=("split", "ticket", "launch", "barrier"),

@@ -62,9 +62,10 @@ constexpr int kWideFuseAnyRanks = 8;
 // Wide work items from 3/4 of an item per CU on, from 7/8 with at most
 // kWideLateRanks ranks.
 constexpr int kWideLateRanks = 16;
-// AUTO: calls of post-order items with fewer ranks than this, on rows of at
-// most seq_fuse_row_bytes(p), run as one fused launch.
-constexpr int kSeqFuseMaxRanks = 1024;
+// AUTO: level work items run split from kLvSplitRanks ranks on, and from
+// kLvSplitManyRanks on with at least one item per CU; else fused.
+constexpr int kLvSplitRanks = 2048;
+constexpr int kLvSplitManyRanks = 1024;
 // Level work item: loads in flight at once (1024 threads, 8 loads each).
 constexpr uint64_t kLvLoadsInFlight = 1024 * 8;
 // Ticket executor: rank loads per claimed batch of work items.
@@ -857,12 +858,17 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
       const uint64_t groups =
           per_round ? 1 : ((uint64_t)s.b + (uint64_t)grp - 1) / (uint64_t)grp;
       // At large p a level item holds only a few quanta of each row; when
-      // that takes more than two level items per CU and the subtree item
-      // can take the call, it is faster (p = 2304, m = 2^14, b = 1:
-      // 1024 level items 0.200 ms, 64 subtree items 0.116 ms; p = 4608:
-      // 0.494 vs 0.213 ms; p = 1152 keeps level items: 512 of them,
-      // 0.054 vs 0.068 ms).
-      const bool crowded = groups * chunks(lg_max) > 2 * cus;
+      // that takes more than two level items per CU (four from
+      // kLvSplitRanks ranks on, where level items run split) and the
+      // subtree item can take the call, it is faster (p = 2304, m = 2^14,
+      // b = 1: 1024 level items 0.200 ms, 64 subtree items 0.116 ms;
+      // p = 4608: 0.494 vs 0.213 ms; p = 1152 keeps level items: 512 of
+      // them, 0.054 vs 0.068 ms; int32 SUM, the rule's b, level items
+      // split: p = 2304, m = 4096, 544 level items 67 us, subtree items
+      // 91 us; m = 8192, 1088 level items 105 us, subtree 95 us; p = 4608,
+      // m = 4096, 1024 level items 149 us, subtree 163 us).
+      const uint64_t crowd = p >= kLvSplitRanks ? 4 : 2;
+      const bool crowded = groups * chunks(lg_max) > crowd * cus;
       // Chunk used: the largest whose p * T loads are all in flight at once
       // (1024 threads with kLvBatch loads each), larger only while the items
       // outnumber the CUs.  Measured, int32 SUM, one fused launch: p = 288,
@@ -1267,13 +1273,31 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // -> 16.4 / 20.4 / 24.2 us; p = 64, m = 393216 (1.5 MB rows) 45.7 ->
   // 42.7 us; p = 128,
   // m = 2^18 (1 MB rows) 60.4 -> 53.4 us; p = 288 120.6 -> 110.7 us;
-  // p = 511 201.7 -> 189.2 us; from p = 700 on within 2% either way; one
+  // p = 511 201.7 -> 189.2 us; p = 700 to 2304 within 2% either way;
+  // p = 4608 2093 -> 1861 us; one
   // step longer the split executor wins (p = 64, 2 MB rows: 58.6 vs 62.0 us;
   // p = 128, 1.5 MB rows: 80.2 vs 85.1 us).
   if (exec == DPAR_EXEC_AUTO && ex == dpar::Exec::SPLIT &&
-      uc.unit == dpar::Unit::SEQ && p < kSeqFuseMaxRanks &&
+      uc.unit == dpar::Unit::SEQ &&
       (uint64_t)m * esz <= seq_fuse_row_bytes(p))
     ex = dpar::Exec::DISPATCH;
+  // AUTO, level items: a fused level item writes its chunk (a few quanta)
+  // to each of the p outputs, piece by piece; with many ranks and many
+  // items the broadcast pass's whole tiles are faster, with few ranks the
+  // fused launch (int32 SUM, the rule's b, fused -> split: p = 400,
+  // m = 16384 33.2 -> 35.2 us; p = 511 24.0 -> 28.6 us; p = 1152,
+  // m = 4096 (128 items) 30.6 -> 31.3 us, m = 8192 (264 items) 57.3 ->
+  // 48.2 us; p = 2304, m = 1024 36.6 -> 33.4 us; p = 4608, m = 256
+  // 45.0 -> 40.6 us, m = 1024 73.9 -> 53.4 us).
+  if (exec == DPAR_EXEC_AUTO && uc.unit == dpar::Unit::LEVEL &&
+      (ex == dpar::Exec::SPLIT || ex == dpar::Exec::DISPATCH)) {
+    const uint64_t lv_items =
+        grouped_units(s, prm.grp) / (uint64_t)s.C * (uint64_t)uc.lv_C;
+    const bool split = p >= kLvSplitRanks ||
+                       (p >= kLvSplitManyRanks &&
+                        lv_items >= (uint64_t)st->num_cus);
+    ex = split ? dpar::Exec::SPLIT : dpar::Exec::DISPATCH;
+  }
   const dpar::Unit unit = uc.unit;
   prm.nlev = ops->height + 1;
   if (unit == dpar::Unit::LEVEL) {

@@ -553,6 +553,18 @@ def test_fused_wide_calls_of_few_ranks_take_full_items(p, n, capfd):
     (128, 1 << 20, 0, "int32", "wide", S),
     (300, 1 << 20, 0, "int32", "wide", S),
     (64, 1 << 18, 0, "u32mat2x2", "wide", S),     # the 64-rank matrix product
+    # many ranks, short rows: post-order items fused on rows of at most 1 MB
+    (1100, 1 << 18, 0, "int32", "postorder", F),
+    (1100, (1 << 18) + 4, 0, "int32", "postorder", S),
+    # level items fused below 1024 ranks, split from 2048 on, and from 1024
+    # on with at least one item per CU
+    (511, 16384, 0, "int32", "level", F),
+    (1152, 4096, 0, "int32", "level", F),
+    (1152, 8192, 0, "int32", "level", S),
+    (2304, 1024, 0, "int32", "level", S),
+    # from 2048 ranks on level items up to four per CU, then subtree items
+    (2304, 4096, 0, "int32", "level", S),
+    (2304, 8192, 0, "int32", "subtree", S),
 ])
 def test_wide_unit_choice(p, m, b, dtype, unit, ex, capfd):
     """The library's own choice under AUTO (256 CUs): wide items where their
@@ -561,8 +573,8 @@ def test_wide_unit_choice(p, m, b, dtype, unit, ex, capfd):
     cap for post-order items, post-order items otherwise; wide items of at
     most 36 ranks and one item per CU, of at most 20 ranks and two per CU,
     or of at most 8 ranks, in one fused launch, else split; post-order items
-    in one fused launch on short rows (shown by DPAR_LOG); bit-exact against
-    the oracle."""
+    in one fused launch on short rows; level items fused with few ranks and
+    split with many (shown by DPAR_LOG); bit-exact against the oracle."""
     from tests._gpu import _Env
     need_gpu()
     if dtype == "u32mat2x2":
