@@ -102,8 +102,8 @@ typedef enum {
  *                     and at least one such item per CU), for calls that
  *                     run in level work items below that, for calls that
  *                     run in post-order work items on rows of at most
- *                     3.5 MB (p <= 16), 2.5 MB (p <= 48), 1.5 MB (p <= 64)
- *                     or 1 MB,
+ *                     3.5 MB (p <= 16), 2.5 MB (p <= 48), 1.5 MB (p <= 64),
+ *                     1 MB (p <= 96) or 512 KB,
  *                     for calls that run in subtree work items (p >= 256
  *                     and at most two such items per CU, at least one per
  *                     two CUs), and for calls that run in wide work items

@@ -726,13 +726,14 @@ bool seq_wg_capped(int p, uint64_t items, const DeviceState& st) {
 
 // Longest rows (bytes) on which AUTO runs post-order items as one fused
 // launch: 3.5 MB up to 16 ranks (where wide items take longer rows), 2.5 MB
-// up to 48, 1.5 MB up to 64, 1 MB beyond (rows of 16 KB chunks: 224, 160,
-// 96, 64).
+// up to 48, 1.5 MB up to 64, 1 MB up to 96, 512 KB beyond (rows of 16 KB
+// chunks: 224, 160, 96, 64, 32).
 uint64_t seq_fuse_row_bytes(int p) {
   return p <= kWideLateRanks ? (7ull << 19)
          : p <= 48           ? (5ull << 19)
          : p <= 64           ? (3ull << 19)
-                             : (1ull << 20);
+         : p <= 96           ? (1ull << 20)
+                             : (1ull << 19);
 }
 
 // Full wide items of a call of n wide chunks.  A wide item holds its CU for
@@ -1274,7 +1275,12 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // 42.7 us; p = 128,
   // m = 2^18 (1 MB rows) 60.4 -> 53.4 us; p = 288 120.6 -> 110.7 us;
   // p = 511 201.7 -> 189.2 us; p = 700 to 2304 within 2% either way;
-  // p = 4608 2093 -> 1861 us; one
+  // p = 4608 2093 -> 1861 us.  With the caches warm from the call before
+  // (back-to-back calls) the split executor gains more: fused on 1 MB rows
+  // is then 9-16% slower from p = 128 on (p = 1152: 388 vs 464 us; at
+  // p = 96 as fast), on 512 KB rows 3-7% slower from p = 400 on and
+  // faster up to p = 200 (44.4 vs 47.8 us), so beyond 96 ranks only rows
+  // of up to 512 KB are fused (cold, p = 400 .. 1152: 12-16% faster).  One
   // step longer the split executor wins (p = 64, 2 MB rows: 58.6 vs 62.0 us;
   // p = 128, 1.5 MB rows: 80.2 vs 85.1 us).
   if (exec == DPAR_EXEC_AUTO && ex == dpar::Exec::SPLIT &&

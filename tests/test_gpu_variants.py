@@ -533,8 +533,8 @@ def test_fused_wide_calls_of_few_ranks_take_full_items(p, n, capfd):
     (128, 4 * (192 * 1024), 0, "int32", "wide", S),
     (128, 4 * (191 * 1024), 0, "int32", "postorder", S),
     # post-order items on short rows in one fused launch: rows of at most
-    # 3.5 MB up to 16 ranks, 2.5 MB up to 48, 1.5 MB up to 64, 1 MB from 65
-    # to 1023 ranks
+    # 3.5 MB up to 16 ranks, 2.5 MB up to 48, 1.5 MB up to 64, 1 MB up to
+    # 96, 512 KB beyond
     (48, 5 << 17, 0, "int32", "postorder", F),
     (48, (5 << 17) + 4, 0, "int32", "postorder", S),
     (16, 4 * (192 * 1024), 0, "int32", "postorder", F),  # 7/8 with p <= 16
@@ -543,6 +543,7 @@ def test_fused_wide_calls_of_few_ranks_take_full_items(p, n, capfd):
     (64, (3 << 17) + 4, 0, "int32", "postorder", S),
     (96, 1 << 18, 0, "int32", "postorder", F),
     (96, (1 << 18) + 4, 0, "int32", "postorder", S),
+    (97, 1 << 18, 0, "int32", "postorder", S),
     (37, 1 << 20, 0, "int32", "wide", S),
     (48, 1 << 20, 0, "int32", "wide", S),
     (16, 4 * (384 * 1024), 0, "int32", "wide", F),  # two per CU, 20 ranks
@@ -553,9 +554,10 @@ def test_fused_wide_calls_of_few_ranks_take_full_items(p, n, capfd):
     (128, 1 << 20, 0, "int32", "wide", S),
     (300, 1 << 20, 0, "int32", "wide", S),
     (64, 1 << 18, 0, "u32mat2x2", "wide", S),     # the 64-rank matrix product
-    # many ranks, short rows: post-order items fused on rows of at most 1 MB
-    (1100, 1 << 18, 0, "int32", "postorder", F),
-    (1100, (1 << 18) + 4, 0, "int32", "postorder", S),
+    # more ranks, short rows: post-order items fused on rows of at most
+    # 512 KB
+    (200, 1 << 17, 0, "int32", "postorder", F),
+    (200, (1 << 17) + 4, 0, "int32", "postorder", S),
     # level items fused below 1024 ranks, split from 2048 on, and from 1024
     # on with at least one item per CU
     (511, 16384, 0, "int32", "level", F),
