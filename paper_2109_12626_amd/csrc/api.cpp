@@ -779,8 +779,9 @@ struct UnitChoice {
 //   WIDE  the post-order walk with kWideQ quanta per lane: a whole call
 //         (split, ticket, one fused launch) on 16-byte lanes whose slots
 //         fit in LDS (p < 1024) with at least 3/4 of a wide item (16 KB
-//         of columns) per CU (7/8 with at most 16 ranks), unless the split up-phase would run
-//         post-order items under its residency cap (measured, int32 SUM,
+//         of columns) per CU (7/8 with at most 16 ranks), unless the split
+//         up-phase would run post-order items under its residency cap
+//         (measured, int32 SUM,
 //         split, 192 items: p = 96 107 -> 100 us, p = 288 291 -> 277 us,
 //         p = 900 893 -> 881 us; 224 items 5-11% faster; with 160 items
 //         post-order items are 0-3% faster; rows of 4 / 8 / 16 MB: p = 36
@@ -903,9 +904,9 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
           (size_t)st.lds_limit - dpar::kStaticLdsReserve;
   const bool seq_capped =
       ex == dpar::Exec::SPLIT && seq_wg_capped(p, all_items, st);
-  // at most kWideLateRanks ranks post-order items in one fused launch
-  // stay faster up to 7/8 of an item per CU (192 items, p = 8 / 12 / 16:
-  // 16.4 / 20.4 / 24.2 us post-order, 18.2 / 21.0 / 25.8 us wide)
+  // With at most kWideLateRanks ranks, post-order items in one fused
+  // launch stay faster up to 7/8 of an item per CU (192 items, p = 8 / 12
+  // / 16: 16.4 / 20.4 / 24.2 us post-order, 18.2 / 21.0 / 25.8 us wide).
   const uint64_t wide_num = p <= kWideLateRanks ? 7 : 6;
   bool want_wide = wide_fits && !seq_capped &&
                    8 * ((s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk) >=
@@ -1272,10 +1273,9 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // 31.9 us; 2.5 MB rows: p = 12 24.2 -> 18.9 us, p = 24 32.6 -> 26.7 us,
   // p = 48 52.7 -> 51.0 us; 3 MB rows: p = 8 / 12 / 16 20.9 / 25.7 / 28.5
   // -> 16.4 / 20.4 / 24.2 us; p = 64, m = 393216 (1.5 MB rows) 45.7 ->
-  // 42.7 us; p = 128,
-  // m = 2^18 (1 MB rows) 60.4 -> 53.4 us; p = 288 120.6 -> 110.7 us;
-  // p = 511 201.7 -> 189.2 us; p = 700 to 2304 within 2% either way;
-  // p = 4608 2093 -> 1861 us.  With the caches warm from the call before
+  // 42.7 us; 1 MB rows: p = 128 60.4 -> 53.4 us, p = 288 120.6 ->
+  // 110.7 us, p = 511 201.7 -> 189.2 us, p = 700 to 2304 within 2% either
+  // way, p = 4608 2093 -> 1861 us.  With the caches warm from the call before
   // (back-to-back calls) the split executor gains more: fused on 1 MB rows
   // is then 9-16% slower from p = 128 on (p = 1152: 388 vs 464 us; at
   // p = 96 as fast), on 512 KB rows 3-7% slower from p = 400 on and
@@ -1358,7 +1358,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
     prm.batch = 1;
     const uint64_t n = (s.Q + dpar::kWideChunk - 1) / dpar::kWideChunk;
     // a fused launch of at most two items per CU with few ranks: full items
-    // only (see the executor choice above)
+    // only (see the executor choice above), unless DPAR_WIDE_ROUND sets the
+    // rounds
     const bool full_only = ex == dpar::Exec::DISPATCH &&
                            p <= kWideFuseTwoRanks &&
                            n <= 2 * (uint64_t)st->num_cus &&
