@@ -74,6 +74,33 @@ def test_random_wide_items(k):
     _check_case(_wide_case(k))
 
 
+def _mid_case(k):
+    r = np.random.default_rng(9800 + k)
+    p = int(r.choice([2, 5, 8, 12, 16, 20, 24, 36, 48, 64, 96, 130, 200, 288,
+                      400, 511, 700, 1100]))
+    dtype, op, dist = PAIRS[int(r.integers(len(PAIRS)))]
+    words = 4 if dtype == "u32mat2x2" else 1
+    # 4 to 32 MB of input: the sizes where AUTO picks between post-order,
+    # wide, subtree and level items and between split and one fused launch
+    mmax = max(2, (1 << 23) // (p * words))
+    m = int(r.integers(max(1, mmax // 8), mmax))
+    return dict(p=p, m=m, b=0, dtype=dtype, op=op, dist=dist,
+                alg=ALGS[int(r.integers(3))], exec="auto", unit=None,
+                misalign=bool(r.integers(4) == 0),
+                inplace=bool(r.integers(6) == 0),
+                separate=bool(r.integers(3) == 0), seed=2800 + k)
+
+
+@pytest.mark.parametrize("k", range(60))
+def test_random_auto_mid_size(k):
+    """Seeded random calls of 4 to 32 MB under AUTO with the rule's b
+    (p = 2 .. 1100, every operator and tree layout, misaligned rows, in
+    place, separate allocations): whatever work item and executor the
+    library picks, bit for bit against the oracle."""
+    need_gpu()
+    _check_case(_mid_case(k))
+
+
 def _check_case(c):
     dpar = lib()
     p, m = c["p"], c["m"]
