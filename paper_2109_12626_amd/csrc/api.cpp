@@ -1275,8 +1275,10 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // -> 16.4 / 20.4 / 24.2 us; p = 64, m = 393216 (1.5 MB rows) 45.7 ->
   // 42.7 us; 1 MB rows: p = 128 60.4 -> 53.4 us, p = 288 120.6 ->
   // 110.7 us, p = 511 201.7 -> 189.2 us, p = 700 to 2304 within 2% either
-  // way, p = 4608 2093 -> 1861 us.  With the caches warm from the call before
-  // (back-to-back calls) the split executor gains more: fused on 1 MB rows
+  // way, p = 4608 2093 -> 1861 us.  Those calls follow a 512 MB write that
+  // flushes the caches; in back-to-back calls (also on two alternating sets
+  // of buffers, so not from reused data; after a 32 MB write too) the split
+  // executor is faster: fused on 1 MB rows
   // is then 9-16% slower from p = 128 on (p = 1152: 388 vs 464 us; at
   // p = 96 as fast), on 512 KB rows 3-7% slower from p = 400 on and
   // faster up to p = 200 (44.4 vs 47.8 us), so beyond 96 ranks only rows
