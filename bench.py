@@ -501,9 +501,10 @@ def auto_audit():
     """AUTO's executor and work-item choice beside the forced alternatives
     (the work items of each grid, split or one fused launch; a forced item
     that does not fit falls back as the library does), int32 SUM over the
-    grids of AUDIT_GRIDS, cold caches, minimum of 6 calls.  Prints one JSON
-    line per case and a summary per grid: how far AUTO is from the best of
-    the forced modes and itself."""
+    grids of AUDIT_GRIDS, minimum of 6 calls, in two regimes: back-to-back
+    calls, and calls each after a 512 MB write that flushes the caches.
+    Prints one JSON line per case and a summary per grid and regime: how far
+    AUTO is from the best of the forced modes and itself."""
     import torch
 
     from paper_2109_12626_amd import dpar
@@ -513,7 +514,8 @@ def auto_audit():
     keys = ("DPAR_UNIT", "DPAR_FUSE_BELOW_KB")
     saved = {k: os.environ.get(k) for k in keys}
     grids = []
-    for title, ps, ms, modes in AUDIT_GRIDS:
+    for (title, ps, ms, modes), flushed in (
+            (g, f) for f in (False, True) for g in AUDIT_GRIDS):
         rows = []
         for p, m in ((p, m) for p in ps for m in ms):
             if 2 * p * m * 4 > 24e9:
@@ -522,7 +524,7 @@ def auto_audit():
                               device=dev)
             y = torch.empty_like(x)
             xs, ys = dpar.pointers(dpar.rows(x)), dpar.pointers(dpar.rows(y))
-            rec = {"p": p, "m": m}
+            rec = {"p": p, "m": m, "flushed": flushed}
             for name, (env, ex) in modes.items():
                 for k in keys:
                     os.environ.pop(k, None)
@@ -533,7 +535,8 @@ def auto_audit():
                 dpar.dpar_check_status(stream)
                 ts = []
                 for it in range(6):
-                    flush.fill_(float(it))
+                    if flushed:
+                        flush.fill_(float(it))
                     e0 = torch.cuda.Event(enable_timing=True)
                     e1 = torch.cuda.Event(enable_timing=True)
                     e0.record(stream)
@@ -551,7 +554,8 @@ def auto_audit():
             del x, y
             torch.cuda.empty_cache()
         over = sorted(r["auto_over_best_pct"] for r in rows)
-        grids.append({"grid": title, "modes": list(modes), "cases": rows,
+        grids.append({"grid": title, "flushed": flushed,
+                      "modes": list(modes), "cases": rows,
                       "auto_over_best_pct": {
                           "mean": round(sum(over) / len(over), 2),
                           "median": over[len(over) // 2],

@@ -98,15 +98,15 @@ typedef enum {
  *   AUTO              SPLIT; one launch of every work item in round order
  *                     with the fused write-out instead for calls moving at
  *                     most 40 MB (2 p m times the element size) unless they
- *                     run in level work items with p >= 2048 (or p >= 1024
- *                     and at least one such item per CU), for calls that
- *                     run in level work items below that, for calls that
+ *                     run in level work items with p >= 1024, for calls
+ *                     that run in level work items below that, for calls
+ *                     that
  *                     run in post-order work items on rows of at most
  *                     3.5 MB (p <= 16), 2.5 MB (p <= 48), 1.5 MB (p <= 64),
  *                     1 MB (p <= 96) or 512 KB,
  *                     for calls that run in subtree work items (p >= 256
  *                     and at most two such items per CU, at least one per
- *                     two CUs), and for calls that run in wide work items
+ *                     four CUs), and for calls that run in wide work items
  *                     with p <= 36 and at most one such item (16 KB of
  *                     columns) per CU, with p <= 20 and at most two, or
  *                     with p <= 8.

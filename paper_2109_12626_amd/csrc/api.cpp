@@ -62,10 +62,11 @@ constexpr int kWideFuseAnyRanks = 8;
 // Wide work items from 3/4 of an item per CU on, from 7/8 with at most
 // kWideLateRanks ranks.
 constexpr int kWideLateRanks = 16;
-// AUTO: level work items run split from kLvSplitRanks ranks on, and from
-// kLvSplitManyRanks on with at least one item per CU; else fused.
-constexpr int kLvSplitRanks = 2048;
-constexpr int kLvSplitManyRanks = 1024;
+// AUTO: level work items run split from kLvSplitRanks ranks on, else
+// fused; from kLvCrowdRanks ranks on they are taken up to four per CU
+// before subtree items (else two).
+constexpr int kLvSplitRanks = 1024;
+constexpr int kLvCrowdRanks = 2048;
 // Level work item: loads in flight at once (1024 threads, 8 loads each).
 constexpr uint64_t kLvLoadsInFlight = 1024 * 8;
 // Ticket executor: rank loads per claimed batch of work items.
@@ -861,15 +862,15 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
           per_round ? 1 : ((uint64_t)s.b + (uint64_t)grp - 1) / (uint64_t)grp;
       // At large p a level item holds only a few quanta of each row; when
       // that takes more than two level items per CU (four from
-      // kLvSplitRanks ranks on, where level items run split) and the
-      // subtree item can take the call, it is faster (p = 2304, m = 2^14,
+      // kLvCrowdRanks ranks on) and the subtree item can take the call,
+      // it is faster (p = 2304, m = 2^14,
       // b = 1: 1024 level items 0.200 ms, 64 subtree items 0.116 ms;
       // p = 4608: 0.494 vs 0.213 ms; p = 1152 keeps level items: 512 of
       // them, 0.054 vs 0.068 ms; int32 SUM, the rule's b, level items
       // split: p = 2304, m = 4096, 544 level items 67 us, subtree items
       // 91 us; m = 8192, 1088 level items 105 us, subtree 95 us; p = 4608,
       // m = 4096, 1024 level items 149 us, subtree 163 us).
-      const uint64_t crowd = p >= kLvSplitRanks ? 4 : 2;
+      const uint64_t crowd = p >= kLvCrowdRanks ? 4 : 2;
       const bool crowded = groups * chunks(lg_max) > crowd * cus;
       // Chunk used: the largest whose p * T loads are all in flight at once
       // (1024 threads with kLvBatch loads each), larger only while the items
@@ -1228,14 +1229,17 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // Measured, int32 SUM, cold caches, the sqrt(m log2 p) rule's b: p = 1152,
   // m = 2^16 (256 items) split 0.126 ms, fused 0.107 ms; p = 2304,
   // m = 57344 (224 items) 0.199 vs 0.180 ms; p = 576, m = 57344 0.063 vs
-  // 0.057 ms; p = 288, m = 115712 (452 items) 0.060 vs 0.055 ms; with fewer
-  // items than half the CUs the chains dominate and fused is no better
+  // 0.057 ms; p = 288, m = 115712 (452 items) 0.060 vs 0.055 ms; down to a
+  // quarter of an item per CU in back-to-back calls (64 items, m = 16384:
+  // p = 700 46.0 -> 41.9 us, p = 1152 58.5 -> 51.0 us, p = 2304 102.0 ->
+  // 93.7 us, p = 4608 185.9 -> 175.2 us; after a cache flush within 2%
+  // either way); with fewer the chains dominate and fused is no better
   // (p = 2304, m = 14336, 56 items: 0.107 vs 0.117 ms).  Calls that take
-  // post-order items stay split, which is faster there from 256 MB up
-  // (p = 36 .. 2304: 8-35% at 1-38 GB).
+  // post-order items on long rows stay split, which is faster there from
+  // 256 MB up (p = 36 .. 2304: 8-35% at 1-38 GB).
   if (exec == DPAR_EXEC_AUTO && ex == dpar::Exec::SPLIT &&
       uc.unit == dpar::Unit::SUB &&
-      2 * ((s.Q + 63) / 64) >= (uint64_t)st->num_cus)
+      4 * ((s.Q + 63) / 64) >= (uint64_t)st->num_cus)
     ex = dpar::Exec::DISPATCH;
   // AUTO, wide items: with at most one per CU they all run at once, read
   // their rows together and then write y together, so one fused launch
@@ -1290,22 +1294,17 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
       (uint64_t)m * esz <= seq_fuse_row_bytes(p))
     ex = dpar::Exec::DISPATCH;
   // AUTO, level items: a fused level item writes its chunk (a few quanta)
-  // to each of the p outputs, piece by piece; with many ranks and many
-  // items the broadcast pass's whole tiles are faster, with few ranks the
-  // fused launch (int32 SUM, the rule's b, fused -> split: p = 400,
-  // m = 16384 33.2 -> 35.2 us; p = 511 24.0 -> 28.6 us; p = 1152,
-  // m = 4096 (128 items) 30.6 -> 31.3 us, m = 8192 (264 items) 57.3 ->
-  // 48.2 us; p = 2304, m = 1024 36.6 -> 33.4 us; p = 4608, m = 256
-  // 45.0 -> 40.6 us, m = 1024 73.9 -> 53.4 us).
+  // to each of the p outputs, piece by piece; with many ranks the
+  // broadcast pass's whole tiles are faster, with few ranks the fused
+  // launch (int32 SUM, the rule's b, fused -> split, after a cache flush:
+  // p = 400, m = 16384 33.2 -> 35.2 us; p = 511 24.0 -> 28.6 us; p = 1152,
+  // m = 8192 57.3 -> 48.2 us; p = 2304, m = 1024 36.6 -> 33.4 us;
+  // p = 4608, m = 1024 73.9 -> 53.4 us; p = 1152, m = 1024 and 4096 2-4%
+  // slower split, but in back-to-back calls 24.7 -> 18.7 us and 31.7 ->
+  // 30.1 us).
   if (exec == DPAR_EXEC_AUTO && uc.unit == dpar::Unit::LEVEL &&
-      (ex == dpar::Exec::SPLIT || ex == dpar::Exec::DISPATCH)) {
-    const uint64_t lv_items =
-        grouped_units(s, prm.grp) / (uint64_t)s.C * (uint64_t)uc.lv_C;
-    const bool split = p >= kLvSplitRanks ||
-                       (p >= kLvSplitManyRanks &&
-                        lv_items >= (uint64_t)st->num_cus);
-    ex = split ? dpar::Exec::SPLIT : dpar::Exec::DISPATCH;
-  }
+      (ex == dpar::Exec::SPLIT || ex == dpar::Exec::DISPATCH))
+    ex = p >= kLvSplitRanks ? dpar::Exec::SPLIT : dpar::Exec::DISPATCH;
   const dpar::Unit unit = uc.unit;
   prm.nlev = ops->height + 1;
   if (unit == dpar::Unit::LEVEL) {

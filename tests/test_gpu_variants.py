@@ -558,12 +558,14 @@ def test_fused_wide_calls_of_few_ranks_take_full_items(p, n, capfd):
     # 512 KB
     (200, 1 << 17, 0, "int32", "postorder", F),
     (200, (1 << 17) + 4, 0, "int32", "postorder", S),
-    # level items fused below 1024 ranks, split from 2048 on, and from 1024
-    # on with at least one item per CU
+    # level items fused below 1024 ranks, split from 1024 on
     (511, 16384, 0, "int32", "level", F),
-    (1152, 4096, 0, "int32", "level", F),
-    (1152, 8192, 0, "int32", "level", S),
+    (1152, 4096, 0, "int32", "level", S),
+    (1152, 1024, 0, "int32", "level", S),
     (2304, 1024, 0, "int32", "level", S),
+    # subtree items fused from a quarter of an item per CU on
+    (1152, 16384, 0, "int32", "subtree", F),
+    (4608, 12288, 0, "int32", "subtree", S),
     # from 2048 ranks on level items up to four per CU, then subtree items
     (2304, 4096, 0, "int32", "level", S),
     (2304, 8192, 0, "int32", "subtree", S),
