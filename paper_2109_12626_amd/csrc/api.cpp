@@ -62,10 +62,12 @@ constexpr int kWideFuseAnyRanks = 8;
 // Wide work items from 3/4 of an item per CU on, from 7/8 with at most
 // kWideLateRanks ranks.
 constexpr int kWideLateRanks = 16;
-// AUTO: level work items run split from kLvSplitRanks ranks on, else
-// fused; from kLvCrowdRanks ranks on they are taken up to four per CU
-// before subtree items (else two).
+// AUTO: level work items run split from kLvSplitRanks ranks on, and from
+// kLvSplitManyRanks on with at least one item per CU, else fused; from
+// kLvCrowdRanks ranks on they are taken up to four per CU before subtree
+// items (else two).
 constexpr int kLvSplitRanks = 1024;
+constexpr int kLvSplitManyRanks = 512;
 constexpr int kLvCrowdRanks = 2048;
 // Level work item: loads in flight at once (1024 threads, 8 loads each).
 constexpr uint64_t kLvLoadsInFlight = 1024 * 8;
@@ -886,7 +888,17 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
       const int forced_lg = env_int("DPAR_LEVEL_LOG2T", -1);
       if (forced_lg >= 0) lg = std::min(forced_lg, tmax);
       const int lv_C = (int)chunks(lg);
-      if (forced || !(crowded && want_sub)) {
+      // A level plan of more than one item per CU ends with a round that
+      // is not full, each of its items as long as a whole round's; subtree
+      // items, at least a quarter of one per CU, take such a call faster
+      // (p = 400, m = 16384: 304 level items 31-33 us, 64 subtree items
+      // 27-31 us; m = 24576, p = 350 .. 600: 384 level items 35-49 us,
+      // 96 subtree items 28-45 us); with fewer subtree items their chains
+      // cost more (p = 1152, m = 8192: 264 level items 43-48 us, 32
+      // subtree items 52-55 us).
+      const uint64_t lv_items = groups * (uint64_t)lv_C;
+      const bool lv_rounds = lv_items > cus && 4 * sub_items >= cus;
+      if (forced || !((crowded || lv_rounds) && want_sub)) {
         uc.unit = dpar::Unit::LEVEL;
         uc.lv_log2t = lg;
         uc.lv_C = lv_C;
@@ -1301,10 +1313,18 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // m = 8192 57.3 -> 48.2 us; p = 2304, m = 1024 36.6 -> 33.4 us;
   // p = 4608, m = 1024 73.9 -> 53.4 us; p = 1152, m = 1024 and 4096 2-4%
   // slower split, but in back-to-back calls 24.7 -> 18.7 us and 31.7 ->
-  // 30.1 us).
+  // 30.1 us; from 512 ranks on with at least one item per CU: p = 700,
+  // m = 8192 38.9 -> 34.3 us back to back, 38.8 -> 35.8 us after a flush;
+  // p = 900 42.9 -> 37.2 us).
   if (exec == DPAR_EXEC_AUTO && uc.unit == dpar::Unit::LEVEL &&
-      (ex == dpar::Exec::SPLIT || ex == dpar::Exec::DISPATCH))
-    ex = p >= kLvSplitRanks ? dpar::Exec::SPLIT : dpar::Exec::DISPATCH;
+      (ex == dpar::Exec::SPLIT || ex == dpar::Exec::DISPATCH)) {
+    const uint64_t lv_items =
+        grouped_units(s, prm.grp) / (uint64_t)s.C * (uint64_t)uc.lv_C;
+    const bool split = p >= kLvSplitRanks ||
+                       (p >= kLvSplitManyRanks &&
+                        lv_items >= (uint64_t)st->num_cus);
+    ex = split ? dpar::Exec::SPLIT : dpar::Exec::DISPATCH;
+  }
   const dpar::Unit unit = uc.unit;
   prm.nlev = ops->height + 1;
   if (unit == dpar::Unit::LEVEL) {

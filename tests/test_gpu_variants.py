@@ -558,8 +558,13 @@ def test_fused_wide_calls_of_few_ranks_take_full_items(p, n, capfd):
     # 512 KB
     (200, 1 << 17, 0, "int32", "postorder", F),
     (200, (1 << 17) + 4, 0, "int32", "postorder", S),
-    # level items fused below 1024 ranks, split from 1024 on
+    # level items fused below 512 ranks, split from 1024 on and from 512
+    # on with at least one item per CU; subtree items instead of more level
+    # items than CUs
     (511, 16384, 0, "int32", "level", F),
+    (400, 12288, 0, "int32", "level", F),
+    (400, 16384, 0, "int32", "subtree", F),
+    (700, 8192, 0, "int32", "level", S),
     (1152, 4096, 0, "int32", "level", S),
     (1152, 1024, 0, "int32", "level", S),
     (2304, 1024, 0, "int32", "level", S),
