@@ -637,8 +637,9 @@ __device__ __forceinline__ void run_unit_sub(const uint64_t* __restrict__ xp,
 // A wide item holds its CU for a chain of p / kWideKF dependent visits,
 // long next to its share of the bandwidth once fewer items than CUs are
 // left; so the columns past the call's last whole round of full items (one
-// item per resident workgroup) go to tail items of kWideTailQ quanta per
-// lane with kWideTailKF visits in flight, whose chains are shorter.
+// item per CU) go to tail items of kWideTailQ quanta per lane with
+// kWideTailKF visits in flight, whose chains are shorter (the host makes
+// that cut).
 //
 // LDS: per wavefront nslots depth slots of QW x 64 lanes, slot d's piece u
 // at [(d QW + u) 64 + lane] (one 16-byte access per lane, conflict-free);
@@ -1182,22 +1183,22 @@ __global__ __launch_bounds__(256) void k_bcast(const uint64_t* __restrict__ yp,
 
 // The same pass with 16-byte lanes for output rows that do not all start on
 // a 128-byte line.  The body of row i starts at the row's own first 4 KB
-// boundary,
-// h dwords in (plan.hpp bcast_row_split), so that every store fills 16
-// aligned bytes and every workgroup's tile is whole cache lines of one
-// page; lane l of the body copies dwords [h + 4 l, h + 4 l + 4), reading
+// boundary, h dwords in (plan.hpp bcast_row_split), so that every store
+// fills 16 aligned bytes and every workgroup's tile is whole cache lines of
+// one page; lane l of the body copies dwords [h + 4 l, h + 4 l + 4), reading
 // them from y_0 at any 4-byte alignment (an L2 hit).  The row's tile-0
 // workgroup also copies the h leading and the (up to 3) trailing dwords,
 // one dword per thread.  At p = 1152, m = 2^22 with rows 4 bytes off a
 // 16-byte boundary this pass takes 3.0 ms, against 3.7 ms with stores that
 // straddle 16-byte boundaries, 3.3 ms with the body shifted to the next
 // 16-byte boundary and 3.06 ms to the next 128-byte line (tiles straddling
-// cache lines leave partial lines to two workgroups); on 16-byte aligned
-// rows the plain pass is faster (2.6 against 3.1 ms), so the library picks
-// this one only when some output row needs it.  Rows on 16-byte boundaries
-// but off the 128-byte lines need it too: their plain tiles leave partial
-// lines to two workgroups (p = 1152, m = 2^22, rows 16 bytes past a line:
-// 3.50 ms plain).
+// cache lines leave partial lines to two workgroups); on rows that start on
+// 128-byte lines (the headline's, 16 MB apart) the plain pass is faster
+// (2.6 against 3.1 ms), so the library picks this one only when some output
+// row needs it.  Rows on 16-byte boundaries but off the 128-byte lines need
+// it too: their plain tiles leave partial lines to two workgroups
+// (p = 1152, m = 2^22, rows 16 bytes past a line: 3.50 ms plain, 3.01 ms
+// with this pass).
 template <bool FAST>
 __global__ __launch_bounds__(256) void k_bcast16_rows(
     const uint64_t* __restrict__ yp, BcastGrid g, uint64_t first) {
