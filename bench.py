@@ -79,7 +79,7 @@ def host_cores():
 
 
 def _oracle_pass(rows, out, threads):
-    """One pass of the oracle over the whole workload: the tree-order
+    """One pass of the numpy oracle over the whole workload: the tree-order
     reduction of all rows and the copy of y into every output row.  With
     threads > 1 the columns are cut into that many contiguous ranges, each
     evaluated by the unchanged oracle on its own thread (numpy releases the
@@ -101,24 +101,24 @@ def _oracle_pass(rows, out, threads):
         list(pool.map(part, range(threads)))
 
 
-def cpu_baseline(x_host, b):
-    """The CPU oracle, as it stands, on the whole workload: tree-order reduce
-    of all 1152 ranks over all 2^22 columns plus the copy of y into 1152
-    outputs, repeated until at least 10 s have passed (at most 8 passes);
-    once on one thread, once with the columns split over the host's cores.
-    Returns the baseline and the oracle's output (for the full-column check
-    of the GPU result)."""
-    import numpy as np
-    out = np.empty((P, M), dtype=np.float32)
-    out.fill(0.0)               # first touch of the pages, outside the timing
-    rows = [x_host[i] for i in range(P)]
+def _c_oracle_pass(rows, out, threads):
+    """One pass of the C oracle over the whole workload (the same reduction
+    and copy-out; its own threads over contiguous column ranges)."""
+    from oracle import c_oracle
+    c_oracle.allreduce_all(rows, "float32", "sum", out, threads=threads)
+
+
+def _time_legs(one_pass, rows, out):
+    """Each pass repeated until at least 10 s have passed (at most 8
+    passes), on one thread and on the host's cores: {threads: (GB/s, runs,
+    seconds, seconds per run)}."""
     legs = {}
     for threads in (1, host_cores()):
         if threads in legs:
             continue
         runs, t0 = 0, time.perf_counter()
         while True:
-            _oracle_pass(rows, out, threads)
+            one_pass(rows, out, threads)
             runs += 1
             dt = time.perf_counter() - t0
             if dt >= 10.0 or runs >= 8:
@@ -126,20 +126,43 @@ def cpu_baseline(x_host, b):
         per_run = dt / runs
         legs[threads] = (2.0 * P * M * ELEM / per_run / 1e9, runs, dt,
                          per_run)
+    return legs
+
+
+def _leg_record(legs, what):
     n = max(legs)
     gbs, runs, dt, per_run = legs[n]
     g1, runs1, dt1, per1 = legs[1]
-    base = {"value": round(gbs, 4), "unit": "GB/s", "cores": n,
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": n,
             "kind": "oracle",
-            "sample": f"the whole workload (p={P}, m={M}): tree-order reduce "
-                      f"+ copy to {P} outputs, columns split over {n} "
+            "sample": f"{what}: the whole workload (p={P}, m={M}), tree-order "
+                      f"reduce + copy to {P} outputs, columns split over {n} "
                       f"threads, {runs} runs in {dt:.1f} s, {per_run:.2f} s "
                       f"per run",
             "single_thread": {"value": round(g1, 4), "unit": "GB/s",
                               "cores": 1,
                               "sample": f"{runs1} runs in {dt1:.1f} s, "
                                         f"{per1:.2f} s per run"}}
-    return base, out
+
+
+def cpu_baseline(x_host, b, check):
+    """The CPU oracles, as they stand, on the whole workload: tree-order
+    reduce of all 1152 ranks over all 2^22 columns plus the copy of y into
+    1152 outputs, once on one thread, once with the columns split over the
+    host's cores.  The plain C oracle's legs are the baseline; the numpy
+    oracle's are reported beside them.  ``check(out, who)`` is called on
+    each oracle's output (the full-column check of the GPU result)."""
+    import numpy as np
+    out = np.empty((P, M), dtype=np.float32)
+    out.fill(0.0)               # first touch of the pages, outside the timing
+    rows = [x_host[i] for i in range(P)]
+    base = _leg_record(_time_legs(_c_oracle_pass, rows, out), "C oracle")
+    check(out, "C oracle")
+    out.fill(0.0)
+    base["numpy_oracle"] = _leg_record(_time_legs(_oracle_pass, rows, out),
+                                       "numpy oracle")
+    check(out, "numpy oracle")
+    return base
 
 
 def calib_copy():
@@ -850,18 +873,28 @@ def main():
 
     cpu = None
     if headline and not args.no_cpu_baseline:
-        cpu, full = cpu_baseline(x_host, b)
         y0 = yd[0].cpu().numpy()
-        bad = np.flatnonzero(y0.view(np.uint32) != full[0].view(np.uint32))
-        if bad.size:
-            log(f"bench: {bad.size} of {m_} columns differ from the oracle, "
-                f"first at {bad[0]}")
-            sys.exit(1)
-        cpu["checked"] = f"all {m_} columns of y_0 equal the oracle's y"
-        del full
-        log(f"cpu oracle: {cpu['value']} GB/s on {cpu['cores']} threads, "
-            f"{cpu['single_thread']['value']} GB/s on one "
-            f"({cpu['sample']}); {cpu['checked']}")
+
+        def check(full, who):
+            for r in (0, p_ // 2, p_ - 1):
+                if not np.array_equal(full[r].view(np.uint32),
+                                      full[0].view(np.uint32)):
+                    log(f"bench: the {who}'s output rows differ")
+                    sys.exit(1)
+            bad = np.flatnonzero(y0.view(np.uint32) != full[0].view(np.uint32))
+            if bad.size:
+                log(f"bench: {bad.size} of {m_} columns differ from the "
+                    f"{who}, first at {bad[0]}")
+                sys.exit(1)
+
+        cpu = cpu_baseline(x_host, b, check)
+        cpu["checked"] = (f"all {m_} columns of y_0 equal the C oracle's y "
+                          "and the numpy oracle's y")
+        npo = cpu["numpy_oracle"]
+        log(f"cpu oracle (C): {cpu['value']} GB/s on {cpu['cores']} threads, "
+            f"{cpu['single_thread']['value']} GB/s on one; numpy oracle: "
+            f"{npo['value']} GB/s on {npo['cores']} threads, "
+            f"{npo['single_thread']['value']} GB/s on one; {cpu['checked']}")
 
     line = {
         "metric": "effective allreduce GB/s and % of HBM peak at p=1152, "

@@ -30,10 +30,16 @@ independent columns):
                      broadcast (Section 2's User-Allreduce1).
 * ``blocks``      -- the block partition and the block-count rule of
                      Section 1.2.
+* ``c_oracle``    -- a second evaluation of y in plain C (``c/``), written
+                     independently of ``reduce``: the trees numbered from
+                     subtree sizes and a stack walk over the ranks in
+                     post-order, on host threads over column ranges
+                     (imported on its own: ``from oracle import c_oracle``).
 
 Parity status: every function here is pinned by ``tests/test_oracle_*.py``
 (hand-derived worked examples, closed forms, brute force, the error bound of
-recursive summation and the independent Algorithm-1 simulation).  The
+recursive summation and the independent Algorithm-1 simulation; the C
+oracle by ``tests/test_oracle_c.py``, planted mistakes included).  The
 ``wbal`` tree shape (an experiment only) is pinned by its p=9 structure, a
 hand-derived fp32 value and the invariants that fix it for every p up to 257
 and larger sizes up to 2000.

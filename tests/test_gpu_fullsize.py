@@ -5,9 +5,9 @@ and executor at that size.
 
 * fp32 SUM: every one of the 2^22 columns of y_0 is compared bit for bit
   with the CPU oracle's full evaluation in the trees' association (a few
-  seconds of numpy per tree layout), and every rank's row with y_0 on the
-  device; the result also lies within the recursive summation bound of the
-  exact sum.
+  seconds of numpy per tree layout; the default call also against the plain
+  C oracle), and every rank's row with y_0 on the device; the result also
+  lies within the recursive summation bound of the exact sum.
 * int32 SUM and MAX: every column equals the exact column sum (wrapped) and
   maximum, the plain definition that the exactly associative operators
   reach; sampled columns are also compared with the oracle's evaluation.
@@ -134,6 +134,27 @@ def test_p1152_fp32_sum_full_size(fp32_full):
         # below the fp32 bound
         assert bool((err <= gamma * mag + 1e-30).all()), f"columns from {c}"
     del yd, y0
+
+
+def test_p1152_fp32_sum_against_the_c_oracle(fp32_full):
+    """The benchmark's call once more, every column of y_0 against the plain
+    C oracle (a second oracle, written independently of the numpy one) on
+    the host's cores, and every row against y_0."""
+    import os
+    from oracle import c_oracle
+    from paper_2109_12626_amd import dpar
+    w, x, xd, _ = fp32_full
+    b = oracle.block_rule_lit(w.p, w.m)
+    yd = poisoned_like(xd)
+    s = torch.cuda.current_stream()
+    dpar.dpar_allreduce(dpar.rows(xd), dpar.rows(yd), w.p, w.m, w.dtype,
+                        "sum", b, s)
+    dpar.dpar_check_status(s)
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    want = c_oracle.allreduce(x, w.dtype, "sum", threads=threads)
+    _check_all_columns(yd, want, "default call, C oracle")
+    _check_rows_identical(yd)
+    del yd
 
 
 @pytest.mark.parametrize("op", ["sum", "max"])

@@ -409,6 +409,23 @@ def test_p64_matmul_full(dist):
     assert_all_ranks_equal(out, _want(x, "u32mat2x2", "matmul"))
 
 
+@pytest.mark.parametrize("w", [w for w in configs.ALL if w.p * w.m <= 1 << 27],
+                         ids=lambda w: w.name)
+def test_every_workload_against_the_c_oracle(w):
+    """Each workload of at most 2^27 elements in its own dtype, operators
+    and block counts, default call: every element of every rank against the
+    plain C oracle (a second oracle, written independently of the numpy
+    one)."""
+    from oracle import c_oracle
+    x = workload_input(w)
+    for op in w.ops:
+        want = c_oracle.allreduce(x, w.dtype, op, threads=8)
+        for b in w.bs:
+            bb = resolve_b(b, w.p, w.m)
+            out = run(x, w.dtype, op, bb)
+            assert_all_ranks_equal(out, want, f"{w.name} {op} b={bb}")
+
+
 @pytest.mark.parametrize("unit", UNITS + [None])
 @pytest.mark.parametrize("k", [4, 10, 16])
 @pytest.mark.parametrize("op", ["max", "sum"])
