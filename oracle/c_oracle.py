@@ -34,7 +34,7 @@ def build(out=None, mutant=0, verbose=False):
     """Compiles the C oracle (or, for tests, a copy with planted mistake
     ``mutant``) to ``out`` (default: next to the source)."""
     lib = out or LIB
-    tmp = lib + ".tmp"
+    tmp = f"{lib}.tmp{os.getpid()}"   # concurrent builders never share it
     cmd = (["gcc"] + CFLAGS + [f"-DDPO_MUTANT={int(mutant)}",
                                "-I", os.path.dirname(SRC), SRC, "-o", tmp])
     if verbose:
