@@ -132,6 +132,9 @@ def allreduce_all(x, dtype, op, out, layout="dual", threads=1, lib=None):
     p = len(rows)
     if len(outs) != p:
         raise ValueError("one output row per rank")
+    for r in rows + outs:
+        if r.dtype != _NP[dtype] or r.shape != rows[0].shape:
+            raise ValueError("rows must share the operator's dtype and shape")
     rc = lib.dpo_allreduce_all(KINDS[(dtype, op)], LAYOUTS[layout],
                                _ptrs(rows), _ptrs(outs), p,
                                rows[0].shape[0], threads)
