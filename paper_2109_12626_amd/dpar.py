@@ -9,6 +9,8 @@ process); torch serves only for device memory and streams.
 import ctypes
 import os
 
+import numpy as np
+
 import torch  # noqa: F401  (must precede loading libdpar: one HIP runtime)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -122,11 +124,22 @@ def _addr(v):
     return int(v)
 
 
+def _array_of(addrs):
+    """A C array of void* viewing a uint64 numpy array (kept alive by it)."""
+    if addrs.size == 0:
+        return (ctypes.c_void_p * 0)()
+    return (ctypes.c_void_p * addrs.size).from_buffer(addrs)
+
+
 def pointers(seq):
     """A reusable C array of device addresses (ints or tensors); passing it
     instead of a list saves the conversion on every call."""
     if isinstance(seq, ctypes.Array):
         return seq
+    if all(type(v) is int for v in seq):
+        # plain addresses: one conversion in numpy instead of one per entry
+        # (p = 1152: about 40 instead of 300 us on the host)
+        return _array_of(np.array(seq, dtype=np.uint64))
     return (ctypes.c_void_p * len(seq))(*[_addr(v) for v in seq])
 
 
@@ -146,12 +159,16 @@ def _enum(table, v):
 
 
 def rows(t):
-    """Device addresses of the rows of a [p, ...] tensor."""
+    """Device addresses of the rows of a [p, ...] tensor, as a reusable C
+    array (indexable and iterable like a list of ints)."""
     if t.dim() < 1:
         raise ValueError("need at least one dimension")
     step = t.stride(0) * t.element_size()
-    base = t.data_ptr()
-    return [base + i * step for i in range(t.shape[0])]
+    if step < 0:
+        raise ValueError("rows with a negative stride")
+    addrs = np.arange(t.shape[0], dtype=np.uint64) * np.uint64(step)
+    addrs += np.uint64(t.data_ptr())
+    return _array_of(addrs)
 
 
 def dpar_allreduce(x, y, p, m, dtype, op, b=0, stream=None):

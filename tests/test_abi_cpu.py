@@ -337,3 +337,28 @@ def test_noalloc_argument_errors_before_device_work():
     assert "32768" in dpar.dpar_last_error()
     # m = 0 is a successful no-op, as for dpar_allreduce
     assert f(xs, ys, 4, 0, "int32", "sum", 0) == 0
+
+
+def test_binding_pointer_arrays():
+    """rows() and pointers() only marshal addresses: the C arrays they
+    build hold exactly the row addresses, whichever route builds them."""
+    import ctypes
+    import torch
+    for shape in ((5, 7), (1, 3), (4, 2, 4), (300, 1)):
+        t = torch.zeros(shape, dtype=torch.float32)
+        r = dpar.rows(t)
+        assert isinstance(r, ctypes.Array) and len(r) == shape[0]
+        step = t.stride(0) * t.element_size()
+        want = [t.data_ptr() + i * step for i in range(shape[0])]
+        assert list(r) == want
+        assert dpar.pointers(r) is r                   # reused as it is
+        assert list(dpar.pointers(want)) == want       # plain ints
+        assert list(dpar.pointers(list(t))) == want    # tensors
+        mixed = [want[0]] + list(t)[1:]
+        assert list(dpar.pointers(mixed)) == want
+    assert len(dpar.rows(torch.zeros(0, 3))) == 0
+    assert len(dpar.pointers([])) == 0
+    big = [(1 << 63) + 4096 * i for i in range(3)]     # above 2^63
+    assert list(dpar.pointers(big)) == big
+    with pytest.raises(ValueError):
+        dpar.rows(torch.tensor(1.0))
