@@ -234,6 +234,11 @@ static void* run_job(void* arg) {
     if (c1 >= 0) {
       /* planted mistake: the second child's value (beneath) is taken first */
       unsigned char* tmp = (unsigned char*)malloc(row);
+      if (!tmp) {
+        free(stack);
+        j->rc = -2;
+        return NULL;
+      }
       memcpy(tmp, stack + (size_t)(top - 1) * row, row);
       memcpy(stack + (size_t)(top - 1) * row, stack + (size_t)(top - 2) * row,
              row);
