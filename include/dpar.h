@@ -207,7 +207,12 @@ typedef struct {
  *           The library copies both arrays before
  *           returning; the caller owns and may free them at once.  The
  *           buffers must stay valid, and x unmodified, until the stream work
- *           completes.
+ *           completes.  The copy goes to a device table once per distinct
+ *           pair of arrays (the last 8 pairs are kept): a call whose arrays
+ *           match a kept pair enqueues its kernels and nothing else.  A
+ *           replaced pair's table is recycled only after the device has
+ *           gone idle, and every 32 replacements the library waits for that
+ *           (hipDeviceSynchronize) in the call that needs a table.
  *   p       number of virtual ranks, >= 1.
  *   m       elements per rank; m == 0 is a successful no-op.
  *   b       number of pipeline blocks, 1 <= b <= m; b == 0 chooses

@@ -43,6 +43,9 @@ using dpar::kCounterStride;            // uint32 words: 128-byte lines
 // then one line for the grid-barrier words
 constexpr int kLinesPerSlot = 2 * dpar::kTicketCounters + 1;
 constexpr int kStageSlots = 8;
+// Retired pointer tables kept before one device-wide synchronisation frees
+// them all (a restage does not wait for the calls that read the table).
+constexpr size_t kRetiredTables = 32;
 // Split executor, post-order work items: workgroups resident per CU in the
 // up-phase (4 of 2 wavefronts read p = 1152 rows about 1.4% faster than the
 // 8 that fit by LDS), applied from kCapMinRanks ranks and kCapMinItemsPerCu
@@ -109,15 +112,32 @@ struct OpsTable {
   int root_a = -1, root_b = -1;  // roots of the real tree(s)
 };
 
+// A staged pointer set.  Its device table is never overwritten while it is
+// staged: restaging the slot retires the table (kernels of earlier calls,
+// on any stream, may still read it) and takes another from the pool, so no
+// call needs to record anything to protect it.  The one event, recorded
+// after each staging copy, guards the pinned source of that copy and orders
+// the copy before calls on other streams.
 struct StageSlot {
   std::vector<uint64_t> key;  // x pointers then y pointers
-  uint64_t* host = nullptr;   // pinned
-  uint64_t* dev = nullptr;
-  size_t cap = 0;             // entries
-  hipEvent_t ev = nullptr;
-  bool pending = false;
+  uint64_t* host = nullptr;   // pinned: the staging copy's source
+  size_t host_cap = 0;        // its entries
+  uint64_t* dev = nullptr;    // the device table the kernels read
+  size_t cap = 0;             // its entries
+  hipEvent_t ev = nullptr;    // recorded after the staging copy
+  hipStream_t copy_stream = nullptr;  // the stream that copy went on
+  bool copy_pending = false;  // that copy may not have run yet
   bool pinned = false;        // read by a captured graph: never restaged
   unsigned long long last_use = 0;
+};
+
+// Device pointer tables not held by a slot: free ones may be written, retired
+// ones may still be read by kernels already enqueued; all of those finish
+// before the next device-wide synchronisation, after which a retired table
+// is free.
+struct TableBuf {
+  uint64_t* dev;
+  size_t cap;  // entries
 };
 
 struct DeviceState {
@@ -130,6 +150,8 @@ struct DeviceState {
   std::map<std::pair<int, int>, OpsTable> ops;  // (p, one tree?)
   StageSlot stage[kStageSlots];
   unsigned long long tick = 0;
+  std::vector<TableBuf> free_tables;
+  std::vector<TableBuf> retired_tables;
 };
 
 std::mutex g_mu;
@@ -313,6 +335,43 @@ bool find_staged(DeviceState* st, const void* const* x, void* const* y, int p,
   return false;
 }
 
+// A device table of at least `need` entries: a free one, else (with
+// kRetiredTables retired) the retired ones once every kernel has finished,
+// else a new allocation.
+int take_table(DeviceState* st, size_t need, TableBuf* out) {
+  auto fit = [&](std::vector<TableBuf>& v) {
+    for (size_t i = 0; i < v.size(); ++i) {
+      if (v[i].cap >= need) {
+        *out = v[i];
+        v.erase(v.begin() + (long)i);
+        return true;
+      }
+    }
+    return false;
+  };
+  if (fit(st->free_tables)) return DPAR_SUCCESS;
+  hipError_t e;
+  if (st->retired_tables.size() >= kRetiredTables) {
+    e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+    for (const TableBuf& t : st->retired_tables) {
+      if (st->free_tables.size() < kRetiredTables)
+        st->free_tables.push_back(t);
+      else
+        (void)hipFree(t.dev);
+    }
+    st->retired_tables.clear();
+    if (fit(st->free_tables)) return DPAR_SUCCESS;
+  }
+  // the kernels read a few entries past the last pointer
+  const size_t cap = std::max<size_t>(need, 512 + dpar::kTablePad);
+  out->cap = cap;
+  e = hipMalloc(&out->dev, cap * sizeof(uint64_t));
+  if (e != hipSuccess) return fail(DPAR_ERR_NOMEM, "pointer table: %s",
+                                   hipGetErrorString(e));
+  return DPAR_SUCCESS;
+}
+
 // Copies the two pointer arrays into the least recently used staging slot
 // (callers look for a slot holding the same arrays first).
 int stage_pointers(DeviceState* st, const void* const* x, void* const* y,
@@ -330,27 +389,33 @@ int stage_pointers(DeviceState* st, const void* const* x, void* const* y,
     return fail(DPAR_ERR_NOMEM, "every pointer staging slot is held by a "
                                 "captured graph (dpar_finalize releases them)");
   hipError_t e;
-  if (s->pending) {  // the slot's previous table may still be read
+  if (s->copy_pending) {  // its pinned source is rewritten below
     e = hipEventSynchronize(s->ev);
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
-    s->pending = false;
+    s->copy_pending = false;
   }
-  if (s->cap < key.size() + dpar::kTablePad) {
-    if (s->host) (void)hipHostFree(s->host);
-    if (s->dev) (void)hipFree(s->dev);
-    s->host = nullptr;
+  if (s->dev) {  // earlier calls may still read it
+    st->retired_tables.push_back(TableBuf{s->dev, s->cap});
     s->dev = nullptr;
     s->cap = 0;
-    // the kernels read a few entries past the last pointer
-    const size_t cap = std::max<size_t>(key.size(), 256) + dpar::kTablePad;
-    e = hipHostMalloc(&s->host, cap * sizeof(uint64_t), hipHostMallocDefault);
+  }
+  s->key.clear();
+  const size_t need = key.size() + dpar::kTablePad;
+  if (s->host_cap < key.size()) {
+    if (s->host) (void)hipHostFree(s->host);
+    s->host = nullptr;
+    s->host_cap = 0;
+    const size_t hcap = std::max<size_t>(key.size(), 512);
+    e = hipHostMalloc(&s->host, hcap * sizeof(uint64_t), hipHostMallocDefault);
     if (e != hipSuccess) return fail(DPAR_ERR_NOMEM, "pinned staging: %s",
                                      hipGetErrorString(e));
-    e = hipMalloc(&s->dev, cap * sizeof(uint64_t));
-    if (e != hipSuccess) return fail(DPAR_ERR_NOMEM, "pointer table: %s",
-                                     hipGetErrorString(e));
-    s->cap = cap;
+    s->host_cap = hcap;
   }
+  TableBuf t{};
+  int rc = take_table(st, need, &t);
+  if (rc) return rc;
+  s->dev = t.dev;
+  s->cap = t.cap;
   if (!s->ev) {
     e = hipEventCreateWithFlags(&s->ev, hipEventDisableTiming);
     if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
@@ -359,9 +424,32 @@ int stage_pointers(DeviceState* st, const void* const* x, void* const* y,
   e = hipMemcpyAsync(s->dev, s->host, key.size() * sizeof(uint64_t),
                      hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync pointer table");
+  e = hipEventRecord(s->ev, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  s->copy_pending = true;
+  s->copy_stream = stream;
   s->key = std::move(key);
   s->last_use = st->tick;
   *used = s;
+  return DPAR_SUCCESS;
+}
+
+// A call on `stream` about to read slot s's table: the staging copy, if it
+// may not have run yet and went on another stream, goes before this call's
+// kernels (a wait on the device; on the host under capture, whose stream
+// cannot wait for work outside the graph).
+int order_after_copy(StageSlot* s, hipStream_t stream, bool capturing) {
+  if (!s->copy_pending || s->copy_stream == stream) return DPAR_SUCCESS;
+  hipError_t e = hipEventQuery(s->ev);
+  if (e == hipSuccess) {
+    s->copy_pending = false;
+    return DPAR_SUCCESS;
+  }
+  if (e != hipErrorNotReady) return hip_fail(e, "hipEventQuery");
+  e = capturing ? hipEventSynchronize(s->ev)
+                : hipStreamWaitEvent(stream, s->ev, 0);
+  if (e != hipSuccess) return hip_fail(e, "waiting for the pointer staging");
+  if (capturing) s->copy_pending = false;
   return DPAR_SUCCESS;
 }
 
@@ -1157,6 +1245,8 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
       rc = stage_pointers(st, x, y, p, stream, &slot);
       if (rc) return rc;
     }
+    rc = order_after_copy(slot, stream, capturing);
+    if (rc) return rc;
     if (capturing) slot->pinned = true;
     ptr_dev = slot->dev;
   }
@@ -1501,12 +1591,6 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
                         rows_lines, span, fastdiv, stream);
     if (e != hipSuccess) return hip_fail(e, "broadcast launch");
   }
-  if (!capturing && !fixed) {  // a pinned slot is never restaged, so never
-                               // waited on
-    e = hipEventRecord(slot->ev, stream);
-    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-    slot->pending = true;
-  }
   return DPAR_SUCCESS;
 }
 
@@ -1582,6 +1666,8 @@ int dpar_finalize(void) {
       if (s.host) (void)hipHostFree(s.host);
       if (s.dev) (void)hipFree(s.dev);
     }
+    for (const TableBuf& t : st->free_tables) (void)hipFree(t.dev);
+    for (const TableBuf& t : st->retired_tables) (void)hipFree(t.dev);
     if (st->counters) (void)hipFree(st->counters);
   }
   g_devices.clear();

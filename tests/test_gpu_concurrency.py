@@ -90,3 +90,61 @@ def test_two_host_threads():
     for t in ts:
         t.join()
     assert not errors, errors
+
+
+def test_pointer_set_staged_on_a_busy_stream_used_on_another():
+    """A call on stream B with the pointer arrays that a call on stream A has
+    just staged: A is still busy, so A's copy of the table has not run, and
+    B's kernels must wait for it."""
+    need_gpu()
+    dpar = lib()
+    p, m = 300, 40000
+    busy = torch.zeros(64 << 20, dtype=torch.float32, device="cuda")
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    for it in range(3):
+        x, want = _case(2140 + it, p, m)
+        xd = to_dev(x)
+        y = _poisoned(xd)
+        torch.cuda.synchronize()
+        xs, ys = dpar.rows(xd), dpar.rows(y)
+        with torch.cuda.stream(sa):
+            for _ in range(30):
+                busy.add_(1.0)
+        for s in (sa, sb):
+            dpar.dpar_allreduce_opt(xs, ys, p, m, "float32", "sum", 0,
+                                    "dual", "auto", 0, -1, s)
+        sb.synchronize()
+        got_b = y.cpu().numpy()       # B's call is done, A's may not be
+        torch.cuda.synchronize()
+        dpar.dpar_check_status(sa)
+        assert_all_ranks_equal(got_b, want, f"stream B, round {it}")
+        assert_all_ranks_equal(y.cpu().numpy(), want, f"both, round {it}")
+
+
+def test_many_pointer_sets_on_two_streams():
+    """More distinct pointer sets than the library keeps staged plus the
+    tables it retires before recycling them, alternating between two
+    streams without synchronisation, twice over: every output equals the
+    oracle (a call reading a recycled table too early would write another
+    set's result, or read another set's inputs)."""
+    need_gpu()
+    dpar = lib()
+    p, m, n = 40, 3001, 50
+    cases = [_case(2200 + k, p, m) for k in range(n)]
+    xds = [to_dev(x) for x, _ in cases]
+    ys = [_poisoned(xd) for xd in xds]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for rnd, order in enumerate((range(n), reversed(range(n)))):
+        for y in ys:
+            y.view(torch.int32).fill_(POISON)
+        torch.cuda.synchronize()
+        for k in order:
+            s = s1 if k % 2 == 0 else s2
+            dpar.dpar_allreduce_opt(dpar.rows(xds[k]), dpar.rows(ys[k]), p, m,
+                                    "float32", "sum", 0, "dual", "auto", 0,
+                                    -1, s)
+        torch.cuda.synchronize()
+        dpar.dpar_check_status(s1)
+        for k in range(n):
+            assert_all_ranks_equal(ys[k].cpu().numpy(), cases[k][1],
+                                   f"round {rnd}, set {k}")
