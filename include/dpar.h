@@ -106,7 +106,9 @@ typedef enum {
  *                     1 MB (p <= 96) or 512 KB,
  *                     for calls that run in subtree work items (p >= 256
  *                     and at most two such items per CU, at least one per
- *                     four CUs), and for calls that run in wide work items
+ *                     four CUs; from p = 4096 on, calls of three or four
+ *                     per CU run them split), and for calls that run in
+ *                     wide work items
  *                     with p <= 36 and at most one such item (16 KB of
  *                     columns) per CU, with p <= 20 and at most two, or
  *                     with p <= 8.

@@ -72,6 +72,8 @@ constexpr int kWideLateRanks = 16;
 constexpr int kLvSplitRanks = 1024;
 constexpr int kLvSplitManyRanks = 512;
 constexpr int kLvCrowdRanks = 2048;
+// Ranks from which subtree items take calls of up to four items per CU.
+constexpr int kSubCrowdRanks = 4096;
 // Level work item: loads in flight at once (1024 threads, 8 loads each).
 constexpr uint64_t kLvLoadsInFlight = 1024 * 8;
 // Ticket executor: rank loads per claimed batch of work items.
@@ -925,8 +927,17 @@ UnitChoice choose_unit(dpar::Exec ex, const dpar::Schedule& s, int grp,
                           ex == dpar::Exec::GRID_BARRIER) &&
                          p >= 256 && (uint64_t)s.C >= cus / 2 &&
                          (uint64_t)s.C <= 2 * cus && s.Q >= 32 * all_items;
+  // From kSubCrowdRanks ranks on subtree items also take calls of up to
+  // four per CU (split; post-order chains of p / 2 loads are then the
+  // longer wait): p = 4608, m = 2^18 (1024 items), median of four runs,
+  // post-order split 1685 us back to back / 2086 us after a cache flush,
+  // subtree split 1528 / 1897 us; at p = 2304 post-order items stay
+  // faster (735 / 884 against 798 / 971 us).
+  const bool sub_crowd = whole_call && p >= kSubCrowdRanks &&
+                         sub_items <= 4 * cus;
   bool want_sub = p >= 256 && sub_fits &&
-                  ((whole_call && sub_items <= 2 * cus) || round_sub);
+                  ((whole_call && sub_items <= 2 * cus) || sub_crowd ||
+                   round_sub);
   if (ops.lvl) {
     int tmax = -1;
     for (int lg = 6; lg >= 0; --lg) {
@@ -1339,9 +1350,14 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
   // (p = 2304, m = 14336, 56 items: 0.107 vs 0.117 ms).  Calls that take
   // post-order items on long rows stay split, which is faster there from
   // 256 MB up (p = 36 .. 2304: 8-35% at 1-38 GB).
+  // Beyond two items per CU (many ranks, above) split stays faster in both
+  // regimes (p = 4608, m = 2^18: fused 1857 / 1722 us, split 1528 /
+  // 1897 us back to back / after a flush; the fused launch's p writes per
+  // item then overlap the reads of the items after it).
   if (exec == DPAR_EXEC_AUTO && ex == dpar::Exec::SPLIT &&
       uc.unit == dpar::Unit::SUB &&
-      4 * ((s.Q + 63) / 64) >= (uint64_t)st->num_cus)
+      4 * ((s.Q + 63) / 64) >= (uint64_t)st->num_cus &&
+      (s.Q + 63) / 64 <= 2 * (uint64_t)st->num_cus)
     ex = dpar::Exec::DISPATCH;
   // AUTO, wide items: with at most one per CU they all run at once, read
   // their rows together and then write y together, so one fused launch

@@ -574,6 +574,8 @@ def test_fused_wide_calls_of_few_ranks_take_full_items(p, n, capfd):
     # from 2048 ranks on level items up to four per CU, then subtree items
     (2304, 4096, 0, "int32", "level", S),
     (2304, 8192, 0, "int32", "subtree", S),
+    # from 4096 ranks on subtree items up to four per CU, split beyond two
+    (4096, 196608, 0, "int32", "subtree", S),
 ])
 def test_wide_unit_choice(p, m, b, dtype, unit, ex, capfd):
     """The library's own choice under AUTO (256 CUs): wide items where their
