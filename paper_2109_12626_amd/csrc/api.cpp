@@ -295,14 +295,14 @@ struct AliasOk {
 };
 std::vector<AliasOk> g_alias_ok;
 
+// The key holds the two arrays' pointer values as they are (8 bytes each),
+// so whole arrays compare with memcmp (p = 1152: two 9 KB compares).
+static_assert(sizeof(void*) == sizeof(uint64_t), "64-bit pointers");
 bool same_key(const std::vector<uint64_t>& k, const void* const* x,
               void* const* y, int p) {
   if (k.size() != 2 * (size_t)p) return false;
-  for (int i = 0; i < p; ++i)
-    if (k[i] != (uint64_t)(uintptr_t)x[i] ||
-        k[p + i] != (uint64_t)(uintptr_t)y[i])
-      return false;
-  return true;
+  return std::memcmp(k.data(), x, (size_t)p * sizeof(uint64_t)) == 0 &&
+         std::memcmp(k.data() + p, y, (size_t)p * sizeof(uint64_t)) == 0;
 }
 
 bool alias_cached(const void* const* x, void* const* y, int p, size_t bytes) {
@@ -1115,20 +1115,30 @@ int allreduce_impl(const void* const* x, void* const* y, int p, size_t m,
                 opt.round_begin, opt.round_end);
   // every output row starts on a 128-byte cache line (else the broadcast
   // pass aligns each row's stores itself)
-  bool rows_lines = true;
-  bool xrows_lines = true;  // every input row starts on a 128-byte line
+  // one branch-free pass (OR of all addresses, any null); only a call that
+  // fails a check walks the ranks again to name the first offender
+  uintptr_t or_x = 0, or_y = 0;
+  bool any_null = false;
   for (int i = 0; i < p; ++i) {
-    if (!x[i] || !y[i])
-      return fail(DPAR_ERR_INVALID_ARG, "null buffer for rank %d", i);
     const uintptr_t a = (uintptr_t)x[i], c = (uintptr_t)y[i];
-    if ((a | c) & 3)
-      return fail(DPAR_ERR_INVALID_ARG, "rank %d buffer not 4-byte aligned",
-                  i);
-    if (c & 127) rows_lines = false;
-    if (a & 127) xrows_lines = false;
-    if (((a | c) >> 48) != 0)
-      return fail(DPAR_ERR_UNSUPPORTED, "rank %d address above 2^48", i);
+    or_x |= a;
+    or_y |= c;
+    any_null |= (a == 0) | (c == 0);
   }
+  if (any_null || ((or_x | or_y) & 3) || ((or_x | or_y) >> 48)) {
+    for (int i = 0; i < p; ++i) {
+      if (!x[i] || !y[i])
+        return fail(DPAR_ERR_INVALID_ARG, "null buffer for rank %d", i);
+      const uintptr_t a = (uintptr_t)x[i], c = (uintptr_t)y[i];
+      if ((a | c) & 3)
+        return fail(DPAR_ERR_INVALID_ARG,
+                    "rank %d buffer not 4-byte aligned", i);
+      if (((a | c) >> 48) != 0)
+        return fail(DPAR_ERR_UNSUPPORTED, "rank %d address above 2^48", i);
+    }
+  }
+  const bool rows_lines = (or_y & 127) == 0;
+  const bool xrows_lines = (or_x & 127) == 0;  // every input row on a line
   if (m == 0) return DPAR_SUCCESS;
   const bool rule_b = b == 0;
   if (b == 0) b = (int)dpar::block_rule(p, m, 0.0, 0.0);
