@@ -38,7 +38,7 @@ def _case(k):
                 separate=bool(r.integers(2)), seed=2200 + k)
 
 
-@pytest.mark.parametrize("k", range(300))
+@pytest.mark.parametrize("k", range(800))
 def test_random_combination(k):
     need_gpu()
     _check_case(_case(k))
@@ -62,7 +62,7 @@ def _wide_case(k):
                 wide_round=[None, 1, 2, 3, 5][int(r.integers(5))])
 
 
-@pytest.mark.parametrize("k", range(60))
+@pytest.mark.parametrize("k", range(160))
 def test_random_wide_items(k):
     """Seeded random calls with the wide post-order work item forced (the
     one-launch executors; on 4-byte lanes the library keeps the plain
@@ -91,7 +91,7 @@ def _mid_case(k):
                 separate=bool(r.integers(3) == 0), seed=2800 + k)
 
 
-@pytest.mark.parametrize("k", range(60))
+@pytest.mark.parametrize("k", range(160))
 def test_random_auto_mid_size(k):
     """Seeded random calls of 4 to 32 MB under AUTO with the rule's b
     (p = 2 .. 1100, every operator and tree layout, misaligned rows, in
