@@ -165,7 +165,7 @@ def _large_case(k):
                 unit=UNITS[int(r.integers(len(UNITS)))], seed=2600 + k)
 
 
-@pytest.mark.parametrize("k", range(40))
+@pytest.mark.parametrize("k", range(100))
 def test_random_large_p(k):
     """Seeded random calls at p = 257 .. 5000 (deeper trees, the subtree
     and level work items and their chunk choices): bit for bit against the
