@@ -99,6 +99,33 @@ def test_sizes_and_types(p, m, dtype, op):
     _check(x, dtype, op, 0, f"p={p} m={m} {dtype}")
 
 
+def _random_case(k):
+    r = np.random.default_rng(9900 + k)
+    p = int(r.choice([1, 2, 3, 7, 36, 64, 255, 300, 1152, 2304, 5000]))
+    dtype, op, dist = [("int32", "sum", "uniform_int"),
+                       ("int32", "max", "uniform_int"),
+                       ("float32", "sum", "normal_f32"),
+                       ("u32mat2x2", "matmul", "odd_det_u32_mat")][
+                           int(r.integers(4))]
+    words = 4 if dtype == "u32mat2x2" else 1
+    m = int(r.integers(1, max(2, min(70000, (1 << 22) // (p * words)))))
+    b = int(r.choice([0, 1, int(r.integers(1, m + 1))]))
+    return p, m, dtype, op, dist, min(b, m)
+
+
+@pytest.mark.parametrize("k", range(40))
+def test_random_calls(k):
+    """Seeded random calls of both entry points in a row (p = 1 .. 5000,
+    every operator, the rule's b, b = 1 or a random b): bit-identical
+    outputs, equal to the oracle; consecutive cases change p, m and the
+    pointer arrays, so the fixed scratch is restaged every time."""
+    need_gpu()
+    p, m, dtype, op, dist, b = _random_case(k)
+    kw = {"lo": -1000, "hi": 1000} if dist == "uniform_int" else {}
+    x = synth.generate(dist, 2400 + k, p, m, **kw)
+    _check(x, dtype, op, b, f"k={k} p={p} m={m} {dtype} {op} b={b}")
+
+
 def test_largest_p_and_the_limit():
     """p = 32768 fits the fixed scratch; one more rank is refused before any
     device work."""
