@@ -31,6 +31,21 @@ def test_captured_wide_items_replay(exec):
     _replays("dual", exec, 36, 1 << 20, 0)
 
 
+@pytest.mark.parametrize("k", range(24))
+def test_random_captured_calls(k):
+    """Seeded random captures (p = 1 .. 1500, m up to 2^18, every tree
+    layout, the executors a graph may hold, the rule's b or a random one),
+    each replayed with new inputs and eager work between the replays."""
+    need_gpu()
+    r = np.random.default_rng(9950 + k)
+    p = int(r.choice([1, 2, 5, 36, 64, 130, 288, 700, 1152, 1500]))
+    m = int(r.integers(1, max(2, min(1 << 18, (1 << 22) // p))))
+    b = int(r.choice([0, 1, int(r.integers(1, m + 1))]))
+    alg = ["dual", "single", "reduce_bcast"][int(r.integers(3))]
+    exec = ["auto", "split", "ticket", "launch", "rounds"][int(r.integers(5))]
+    _replays(alg, exec, p, m, min(b, m))
+
+
 def _replays(alg, exec, p, m, b):
     dpar = lib()
     trees = oracle.build_trees(p) if alg == "dual" else \
