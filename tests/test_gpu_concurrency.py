@@ -148,3 +148,45 @@ def test_many_pointer_sets_on_two_streams():
         for k in range(n):
             assert_all_ranks_equal(ys[k].cpu().numpy(), cases[k][1],
                                    f"round {rnd}, set {k}")
+
+
+@pytest.mark.parametrize("k", range(16))
+def test_random_calls_on_two_streams(k):
+    """Seeded random pairs of calls interleaved on two streams, three rounds
+    with fresh outputs (new pointer sets, staged on either stream), then
+    one pointer set used on both streams in turn without synchronisation:
+    every output equals the oracle."""
+    need_gpu()
+    dpar = lib()
+    r = np.random.default_rng(9990 + k)
+    cases = []
+    for j in range(2):
+        p = int(r.choice([2, 7, 36, 130, 300, 1152]))
+        m = int(r.integers(1, max(2, min(1 << 17, (1 << 21) // p))))
+        ex = EXECS[int(r.integers(len(EXECS)))]
+        x, want = _case(2500 + 2 * k + j, p, m)
+        cases.append((p, m, ex, to_dev(x), want))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = []
+    torch.cuda.synchronize()
+    for rnd in range(3):
+        for j, (p, m, ex, xd, want) in enumerate(cases):
+            y = _poisoned(xd)
+            torch.cuda.synchronize()
+            dpar.dpar_allreduce_opt(dpar.rows(xd), dpar.rows(y), p, m,
+                                    "float32", "sum", 0, "dual", ex, 0, -1,
+                                    streams[(j + rnd) % 2])
+            outs.append((y, want, f"round {rnd} case {j} p={p} m={m} {ex}"))
+    p, m, ex, xd, want = cases[0]
+    y = _poisoned(xd)
+    torch.cuda.synchronize()
+    xs, ys = dpar.rows(xd), dpar.rows(y)
+    for s in streams:
+        dpar.dpar_allreduce_opt(xs, ys, p, m, "float32", "sum", 0, "dual",
+                                ex, 0, -1, s)
+    outs.append((y, want, f"shared set p={p} m={m} {ex}"))
+    torch.cuda.synchronize()
+    for s in streams:
+        dpar.dpar_check_status(s)
+    for y, want, what in outs:
+        assert_all_ranks_equal(y.cpu().numpy(), want, what)
