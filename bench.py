@@ -69,8 +69,8 @@ def traffic_per_launch(phase):
 
 
 def host_cores():
-    """Cores the oracle may use: the process's CPU affinity, at most 16 (a
-    GPU machine's share per GPU)."""
+    """Cores the oracle may use: the process's CPU affinity, at most 16 (one
+    GPU's share of the host cores of an 8-GPU node)."""
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:
