@@ -269,7 +269,11 @@ int dpar_allreduce_opt(const void* const* x, void* const* y, int p, size_t m,
  * DPAR_ERR_UNSUPPORTED).  Under capture a call only enqueues kernels, so an
  * eager call with the same p, algorithm and pointer arrays must come first
  * (it builds the device tables and stages the pointers; otherwise
- * DPAR_ERR_UNSUPPORTED).  The staged pointer table is then held for the
+ * DPAR_ERR_UNSUPPORTED).  If that eager call ran on another stream and its
+ * copy of the pointer table may not have run yet, the capturing call waits
+ * for it on the host (synchronise first to avoid the wait; a capture mode
+ * that forbids it makes the call fail with DPAR_ERR_HIP and leaves the
+ * capture to the runtime).  The staged pointer table is then held for the
  * graph: it is never restaged, and dpar_finalize, which frees it, must wait
  * until no graph that captured a call is replayed again.  A replay computes
  * from the buffers' contents at replay time.  Replays of one graph, and a
