@@ -125,7 +125,8 @@ def _check_invariants(p, layout):
 
 
 @pytest.mark.parametrize("p", list(range(1, 130)) + [255, 256, 511, 576, 1000,
-                                                     1151, 1152, 2000])
+                                                     1151, 1152, 2000, 4608,
+                                                     32768, 100003])
 def test_tree_invariants(p):
     _check_invariants(p, "dual")
     _check_invariants(p, "single")
